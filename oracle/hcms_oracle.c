@@ -1,0 +1,152 @@
+/*
+ * Oracle for the single-GPU share of HCMS (head-chunked multi-stream
+ * attention, arXiv 2607.01817).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path links, loads or calls
+ * this file: only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg do.  It shares no source, header, table or helper with the HIP
+ * library; the two are compared on the same seeded inputs.
+ *
+ * Everything here is deliberately plain: explicit loops, fp64 arithmetic,
+ * no tiling, no fusion, no online softmax.
+ *
+ *   oracle_attention_rows  Sec. 3.3, Property "Computational Independence of
+ *                          Multi-Head Attention": the output of one head is a
+ *                          function of that head's Q, K, V only.  The function
+ *                          f is scaled-dot-product softmax attention (Alg. 1
+ *                          names FlashAttention or SDPA as the kernel), over the
+ *                          full sequence with no mask (bidirectional video DiT
+ *                          attention, Sec. 2.1).  Written as the textbook
+ *                          two-pass softmax.
+ *   oracle_pack            Sec. 3.3, split of Q/K/V along the head dimension
+ *                          into chunk c (heads [h0, h0+Hc)), combined with the
+ *                          local share of the input all-to-all of Sec. 3.1
+ *                          (sequence-sharded -> head-sharded).  Index formula:
+ *                            dst[j][p*(S/P)+s][e] = src[p][s][h0+j][e].
+ *   oracle_unpack          The inverse (output all-to-all + concatenation along
+ *                          heads, Alg. 1): dst[p][s][h0+j][e] = src[j][p*(S/P)+s][e];
+ *                          heads outside the chunk are left untouched.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/*
+ * One head, a list of query rows.
+ *   q       : [Sq][d] row-major fp64 queries (the exact stored values, widened)
+ *   k, v    : [S][d] row-major fp64 keys and values
+ *   rows    : n_rows query indices in [0, Sq)
+ *   out     : [n_rows][d]
+ * For each listed query i:
+ *   s_j = scale * sum_t q[i][t] * k[j][t]          for all j < S
+ *   m   = max_j s_j
+ *   l   = sum_j exp(s_j - m)
+ *   out[i][t] = sum_j exp(s_j - m) * v[j][t] / l
+ * Returns 0, or -1 if a scratch allocation fails.
+ */
+int oracle_attention_rows(const double *q, const double *k, const double *v,
+                          int64_t S, int64_t d, double scale,
+                          const int64_t *rows, int64_t n_rows, double *out)
+{
+    int failed = 0;
+#pragma omp parallel
+    {
+        double *s = (double *)malloc((size_t)S * sizeof(double));
+        if (!s) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < n_rows; ++r) {
+            if (!s) continue;
+            const int64_t i = rows[r];
+            const double *qi = q + i * d;
+            /* pass 1: scores and their maximum */
+            double m = -INFINITY;
+            for (int64_t j = 0; j < S; ++j) {
+                const double *kj = k + j * d;
+                double dot = 0.0;
+                for (int64_t t = 0; t < d; ++t) dot += qi[t] * kj[t];
+                s[j] = scale * dot;
+                if (s[j] > m) m = s[j];
+            }
+            /* pass 2: exponentials, their sum, and the weighted sum of V rows */
+            double *o = out + r * d;
+            for (int64_t t = 0; t < d; ++t) o[t] = 0.0;
+            double l = 0.0;
+            for (int64_t j = 0; j < S; ++j) {
+                const double w = exp(s[j] - m);
+                l += w;
+                const double *vj = v + j * d;
+                for (int64_t t = 0; t < d; ++t) o[t] += w * vj[t];
+            }
+            for (int64_t t = 0; t < d; ++t) o[t] /= l;
+        }
+        free(s);
+    }
+    return failed ? -1 : 0;
+}
+
+/*
+ * Pack one head chunk.  src is [P][S/P][H][d] elements of elem_bytes bytes,
+ * dst is [Hc][S][d].  Returns 0, or -1 on a shape the formula does not cover.
+ */
+int oracle_pack(const void *src, void *dst, int64_t P, int64_t S, int64_t H,
+                int64_t d, int64_t h0, int64_t Hc, int64_t elem_bytes)
+{
+    if (P <= 0 || S % P != 0 || h0 < 0 || Hc < 0 || h0 + Hc > H) return -1;
+    const int64_t Ss = S / P;
+    const unsigned char *sp = (const unsigned char *)src;
+    unsigned char *dp = (unsigned char *)dst;
+    for (int64_t p = 0; p < P; ++p)
+        for (int64_t s = 0; s < Ss; ++s)
+            for (int64_t j = 0; j < Hc; ++j)
+                for (int64_t e = 0; e < d; ++e) {
+                    const int64_t from = ((p * Ss + s) * H + (h0 + j)) * d + e;
+                    const int64_t to = (j * S + (p * Ss + s)) * d + e;
+                    memcpy(dp + to * elem_bytes, sp + from * elem_bytes, (size_t)elem_bytes);
+                }
+    return 0;
+}
+
+/*
+ * Unpack one head chunk.  src is [Hc][S][d], dst is [P][S/P][H][d]; only the
+ * head slots [h0, h0+Hc) of dst are written.
+ */
+int oracle_unpack(const void *src, void *dst, int64_t P, int64_t S, int64_t H,
+                  int64_t d, int64_t h0, int64_t Hc, int64_t elem_bytes)
+{
+    if (P <= 0 || S % P != 0 || h0 < 0 || Hc < 0 || h0 + Hc > H) return -1;
+    const int64_t Ss = S / P;
+    const unsigned char *sp = (const unsigned char *)src;
+    unsigned char *dp = (unsigned char *)dst;
+    for (int64_t p = 0; p < P; ++p)
+        for (int64_t s = 0; s < Ss; ++s)
+            for (int64_t j = 0; j < Hc; ++j)
+                for (int64_t e = 0; e < d; ++e) {
+                    const int64_t from = (j * S + (p * Ss + s)) * d + e;
+                    const int64_t to = ((p * Ss + s) * H + (h0 + j)) * d + e;
+                    memcpy(dp + to * elem_bytes, sp + from * elem_bytes, (size_t)elem_bytes);
+                }
+    return 0;
+}
+
+/* Number of OpenMP threads the attention oracle runs on (for reporting). */
+int oracle_num_threads(void)
+{
+    int n = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        {
+#ifdef _OPENMP
+            n = omp_get_num_threads();
+#endif
+        }
+    }
+    return n;
+}

@@ -1,0 +1,117 @@
+"""Seeded synthetic workloads shared by the tests, the smoke check and the bench.
+
+This module draws inputs only.  It holds none of the method's arithmetic, and it
+imports neither the HIP binding nor the oracle, so both sides can be fed the
+same host tensors.
+
+The paper's workload is Wan2.2 latent-video self-attention: 40 heads of
+dimension 128 and 60 x 104 latents, i.e. 6240 tokens per latent frame
+(Sec. 4.1, model configuration table).  A Ulysses rank with P shards holds
+H = 40 / P heads over the whole sequence.  The paper gives no distribution
+for the activations, so Q, K and V are i.i.d. Gaussians of the stated scale.
+The "planted peak" variant sets each query to twice a chosen key, giving a
+softmax dominated by that key.  It stands in for peaked real attention maps
+and makes the parity tolerance meaningful.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    S: int
+    H: int
+    d: int
+    dtype: str            # "bf16" or "fp32" storage
+    sigma: float          # Q, K, V ~ N(0, 1) * sigma
+    P: int                # sequence shards of the Ulysses layout
+    chunkings: tuple      # tuple of tuples of head counts
+    seed: int
+    oracle_rows: int      # query rows per head checked against the oracle (0 = all)
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.d)
+
+    @property
+    def flops(self) -> float:
+        """Algorithmic attention FLOPs: two GEMMs of S x S x d per head."""
+        return 4.0 * self.S * self.S * self.H * self.d
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.dtype == "bf16" else 4
+
+
+WORKLOADS = {
+    "tiny": Workload("tiny", 512, 4, 64, "fp32", 1.0, 4, ((2, 2), (4,)), 1, 0),
+    "small": Workload("small", 4096, 8, 128, "bf16", 1.0, 8,
+                      ((8,), (4, 4), (2, 2, 2, 2), (3, 3, 2)), 2, 0),
+    # Wan2.2-14B shape, rank share at P=4: 21 latent frames x 1560 tokens.
+    "wan_p4": Workload("wan_p4", 32760, 10, 128, "bf16", 0.5, 4,
+                       ((10,), (5, 5), (4, 3, 3)), 3, 256),
+    # Wan2.2-14B shape, rank share at P=8: 36 latent frames x 1560 tokens.
+    "wan_p8": Workload("wan_p8", 56160, 5, 128, "bf16", 0.5, 8,
+                       ((5,), (2, 2, 1), (1, 1, 1, 1, 1)), 4, 256),
+    # All 40 heads of one layer on one GPU, 100k tokens.
+    "stress": Workload("stress", 100000, 40, 128, "bf16", 0.5, 8,
+                       ((40,), (10, 10, 10, 10), (14, 13, 13)), 5, 128),
+}
+
+
+def torch_dtype(w: Workload):
+    return torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+
+def make_qkv(w: Workload, planted: bool = False, seed: int | None = None):
+    """Q, K, V as host tensors of shape [S][H][d] (= [P][S/P][H][d]).
+
+    Drawn as fp32 ``randn`` in the order Q, K, V from a CPU generator seeded
+    with ``seed`` (default ``w.seed``), multiplied by ``sigma`` and rounded to
+    the storage dtype (round-to-nearest-even for bf16).
+
+    With ``planted=True``, K is drawn with unit scale and each query row of
+    head h is replaced by ``2 * K[π_h(i)]`` for a seeded permutation π_h of the
+    keys (the doubling is exact in bf16).  With scale 1/sqrt(d) the planted
+    logit is then about 2*sqrt(d) (22.6 at d = 128) while the other logits
+    have standard deviation 2, so the softmax puts nearly all of its weight on
+    one key and |O| is of the order of |V|.
+    """
+    seed = w.seed if seed is None else seed
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    dt = torch_dtype(w)
+    shape = (w.S, w.H, w.d)
+    k_sigma = 1.0 if planted else w.sigma
+    q = (torch.randn(shape, generator=g, dtype=torch.float32) * w.sigma).to(dt)
+    k = (torch.randn(shape, generator=g, dtype=torch.float32) * k_sigma).to(dt)
+    v = (torch.randn(shape, generator=g, dtype=torch.float32) * w.sigma).to(dt)
+    if planted:
+        q = torch.empty_like(k)
+        for h in range(w.H):
+            perm = torch.from_numpy(planted_permutation(w, h, seed))
+            q[:, h, :] = k[perm, h, :] * 2
+    return q, k, v
+
+
+def planted_permutation(w: Workload, h: int, seed: int | None = None) -> np.ndarray:
+    """The key index each query of head ``h`` is planted on (a permutation)."""
+    seed = w.seed if seed is None else seed
+    return np.random.default_rng(seed * 7919 + h).permutation(w.S)
+
+
+def sample_rows(w: Workload, n: int | None = None, seed: int | None = None):
+    """Sorted query indices per head for oracle checks on the large shapes."""
+    n = w.oracle_rows if n is None else n
+    seed = w.seed if seed is None else seed
+    if n == 0 or n >= w.S:
+        return [np.arange(w.S, dtype=np.int64) for _ in range(w.H)]
+    rng = np.random.default_rng(seed + 1000)
+    return [np.sort(rng.choice(w.S, size=n, replace=False)).astype(np.int64)
+            for _ in range(w.H)]
+
