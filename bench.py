@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of the HCMS single-GPU hot path on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+pack Q/K/V of every head chunk, attention of every chunk, unpack of every
+chunk, scheduled on the copy and compute streams (``hcms_forward``, pipelined
+mode).  The workload is the Wan2.2-14B-shaped rank share at P = 8: S = 56160
+tokens (36 latent frames x 1560), H = 5 local heads, d = 128, bf16, chunks
+2 + 2 + 1 (the paper's uneven rule for C = 3).
+
+Printed: one JSON line with the metric (attention TFLOP/s, 4 S^2 H d per step
+over the pipelined step time), the roofline of the dominant kernel (attention,
+bf16 MFMA), the layout kernels' HBM rates, serial versus pipelined times, and
+the oracle timed on the host cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import paper_2607_01817_amd as hcms  # noqa: E402
+from paper_2607_01817_amd import inputs  # noqa: E402
+
+MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16: 256 CU x 2.4 GHz x 4096 FLOP/clk
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse_chunks(s: str) -> tuple[int, ...]:
+    return tuple(int(x) for x in s.replace("+", ",").split(",") if x)
+
+
+def flush_mall(buf: torch.Tensor):
+    """Overwrite a buffer larger than the 256 MB infinity cache."""
+    buf.add_(1)
+
+
+def time_region(fn, reps: int, stream=None) -> list[float]:
+    """Per-rep milliseconds of fn() from events on `stream` (default: current)."""
+    stream = stream or torch.cuda.current_stream()
+    out = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        b.synchronize()
+        out.append(a.elapsed_time(b))
+    return out
+
+
+def cpu_baseline(w, q, k, v, seconds: float):
+    """Time the oracle on sampled query rows of the same workload."""
+    import oracle
+    rows_all = inputs.sample_rows(w, 4096, seed=w.seed + 77)
+    heads = [(x[:, h, :].to(torch.float64).numpy() for x in (q, k, v)) for h in range(w.H)]
+    heads = [tuple(t) for t in heads]
+    done_rows = 0
+    t_cpu = 0.0
+    batch = 128
+    h = 0
+    pos = [0] * w.H
+    while t_cpu < seconds and done_rows < w.H * 4096:
+        qh, kh, vh = heads[h]
+        rows = rows_all[h][pos[h]:pos[h] + batch]
+        pos[h] += batch
+        t0 = time.perf_counter()
+        oracle.attention_head(qh, kh, vh, w.scale, rows)
+        t_cpu += time.perf_counter() - t0
+        done_rows += rows.size
+        h = (h + 1) % w.H
+    flops = 4.0 * done_rows * w.S * w.d
+    return {
+        "value": flops / t_cpu / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"{done_rows} query rows (128-row batches over the {w.H} heads) of the "
+                  f"same workload against all S={w.S} keys, fp64, {t_cpu:.1f} s; "
+                  f"full-problem time extrapolates to {w.flops / (flops / t_cpu):.0f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="wan_p8", choices=sorted(inputs.WORKLOADS))
+    ap.add_argument("--chunks", default="2,2,1")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time the step only (for profiler runs)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the hot path "
+              "is one GPU's share of HCMS and this build has no multi-GPU exchange.",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    w = inputs.WORKLOADS[args.workload]
+    sizes = parse_chunks(args.chunks)
+    assert sum(sizes) == w.H, f"chunks {sizes} do not sum to H={w.H}"
+    hcms.load()
+    dev = torch.device("cuda:0")
+    log(f"workload {w.name}: S={w.S} H={w.H} d={w.d} {w.dtype} P={w.P} chunks={sizes}")
+    q, k, v = inputs.make_qkv(w)
+    qd, kd, vd = (x.to(dev) for x in (q, k, v))
+    ctx = hcms.Context(max_chunks=max(16, len(sizes)))
+    out = torch.empty_like(qd)
+    ws = ctx.workspaces(w.S, w.H, w.d, qd.dtype)
+
+    def step(mode=hcms.MODE_PIPELINED, chunks=sizes):
+        ctx.forward(qd, kd, vd, w.P, w.scale, chunks, mode=mode, out=out, workspaces=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: K pipelined steps, kernels bracketed by events ----
+    ctx.set_timing(args.steps)
+    main_stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(main_stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(main_stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    attn_ms = ctx.kernel_ms(hcms.OP_ATTENTION)
+    pack_ms = ctx.kernel_ms(hcms.OP_PACK)
+    unpack_ms = ctx.kernel_ms(hcms.OP_UNPACK)
+    ctx.set_timing(0)
+
+    tflops = w.flops / (ms_per_step * 1e-3) / 1e12
+    # Attention roofline: algorithmic FLOPs of each launch / its duration.
+    C = len(sizes)
+    launch_flops = [4.0 * w.S * w.S * sizes[i % C] * w.d for i in range(len(attn_ms))]
+    avg_attn_ms = statistics.mean(attn_ms)
+    achieved = sum(launch_flops) / (sum(attn_ms) * 1e-3) / 1e12
+    result = {
+        "metric": "attention TFLOP/s (4·S²·H·d) + pipelined vs serial chunk time, 1 MI355X",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: seeded N(0,1)*0.5 Q/K/V, Wan2.2-shaped (no real activations)",
+        "config": {
+            "workload": f"{w.name}: S={w.S} (36 frames x 1560 tokens), H={w.H} local heads, "
+                        f"d={w.d}, {w.dtype}, P={w.P} shards, chunks {'+'.join(map(str, sizes))}, "
+                        "pipelined pack+attention+unpack",
+            "S": w.S, "H": w.H, "d": w.d, "P": w.P, "chunks": list(sizes),
+            "mode": "pipelined",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+            "kernel": "attention_kernel<128, bf16>",
+            "per_launch": f"4*S^2*H_c*d FLOP per chunk launch; avg launch {avg_attn_ms:.4f} ms "
+                          f"over {len(attn_ms)} launches in the timed region",
+        },
+    }
+
+    if not args.no_extras:
+        es = w.elem_bytes
+        seq_bytes = w.S * w.H * w.d * es
+        pk_bytes = [3 * 2 * w.S * sizes[i % C] * w.d * es for i in range(len(pack_ms))]
+        up_bytes = [2 * w.S * sizes[i % C] * w.d * es for i in range(len(unpack_ms))]
+        pipe = {"pack_in_pipeline_GBps": round(sum(pk_bytes) / (sum(pack_ms) * 1e-3) / 1e9, 1),
+                "unpack_in_pipeline_GBps": round(sum(up_bytes) / (sum(unpack_ms) * 1e-3) / 1e9, 1)}
+
+        # ---- layout kernels alone, MALL flushed before every rep ----
+        scratch = torch.zeros(768 * 2**20 // 4, dtype=torch.float32, device=dev)
+        hm = torch.empty((w.H, w.S, w.d), dtype=qd.dtype, device=dev)
+        reps = 20
+
+        def pack_rep():
+            hcms.pack(qd, w.P, 0, w.H, out=hm)
+
+        def unpack_rep():
+            hcms.unpack(hm, out, w.P, 0)
+
+        res = {}
+        for name, fn in (("pack", pack_rep), ("unpack", unpack_rep)):
+            ts = []
+            for _ in range(reps):
+                flush_mall(scratch)
+                ts += time_region(fn, 1)
+            med = statistics.median(ts)
+            gbs = 2 * seq_bytes / (med * 1e-3) / 1e9
+            res[name] = {"GBps": round(gbs, 1), "frac_of_hbm": round(gbs / HBM_PEAK_GBS, 4),
+                         "median_ms": round(med, 5), "bytes": 2 * seq_bytes}
+        del scratch, hm
+        res["note"] = ("one tensor, all heads, MALL overwritten before each rep; bytes = read + "
+                       "write of [S][H][d]")
+        res.update(pipe)
+        result["layout"] = res
+
+        # ---- serial vs pipelined, interleaved (ABAB) ----
+        torch.cuda.synchronize()
+        reps = max(10, args.steps)
+        cmp = {}
+        for label, chunks in (("chunked", sizes), ("unchunked", (w.H,))):
+            a, b = [], []
+            for _ in range(reps):
+                a += time_region(lambda: step(hcms.MODE_SERIAL, chunks), 1)
+                b += time_region(lambda: step(hcms.MODE_PIPELINED, chunks), 1)
+            qa, qb = np.percentile(a, [25, 50, 75]), np.percentile(b, [25, 50, 75])
+            cmp[label] = {"chunks": list(chunks),
+                          "serial_ms": {"median": round(qa[1], 4), "iqr": [round(qa[0], 4), round(qa[2], 4)]},
+                          "pipelined_ms": {"median": round(qb[1], 4), "iqr": [round(qb[0], 4), round(qb[2], 4)]},
+                          "pipelined_below_serial": bool(qb[2] < qa[0])}
+        result["pipeline"] = cmp
+
+    if not args.no_cpu:
+        log("timing the oracle on the host ...")
+        result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
+
+    ctx.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,236 @@
+/*
+ * hcms.h -- C ABI of the single-GPU hot path of HCMS (Head-Chunked Multi-Stream
+ * pipeline for sequence-parallel attention, arXiv 2607.01817) on AMD MI355X
+ * (gfx950).
+ *
+ * One GPU's share of HCMS under Ulysses sequence parallelism is: a layout
+ * permutation of each head chunk from sequence-sharded [P][S/P][H][d] to
+ * head-major [H_c][S][d] ("pack", the local share of the input all-to-all),
+ * full-sequence non-causal softmax attention on the chunk, and the inverse
+ * permutation back ("unpack", the local share of the output all-to-all plus the
+ * concatenation along heads), scheduled on a copy stream and a compute stream
+ * ordered by events (Sec. 3.4-3.6, Alg. 1).
+ *
+ * Conventions for every entry point
+ *   - Buffers are device memory owned by the caller, contiguous, row-major,
+ *     16-byte aligned.  The library allocates no device memory on any call
+ *     except hcms_ctx_create (which creates events only).
+ *   - `stream` arguments are hipStream_t handles passed as void*.  NULL is the
+ *     null stream of the current device.  Streams are borrowed, never destroyed.
+ *   - All compute calls are asynchronous and stream-ordered; a kernel fault
+ *     surfaces at the caller's next synchronisation.
+ *   - Arguments are validated completely before any HIP call: on error nothing
+ *     is enqueued and a negative hcms_status is returned.  hcms_last_error()
+ *     then gives a thread-local human-readable detail.  No C++ exception
+ *     crosses this boundary.
+ *   - Input and output buffers of one call must not overlap (checked; returns
+ *     HCMS_ERR_ALIAS).
+ *   - S = 0 (an empty sequence) is valid and enqueues nothing.
+ *   - Supported: d in {64, 128} for attention; for pack/unpack any d whose row
+ *     (d * element size) is a power of two from 16 to 1024 bytes; dtype bf16 or
+ *     fp32 storage.
+ *     Attention computes with bf16 MFMA operands and fp32 accumulation; fp32
+ *     storage is rounded to bf16 (nearest-even) when loaded.
+ *   - Calls on different streams that write the same buffer race; ordering is
+ *     the caller's (or hcms_forward's) business.
+ */
+#ifndef HCMS_H
+#define HCMS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HCMS_ABI_VERSION 1
+
+#if defined(__GNUC__)
+#define HCMS_API __attribute__((visibility("default")))
+#else
+#define HCMS_API
+#endif
+
+typedef enum hcms_dtype {
+    HCMS_BF16 = 0, /* 2-byte bfloat16 storage */
+    HCMS_FP32 = 1  /* 4-byte IEEE float storage */
+} hcms_dtype;
+
+typedef enum hcms_status {
+    HCMS_OK = 0,
+    HCMS_ERR_NULL = -1,     /* a required pointer is NULL */
+    HCMS_ERR_SHAPE = -2,    /* S < 0, H < 1, P < 1, S % P != 0, unsupported d, size overflow */
+    HCMS_ERR_CHUNKS = -3,   /* n_chunks < 1 or > H, a size < 1, sizes not summing to H,
+                               head range outside [0, H), more chunks than the context holds */
+    HCMS_ERR_DTYPE = -4,    /* dtype not one of hcms_dtype */
+    HCMS_ERR_ALIGN = -5,    /* a buffer is not 16-byte aligned */
+    HCMS_ERR_HIP = -6,      /* a HIP runtime call or kernel launch failed */
+    HCMS_ERR_ARG = -7,      /* bad scalar argument: scale not finite and > 0, bad mode,
+                               context bound to another device */
+    HCMS_ERR_ALIAS = -8,    /* an input buffer overlaps an output buffer */
+    HCMS_ERR_CAPACITY = -9  /* output array too small (hcms_plan, timing queries) */
+} hcms_status;
+
+/* ABI version of the loaded library (HCMS_ABI_VERSION it was built with). */
+HCMS_API int hcms_abi_version(void);
+
+/* Static string naming a status code ("HCMS_OK", "HCMS_ERR_SHAPE", ...). */
+HCMS_API const char *hcms_status_string(int status);
+
+/* Thread-local detail of the last error returned on this thread ("" if none).
+   Valid until the next hcms_* call on the same thread. */
+HCMS_API const char *hcms_last_error(void);
+
+/*
+ * Head-chunk sizes for H heads in C chunks, larger chunks first
+ * (Sec. 3.3, chunk-size equation: H_c = floor(H/C) + 1 if c < H mod C, else
+ * floor(H/C); Sec. 4.1 calls it "more-first-less-later").
+ *   sizes_out : host array of C ints, written on success.
+ * Returns HCMS_OK, HCMS_ERR_NULL, or HCMS_ERR_CHUNKS unless 1 <= C <= H.
+ */
+HCMS_API int hcms_default_chunks(int H, int C, int *sizes_out);
+
+/*
+ * Pack one head chunk (Sec. 3.3 split along heads + the local share of the
+ * input all-to-all of Sec. 3.1, Alg. 1 SplitByHeads / AllToAll):
+ *   dst_hm[j][p*(S/P) + s][e] = src_seq[p][s][h_begin + j][e]
+ * for p < P, s < S/P, j < h_count, e < d.  A pure byte move.
+ *   src_seq : device, [P][S/P][H][d] (identical bytes to [S][H][d])
+ *   dst_hm  : device, [h_count][S][d]
+ *   dtype   : element size only (the move is bit-exact)
+ * Errors: NULL, SHAPE (S % P, row size), CHUNKS (head range), DTYPE,
+ * ALIGN, ALIAS, HIP.
+ */
+HCMS_API int hcms_pack(const void *src_seq, void *dst_hm, int P, int S, int H, int d,
+              int h_begin, int h_count, int dtype, void *stream);
+
+/*
+ * Inverse of hcms_pack (the local share of the output all-to-all and the
+ * concatenation along heads of Alg. 1):
+ *   dst_seq[p][s][h_begin + j][e] = src_hm[j][p*(S/P) + s][e]
+ * Head slots outside [h_begin, h_begin + h_count) of dst_seq are not touched.
+ * Same arguments and errors as hcms_pack.
+ */
+HCMS_API int hcms_unpack(const void *src_hm, void *dst_seq, int P, int S, int H, int d,
+                int h_begin, int h_count, int dtype, void *stream);
+
+/*
+ * Head-chunked attention (Sec. 3.3 Property of computational independence;
+ * Alg. 1, compute-stream loop): for every head h < H and query i < S
+ *   O[h][i] = sum_j softmax_j(scale * <Q[h][i], K[h][j]>) V[h][j]
+ * over all S keys (non-causal, no mask).  The heads are processed as
+ * n_chunks consecutive ranges of chunk_sizes[c] heads, one kernel launch per
+ * chunk, in order, on `stream`.
+ *   q, k, v, out : device, head-major [H][S][d]
+ *   scale        : finite and > 0 (1/sqrt(d) for the usual attention)
+ *   chunk_sizes  : host array of n_chunks positive ints summing to H
+ * The result for a head does not depend on how the heads are chunked: any two
+ * chunkings give bit-identical outputs.  Runs are deterministic.
+ * Errors: NULL, SHAPE (d not 64/128), CHUNKS, DTYPE, ALIGN, ARG, ALIAS, HIP.
+ */
+HCMS_API int hcms_attention(const void *q, const void *k, const void *v, void *out,
+                   int S, int H, int d, float scale,
+                   const int *chunk_sizes, int n_chunks, int dtype, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Scheduler                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Modes of hcms_forward / hcms_plan. */
+#define HCMS_MODE_SERIAL 0     /* every op on the main stream, chunk by chunk */
+#define HCMS_MODE_PIPELINED 1  /* Alg. 1: copy stream + compute stream + events */
+
+/* Op kinds, streams and event ids of a plan (hcms_plan). */
+#define HCMS_OP_RECORD 0     /* record event `event` on `stream` */
+#define HCMS_OP_WAIT 1       /* make `stream` wait for event `event` */
+#define HCMS_OP_PACK 2       /* pack Q, K and V of chunk `chunk` */
+#define HCMS_OP_ATTENTION 3  /* attention of chunk `chunk` */
+#define HCMS_OP_UNPACK 4     /* unpack O of chunk `chunk` */
+
+#define HCMS_STREAM_MAIN 0
+#define HCMS_STREAM_COPY 1
+#define HCMS_STREAM_COMPUTE 2
+
+typedef struct hcms_op {
+    int kind;    /* HCMS_OP_* */
+    int stream;  /* HCMS_STREAM_* */
+    int chunk;   /* chunk index of PACK / ATTENTION / UNPACK, else -1 */
+    int event;   /* event id of RECORD / WAIT, else -1.  With C chunks:
+                    0 = E_main, 1 + c = E_c^pack, 1 + C + c = E_c^attn,
+                    1 + 2C = E_done */
+} hcms_op;
+
+/*
+ * Dry run of the scheduler: the exact op sequence hcms_forward issues, in host
+ * issue order.  Pipelined mode follows Alg. 1: record E_main on main; the copy
+ * stream waits E_main and packs chunk c then records E_c^pack, for every c;
+ * the compute stream waits E_main, then for every c waits E_c^pack, runs the
+ * attention of c and records E_c^attn; the copy stream then, for every c, waits
+ * E_c^attn and unpacks c; finally E_done is recorded on the copy stream and the
+ * main stream waits it (the join of Alg. 1 as a stream wait, not a host sync).
+ * Serial mode is pack c, attention c, unpack c on the main stream for every c.
+ *   ops : host array of `cap` entries, or NULL to query the count.
+ * Returns the number of ops (>= 0), HCMS_ERR_CHUNKS (n_chunks < 1),
+ * HCMS_ERR_ARG (mode) or HCMS_ERR_CAPACITY (cap too small; nothing written).
+ */
+HCMS_API int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap);
+
+typedef struct hcms_ctx hcms_ctx;
+
+/*
+ * Create a scheduler context bound to HIP device `device`: it owns the events
+ * of up to `max_chunks` chunks (created once, reused by every call; the
+ * device-level stream/event caching of Sec. 4.1), so hcms_forward creates
+ * nothing.  Errors: NULL, ARG (device out of range), CHUNKS (max_chunks < 1),
+ * HIP.
+ */
+HCMS_API int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out);
+
+/* Destroy a context (its events).  The caller must not destroy it while work
+   that waits on its events is still pending.  NULL is accepted. */
+HCMS_API int hcms_ctx_destroy(hcms_ctx *ctx);
+
+/*
+ * Per-kernel timing (for benchmarks).  hcms_ctx_set_timing(ctx, max_calls)
+ * with max_calls > 0 makes the next max_calls hcms_forward calls bracket every
+ * pack, attention and unpack launch with timing events on the stream that
+ * runs it (events are created here, once; later calls are not timed);
+ * max_calls = 0 turns timing off.  Each call resets the record.
+ * hcms_ctx_kernel_ms waits for the recorded events and writes the durations in
+ * milliseconds, call by call and chunk by chunk, in issue order.
+ *   kind : HCMS_OP_PACK, HCMS_OP_ATTENTION or HCMS_OP_UNPACK
+ * Returns the number of durations written, HCMS_ERR_ARG (timing off / bad
+ * kind / max_calls < 0), HCMS_ERR_CAPACITY or HCMS_ERR_HIP.
+ */
+HCMS_API int hcms_ctx_set_timing(hcms_ctx *ctx, int max_calls);
+HCMS_API int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap);
+
+/*
+ * The single-GPU share of one HCMS forward (Alg. 1 from SplitByHeads to the
+ * final Concat): for every chunk c with heads [h0_c, h0_c + H_c),
+ *   pack Q, K, V of the chunk into heads [h0_c, h0_c + H_c) of the head-major
+ *   workspaces, run attention on them into o_hm, and unpack o_hm's chunk into
+ *   the head slots [h0_c, h0_c + H_c) of o_seq,
+ * scheduled as hcms_plan(n_chunks, mode) describes.  Returns when everything
+ * is enqueued; `main_stream` is ordered after all of it on return (no host
+ * synchronisation).  Serial and pipelined modes, and all chunkings, give
+ * bit-identical o_seq.
+ *   q_seq, k_seq, v_seq, o_seq : device, [P][S/P][H][d]
+ *   q_hm, k_hm, v_hm, o_hm     : device workspaces, [H][S][d] each
+ *   copy_stream, compute_stream: used in pipelined mode; must be distinct from
+ *                                each other and from main_stream
+ * Errors: as hcms_pack and hcms_attention, plus ARG (mode, stream reuse,
+ * context of another device) and CHUNKS (n_chunks > the context's max_chunks).
+ */
+HCMS_API int hcms_forward(hcms_ctx *ctx,
+                 const void *q_seq, const void *k_seq, const void *v_seq, void *o_seq,
+                 void *q_hm, void *k_hm, void *v_hm, void *o_hm,
+                 int P, int S, int H, int d, float scale,
+                 const int *chunk_sizes, int n_chunks, int dtype, int mode,
+                 void *main_stream, void *copy_stream, void *compute_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HCMS_H */

@@ -1,1 +1,276 @@
-"""HCMS single-GPU hot path on MI355X (binding is added with the C ABI)."""
+"""HCMS single-GPU hot path on AMD MI355X (gfx950).
+
+A thin ctypes binding over ``libhcms.so`` (the C ABI in ``include/hcms.h``).
+Every step runs in the library's HIP kernels.  This module only checks tensors
+(device, dtype, shape, contiguity), passes their device pointers and HIP
+stream handles, and turns status codes into exceptions.  PyTorch provides
+device memory and streams.
+
+Names follow the paper (arXiv 2607.01817): ``pack``/``unpack`` are one GPU's
+share of the input/output all-to-all of a head chunk, ``attention`` runs the
+chunks' attention, and :class:`Context` is the dual-stream chunk scheduler
+of Alg. 1 with its cached events.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhcms.so")
+
+BF16, FP32 = 0, 1
+MODE_SERIAL, MODE_PIPELINED = 0, 1
+OP_RECORD, OP_WAIT, OP_PACK, OP_ATTENTION, OP_UNPACK = 0, 1, 2, 3, 4
+STREAM_MAIN, STREAM_COPY, STREAM_COMPUTE = 0, 1, 2
+
+_DTYPES = {torch.bfloat16: BF16, torch.float32: FP32}
+_lib = None
+
+
+class HcmsError(RuntimeError):
+    """A negative status from the C ABI, with the library's detail string."""
+
+    def __init__(self, status: int, name: str, detail: str):
+        super().__init__(f"{name} ({status}): {detail}")
+        self.status = status
+        self.name = name
+        self.detail = detail
+
+
+class Op(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("stream", ctypes.c_int),
+                ("chunk", ctypes.c_int), ("event", ctypes.c_int)]
+
+
+def load():
+    """Load ``libhcms.so`` (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2607_01817_amd.build` (no CPU fallback exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i, vp, f = ctypes.c_int, ctypes.c_void_p, ctypes.c_float
+    ip = ctypes.POINTER(ctypes.c_int)
+    sig = {
+        "hcms_abi_version": ([], i),
+        "hcms_status_string": ([i], ctypes.c_char_p),
+        "hcms_last_error": ([], ctypes.c_char_p),
+        "hcms_default_chunks": ([i, i, ip], i),
+        "hcms_pack": ([vp, vp, i, i, i, i, i, i, i, vp], i),
+        "hcms_unpack": ([vp, vp, i, i, i, i, i, i, i, vp], i),
+        "hcms_attention": ([vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
+        "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
+        "hcms_ctx_create": ([i, i, ctypes.POINTER(vp)], i),
+        "hcms_ctx_destroy": ([vp], i),
+        "hcms_ctx_set_timing": ([vp, i], i),
+        "hcms_ctx_kernel_ms": ([vp, i, ctypes.POINTER(ctypes.c_float), i], i),
+        "hcms_forward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, ip, i, i, i,
+                          vp, vp, vp], i),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> int:
+    if status < 0:
+        lib = load()
+        raise HcmsError(status, lib.hcms_status_string(status).decode(),
+                        lib.hcms_last_error().decode())
+    return status
+
+
+def _ints(xs):
+    xs = [int(x) for x in xs]
+    return (ctypes.c_int * max(1, len(xs)))(*xs), len(xs)
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32")
+    return _DTYPES[t.dtype]
+
+
+def _dev(t: torch.Tensor, name: str):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream(s) -> ctypes.c_void_p:
+    if s is None:
+        s = torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def abi_version() -> int:
+    return load().hcms_abi_version()
+
+
+def default_chunks(H: int, C: int) -> list[int]:
+    """Chunk sizes of the paper's rule (more first, less later)."""
+    buf = (ctypes.c_int * max(1, C))()
+    _check(load().hcms_default_chunks(H, C, buf))
+    return list(buf[:C])
+
+
+def plan(n_chunks: int, mode: int = MODE_PIPELINED) -> list[tuple[int, int, int, int]]:
+    """The op list hcms_forward issues: (kind, stream, chunk, event) tuples."""
+    lib = load()
+    n = _check(lib.hcms_plan(n_chunks, mode, None, 0))
+    ops = (Op * n)()
+    _check(lib.hcms_plan(n_chunks, mode, ops, n))
+    return [(o.kind, o.stream, o.chunk, o.event) for o in ops]
+
+
+def pack(src_seq: torch.Tensor, P: int, h_begin: int, h_count: int,
+         out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """[S][H][d] (= [P][S/P][H][d]) -> [h_count][S][d] chunk of heads."""
+    _dev(src_seq, "src_seq")
+    S, H, d = src_seq.shape
+    if out is None:
+        out = torch.empty((h_count, S, d), dtype=src_seq.dtype, device=src_seq.device)
+    _dev(out, "out")
+    if out.shape != (h_count, S, d) or out.dtype != src_seq.dtype:
+        raise ValueError("out must be [h_count][S][d] of the source dtype")
+    _check(load().hcms_pack(src_seq.data_ptr(), out.data_ptr(), P, S, H, d, h_begin, h_count,
+                            _dtype(src_seq), _stream(stream)))
+    return out
+
+
+def unpack(src_hm: torch.Tensor, dst_seq: torch.Tensor, P: int, h_begin: int,
+           stream=None) -> torch.Tensor:
+    """Write the [h_count][S][d] chunk into head slots of dst_seq [S][H][d]."""
+    _dev(src_hm, "src_hm")
+    _dev(dst_seq, "dst_seq")
+    hc, S, d = src_hm.shape
+    if dst_seq.dim() != 3 or dst_seq.shape[0] != S or dst_seq.shape[2] != d \
+            or dst_seq.dtype != src_hm.dtype:
+        raise ValueError("dst_seq must be [S][H][d] of the chunk's dtype")
+    H = dst_seq.shape[1]
+    _check(load().hcms_unpack(src_hm.data_ptr(), dst_seq.data_ptr(), P, S, H, d, h_begin, hc,
+                              _dtype(src_hm), _stream(stream)))
+    return dst_seq
+
+
+def attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float,
+              chunk_sizes=None, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Non-causal softmax attention on head-major [H][S][d] tensors, run as
+    one kernel launch per head chunk (default: one chunk of all heads)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _dev(t, n)
+    if not (q.shape == k.shape == v.shape) or q.dim() != 3:
+        raise ValueError("q, k, v must all be [H][S][d]")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise ValueError("q, k, v must share a dtype")
+    H, S, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out")
+    if out.shape != q.shape or out.dtype != q.dtype:
+        raise ValueError("out must match q")
+    sizes, n = _ints([H] if chunk_sizes is None else chunk_sizes)
+    _check(load().hcms_attention(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                 S, H, d, float(scale), sizes, n, _dtype(q), _stream(stream)))
+    return out
+
+
+class Context:
+    """The dual-stream chunk scheduler (Alg. 1) bound to one device.
+
+    Owns the library context (cached events), a copy stream and a compute
+    stream (default priority), and head-major workspaces that are reallocated
+    only when the problem shape grows.
+    """
+
+    def __init__(self, device: int = 0, max_chunks: int = 64):
+        lib = load()
+        self.device = device
+        self.max_chunks = max_chunks
+        h = ctypes.c_void_p()
+        with torch.cuda.device(device):
+            _check(lib.hcms_ctx_create(device, max_chunks, ctypes.byref(h)))
+            self.copy_stream = torch.cuda.Stream(device=device)
+            self.compute_stream = torch.cuda.Stream(device=device)
+        self._h = h
+        self._ws = None
+        self._ws_key = None
+
+    def close(self):
+        if self._h:
+            torch.cuda.synchronize(self.device)
+            load().hcms_ctx_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            if self._h and _lib is not None:
+                _lib.hcms_ctx_destroy(self._h)
+        except Exception:
+            pass
+
+    def workspaces(self, S: int, H: int, d: int, dtype: torch.dtype):
+        key = (S, H, d, dtype)
+        if self._ws_key != key:
+            self._ws = [torch.empty((H, S, d), dtype=dtype, device=f"cuda:{self.device}")
+                        for _ in range(4)]
+            self._ws_key = key
+        return self._ws
+
+    def set_timing(self, max_calls: int):
+        """Time every kernel of the next ``max_calls`` forward calls (0: off)."""
+        _check(load().hcms_ctx_set_timing(self._h, int(max_calls)))
+        self._timing_calls = int(max_calls)
+
+    def kernel_ms(self, kind: int) -> list[float]:
+        """Durations (ms) of the timed calls' kernels of one kind, call by call
+        and chunk by chunk (waits for them)."""
+        cap = max(1, getattr(self, "_timing_calls", 0)) * self.max_chunks
+        buf = (ctypes.c_float * cap)()
+        n = _check(load().hcms_ctx_kernel_ms(self._h, kind, buf, cap))
+        return list(buf[:n])
+
+    def forward(self, q_seq: torch.Tensor, k_seq: torch.Tensor, v_seq: torch.Tensor, P: int,
+                scale: float, chunk_sizes, mode: int = MODE_PIPELINED,
+                out: torch.Tensor | None = None, workspaces=None,
+                main_stream=None) -> torch.Tensor:
+        """One GPU's share of an HCMS forward: [S][H][d] in, [S][H][d] out.
+
+        The result is ordered on ``main_stream`` (default: the current stream)
+        when this returns; nothing blocks the host.
+        """
+        for t, n in ((q_seq, "q_seq"), (k_seq, "k_seq"), (v_seq, "v_seq")):
+            _dev(t, n)
+        if not (q_seq.shape == k_seq.shape == v_seq.shape) or q_seq.dim() != 3:
+            raise ValueError("q_seq, k_seq, v_seq must all be [S][H][d]")
+        if not (q_seq.dtype == k_seq.dtype == v_seq.dtype):
+            raise ValueError("q_seq, k_seq, v_seq must share a dtype")
+        S, H, d = q_seq.shape
+        if out is None:
+            out = torch.empty_like(q_seq)
+        _dev(out, "out")
+        if out.shape != q_seq.shape or out.dtype != q_seq.dtype:
+            raise ValueError("out must match q_seq")
+        ws = workspaces if workspaces is not None else self.workspaces(S, H, d, q_seq.dtype)
+        for t in ws:
+            _dev(t, "workspace")
+            if t.numel() != q_seq.numel() or t.dtype != q_seq.dtype:
+                raise ValueError("each workspace must hold [H][S][d] of the input dtype")
+        sizes, n = _ints(chunk_sizes)
+        main = _stream(main_stream)
+        _check(load().hcms_forward(
+            self._h, q_seq.data_ptr(), k_seq.data_ptr(), v_seq.data_ptr(), out.data_ptr(),
+            ws[0].data_ptr(), ws[1].data_ptr(), ws[2].data_ptr(), ws[3].data_ptr(),
+            P, S, H, d, float(scale), sizes, n, _dtype(q_seq), int(mode), main,
+            ctypes.c_void_p(self.copy_stream.cuda_stream),
+            ctypes.c_void_p(self.compute_stream.cuda_stream)))
+        return out

@@ -1,0 +1,516 @@
+// C ABI of the HCMS single-GPU hot path: argument validation, the chunk
+// scheduler (Alg. 1 as an op list plus an executor on HIP streams/events) and
+// the event-caching context.  Declarations and the contract live in hcms.h.
+#include "hcms.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <new>
+#include <vector>
+
+#include "hcms_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok() {
+    g_last_error[0] = '\0';
+    return HCMS_OK;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(HCMS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int elem_bytes(int dtype) { return dtype == HCMS_BF16 ? 2 : 4; }
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Byte ranges [a, a + na) and [b, b + nb) overlap.
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+    if (na <= 0 || nb <= 0) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + static_cast<uintptr_t>(nb) && y < x + static_cast<uintptr_t>(na);
+}
+
+int check_dtype(int dtype) {
+    if (dtype != HCMS_BF16 && dtype != HCMS_FP32)
+        return fail(HCMS_ERR_DTYPE, "dtype %d is neither HCMS_BF16 (0) nor HCMS_FP32 (1)", dtype);
+    return HCMS_OK;
+}
+
+// S >= 0, H >= 1, P >= 1, S % P == 0, and the [S][H][d] tensor fits int64
+// bytes and each head's [S][d] fits the 32-bit range of a buffer resource.
+int check_dims(int P, int S, int H, int d, int dtype) {
+    if (S < 0 || H < 1 || P < 1 || d < 1)
+        return fail(HCMS_ERR_SHAPE, "need S >= 0, H >= 1, P >= 1, d >= 1 (S=%d H=%d P=%d d=%d)", S,
+                    H, P, d);
+    if (S % P != 0)
+        return fail(HCMS_ERR_SHAPE, "S=%d is not a multiple of the shard count P=%d", S, P);
+    const int64_t head_bytes = static_cast<int64_t>(S) * d * elem_bytes(dtype);
+    if (head_bytes > 0x7fffffffLL)
+        return fail(HCMS_ERR_SHAPE, "one head is %lld bytes; the limit is 2^31 - 1",
+                    static_cast<long long>(head_bytes));
+    return HCMS_OK;
+}
+
+// Pack / unpack rows are moved as 16-byte units: d * elem must be 16 << k.
+int row_log2_units(int d, int dtype, int *log2_units) {
+    const int row = d * elem_bytes(dtype);
+    for (int k = 0; k <= 6; ++k)
+        if (row == (16 << k)) {
+            *log2_units = k;
+            return HCMS_OK;
+        }
+    return fail(HCMS_ERR_SHAPE,
+                "pack/unpack need d * element size in {16, 32, ..., 1024} bytes (d=%d, %d bytes)", d,
+                row);
+}
+
+int check_chunks(int H, const int *sizes, int n) {
+    if (!sizes) return fail(HCMS_ERR_NULL, "chunk_sizes is NULL");
+    if (n < 1 || n > H) return fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be in [1, H=%d]", n, H);
+    int64_t sum = 0;
+    for (int c = 0; c < n; ++c) {
+        if (sizes[c] < 1) return fail(HCMS_ERR_CHUNKS, "chunk %d has %d heads", c, sizes[c]);
+        sum += sizes[c];
+    }
+    if (sum != H)
+        return fail(HCMS_ERR_CHUNKS, "chunk sizes sum to %lld, not H=%d", static_cast<long long>(sum), H);
+    return HCMS_OK;
+}
+
+int check_scale(float scale) {
+    if (!std::isfinite(scale) || !(scale > 0.0f))
+        return fail(HCMS_ERR_ARG, "scale must be finite and > 0 (got %g)", static_cast<double>(scale));
+    return HCMS_OK;
+}
+
+int check_pack_args(const void *a, const void *b, int P, int S, int H, int d, int h_begin,
+                    int h_count, int dtype, int *log2_units) {
+    int st;
+    if (!a || !b) return fail(HCMS_ERR_NULL, "source or destination is NULL");
+    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
+    if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
+    if ((st = row_log2_units(d, dtype, log2_units)) != HCMS_OK) return st;
+    if (h_begin < 0 || h_count < 1 || h_begin > H - h_count)
+        return fail(HCMS_ERR_CHUNKS, "head range [%d, %d + %d) is not inside [0, H=%d)", h_begin,
+                    h_begin, h_count, H);
+    if (!aligned16(a) || !aligned16(b)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t es = elem_bytes(dtype);
+    const int64_t seq_bytes = static_cast<int64_t>(S) * H * d * es;
+    const int64_t hm_bytes = static_cast<int64_t>(S) * h_count * d * es;
+    if (overlaps(a, seq_bytes, b, hm_bytes) || overlaps(a, hm_bytes, b, seq_bytes))
+        return fail(HCMS_ERR_ALIAS, "source and destination overlap");
+    return HCMS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Plan (Alg. 1 as an op list)
+// ---------------------------------------------------------------------------
+struct PlanWriter {
+    hcms_op *ops;
+    int cap;
+    int n = 0;
+    void put(int kind, int stream, int chunk, int event) {
+        if (ops && n < cap) ops[n] = hcms_op{kind, stream, chunk, event};
+        ++n;
+    }
+};
+
+int build_plan(int C, int mode, PlanWriter &w) {
+    const int e_main = 0, e_done = 1 + 2 * C;
+    auto e_pack = [](int c) { return 1 + c; };
+    auto e_attn = [C](int c) { return 1 + C + c; };
+    if (mode == HCMS_MODE_SERIAL) {
+        for (int c = 0; c < C; ++c) {
+            w.put(HCMS_OP_PACK, HCMS_STREAM_MAIN, c, -1);
+            w.put(HCMS_OP_ATTENTION, HCMS_STREAM_MAIN, c, -1);
+            w.put(HCMS_OP_UNPACK, HCMS_STREAM_MAIN, c, -1);
+        }
+        return w.n;
+    }
+    // Main stream: fork.
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_MAIN, -1, e_main);
+    // Copy stream: input layout of every chunk.
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COPY, -1, e_main);
+    for (int c = 0; c < C; ++c) {
+        w.put(HCMS_OP_PACK, HCMS_STREAM_COPY, c, -1);
+        w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_pack(c));
+    }
+    // Compute stream: attention of chunk c as soon as its inputs are laid out.
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COMPUTE, -1, e_main);
+    for (int c = 0; c < C; ++c) {
+        w.put(HCMS_OP_WAIT, HCMS_STREAM_COMPUTE, -1, e_pack(c));
+        w.put(HCMS_OP_ATTENTION, HCMS_STREAM_COMPUTE, c, -1);
+        w.put(HCMS_OP_RECORD, HCMS_STREAM_COMPUTE, -1, e_attn(c));
+    }
+    // Copy stream: output layout of chunk c once its attention is done.
+    for (int c = 0; c < C; ++c) {
+        w.put(HCMS_OP_WAIT, HCMS_STREAM_COPY, -1, e_attn(c));
+        w.put(HCMS_OP_UNPACK, HCMS_STREAM_COPY, c, -1);
+    }
+    // Join: the main stream is ordered after the last unpack, which is itself
+    // ordered after the last attention.
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_done);
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
+    return w.n;
+}
+
+int plan_size(int C, int mode) { return mode == HCMS_MODE_SERIAL ? 3 * C : 7 * C + 5; }
+
+// Saves the current device, switches to `dev`, restores on scope exit.
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t err = hipSuccess;
+    explicit DeviceGuard(int dev) {
+        err = hipGetDevice(&prev);
+        if (err == hipSuccess && prev != dev) err = hipSetDevice(dev);
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+}  // namespace
+
+struct hcms_ctx {
+    int device = 0;
+    int max_chunks = 0;
+    std::vector<hipEvent_t> events;      // 2 * max_chunks + 2 sync events
+    std::vector<hcms_op> plan;           // scratch for the op list
+    int timing_calls = 0;                // calls to time (0 = off)
+    std::vector<hipEvent_t> t_begin;     // [call][kind][chunk] timing events
+    std::vector<hipEvent_t> t_end;
+    std::vector<int> timed_chunks;       // chunk count of each timed call
+};
+
+extern "C" {
+
+int hcms_abi_version(void) { return HCMS_ABI_VERSION; }
+
+const char *hcms_status_string(int status) {
+    switch (status) {
+        case HCMS_OK: return "HCMS_OK";
+        case HCMS_ERR_NULL: return "HCMS_ERR_NULL";
+        case HCMS_ERR_SHAPE: return "HCMS_ERR_SHAPE";
+        case HCMS_ERR_CHUNKS: return "HCMS_ERR_CHUNKS";
+        case HCMS_ERR_DTYPE: return "HCMS_ERR_DTYPE";
+        case HCMS_ERR_ALIGN: return "HCMS_ERR_ALIGN";
+        case HCMS_ERR_HIP: return "HCMS_ERR_HIP";
+        case HCMS_ERR_ARG: return "HCMS_ERR_ARG";
+        case HCMS_ERR_ALIAS: return "HCMS_ERR_ALIAS";
+        case HCMS_ERR_CAPACITY: return "HCMS_ERR_CAPACITY";
+        default: return "HCMS_UNKNOWN_STATUS";
+    }
+}
+
+const char *hcms_last_error(void) { return g_last_error; }
+
+int hcms_default_chunks(int H, int C, int *sizes_out) {
+    if (!sizes_out) return fail(HCMS_ERR_NULL, "sizes_out is NULL");
+    if (H < 1 || C < 1 || C > H) return fail(HCMS_ERR_CHUNKS, "need 1 <= C <= H (H=%d, C=%d)", H, C);
+    const int base = H / C, extra = H % C;
+    for (int c = 0; c < C; ++c) sizes_out[c] = base + (c < extra ? 1 : 0);
+    return ok();
+}
+
+int hcms_pack(const void *src_seq, void *dst_hm, int P, int S, int H, int d, int h_begin,
+              int h_count, int dtype, void *stream) {
+    int log2u = 0;
+    const int st = check_pack_args(src_seq, dst_hm, P, S, H, d, h_begin, h_count, dtype, &log2u);
+    if (st != HCMS_OK) return st;
+    const void *src[1] = {src_seq};
+    void *dst[1] = {dst_hm};
+    const hipError_t e = hcms::launch_pack(src, dst, 1, S, H, h_begin, h_count, log2u,
+                                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "pack launch");
+    return ok();
+}
+
+int hcms_unpack(const void *src_hm, void *dst_seq, int P, int S, int H, int d, int h_begin,
+                int h_count, int dtype, void *stream) {
+    int log2u = 0;
+    const int st = check_pack_args(src_hm, dst_seq, P, S, H, d, h_begin, h_count, dtype, &log2u);
+    if (st != HCMS_OK) return st;
+    const hipError_t e = hcms::launch_unpack(src_hm, dst_seq, S, H, h_begin, h_count, log2u,
+                                             static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "unpack launch");
+    return ok();
+}
+
+static int check_attention_args(const void *q, const void *k, const void *v, const void *out, int S,
+                                int H, int d, float scale, const int *sizes, int n, int dtype) {
+    int st;
+    if (!q || !k || !v || !out) return fail(HCMS_ERR_NULL, "q, k, v or out is NULL");
+    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
+    if ((st = check_dims(1, S, H, d, dtype)) != HCMS_OK) return st;
+    if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
+    if ((st = check_chunks(H, sizes, n)) != HCMS_OK) return st;
+    if ((st = check_scale(scale)) != HCMS_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+        return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
+    if (overlaps(q, bytes, out, bytes) || overlaps(k, bytes, out, bytes) || overlaps(v, bytes, out, bytes))
+        return fail(HCMS_ERR_ALIAS, "out overlaps q, k or v");
+    return HCMS_OK;
+}
+
+static float scale_log2e(float scale) {
+    return static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+}
+
+int hcms_attention(const void *q, const void *k, const void *v, void *out, int S, int H, int d,
+                   float scale, const int *chunk_sizes, int n_chunks, int dtype, void *stream) {
+    const int st = check_attention_args(q, k, v, out, S, H, d, scale, chunk_sizes, n_chunks, dtype);
+    if (st != HCMS_OK) return st;
+    const int64_t head = static_cast<int64_t>(S) * d * elem_bytes(dtype);
+    const float c = scale_log2e(scale);
+    int h0 = 0;
+    for (int i = 0; i < n_chunks; ++i) {
+        const int64_t off = head * h0;
+        const hipError_t e = hcms::launch_attention(
+            static_cast<const char *>(q) + off, static_cast<const char *>(k) + off,
+            static_cast<const char *>(v) + off, static_cast<char *>(out) + off, S, chunk_sizes[i], d,
+            c, dtype, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "attention launch");
+        h0 += chunk_sizes[i];
+    }
+    return ok();
+}
+
+int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
+    if (n_chunks < 1) return fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be >= 1", n_chunks);
+    if (mode != HCMS_MODE_SERIAL && mode != HCMS_MODE_PIPELINED)
+        return fail(HCMS_ERR_ARG, "mode %d is neither serial (0) nor pipelined (1)", mode);
+    const int need = plan_size(n_chunks, mode);
+    if (ops == nullptr) {
+        ok();
+        return need;
+    }
+    if (cap < need) return fail(HCMS_ERR_CAPACITY, "plan needs %d ops, capacity is %d", need, cap);
+    PlanWriter w{ops, cap};
+    const int n = build_plan(n_chunks, mode, w);
+    ok();
+    return n;
+}
+
+int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out) {
+    if (!out) return fail(HCMS_ERR_NULL, "out is NULL");
+    *out = nullptr;
+    if (max_chunks < 1) return fail(HCMS_ERR_CHUNKS, "max_chunks=%d must be >= 1", max_chunks);
+    int n_dev = 0;
+    hipError_t e = hipGetDeviceCount(&n_dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceCount");
+    if (device < 0 || device >= n_dev)
+        return fail(HCMS_ERR_ARG, "device %d out of range [0, %d)", device, n_dev);
+    DeviceGuard guard(device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    hcms_ctx *ctx = new (std::nothrow) hcms_ctx;
+    if (!ctx) return fail(HCMS_ERR_ARG, "out of host memory");
+    ctx->device = device;
+    ctx->max_chunks = max_chunks;
+    ctx->plan.resize(plan_size(max_chunks, HCMS_MODE_PIPELINED));
+    const int n_sync = 2 * max_chunks + 2;
+    for (int i = 0; i < n_sync; ++i) {
+        hipEvent_t ev;
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            hcms_ctx_destroy(ctx);
+            return hip_fail(e, "hipEventCreateWithFlags");
+        }
+        ctx->events.push_back(ev);
+    }
+    *out = ctx;
+    return ok();
+}
+
+int hcms_ctx_destroy(hcms_ctx *ctx) {
+    if (!ctx) return ok();
+    DeviceGuard guard(ctx->device);
+    for (hipEvent_t ev : ctx->events) (void)hipEventDestroy(ev);
+    for (hipEvent_t ev : ctx->t_begin) (void)hipEventDestroy(ev);
+    for (hipEvent_t ev : ctx->t_end) (void)hipEventDestroy(ev);
+    delete ctx;
+    return ok();
+}
+
+int hcms_ctx_set_timing(hcms_ctx *ctx, int max_calls) {
+    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    if (max_calls < 0) return fail(HCMS_ERR_ARG, "max_calls=%d must be >= 0", max_calls);
+    const size_t need = static_cast<size_t>(max_calls) * 3 * ctx->max_chunks;
+    if (need > ctx->t_begin.size()) {
+        DeviceGuard guard(ctx->device);
+        if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+        while (ctx->t_begin.size() < need) {
+            hipEvent_t a, b;
+            hipError_t e = hipEventCreate(&a);
+            if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+            e = hipEventCreate(&b);
+            if (e != hipSuccess) {
+                (void)hipEventDestroy(a);
+                return hip_fail(e, "hipEventCreate");
+            }
+            ctx->t_begin.push_back(a);
+            ctx->t_end.push_back(b);
+        }
+    }
+    ctx->timing_calls = max_calls;
+    ctx->timed_chunks.clear();
+    return ok();
+}
+
+int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap) {
+    if (!ctx || !ms_out) return fail(HCMS_ERR_NULL, "ctx or ms_out is NULL");
+    if (ctx->timing_calls == 0) return fail(HCMS_ERR_ARG, "timing is off");
+    if (kind != HCMS_OP_PACK && kind != HCMS_OP_ATTENTION && kind != HCMS_OP_UNPACK)
+        return fail(HCMS_ERR_ARG, "kind %d is not PACK, ATTENTION or UNPACK", kind);
+    int total = 0;
+    for (int n : ctx->timed_chunks) total += n;
+    if (cap < total) return fail(HCMS_ERR_CAPACITY, "need %d entries, capacity is %d", total, cap);
+    DeviceGuard guard(ctx->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    int w = 0;
+    for (size_t call = 0; call < ctx->timed_chunks.size(); ++call) {
+        for (int c = 0; c < ctx->timed_chunks[call]; ++c) {
+            const size_t slot = (call * 3 + (kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
+            hipError_t e = hipEventSynchronize(ctx->t_end[slot]);
+            if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+            e = hipEventElapsedTime(&ms_out[w++], ctx->t_begin[slot], ctx->t_end[slot]);
+            if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+        }
+    }
+    ok();
+    return total;
+}
+
+int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void *v_seq, void *o_seq,
+                 void *q_hm, void *k_hm, void *v_hm, void *o_hm, int P, int S, int H, int d,
+                 float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
+                 void *main_stream, void *copy_stream, void *compute_stream) {
+    int st;
+    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    if (!q_seq || !k_seq || !v_seq || !o_seq || !q_hm || !k_hm || !v_hm || !o_hm)
+        return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
+    if (mode != HCMS_MODE_SERIAL && mode != HCMS_MODE_PIPELINED)
+        return fail(HCMS_ERR_ARG, "mode %d is neither serial (0) nor pipelined (1)", mode);
+    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
+    if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
+    int log2u = 0;
+    if ((st = row_log2_units(d, dtype, &log2u)) != HCMS_OK) return st;
+    if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
+    if ((st = check_chunks(H, chunk_sizes, n_chunks)) != HCMS_OK) return st;
+    if (n_chunks > ctx->max_chunks)
+        return fail(HCMS_ERR_CHUNKS, "n_chunks=%d exceeds the context's max_chunks=%d", n_chunks,
+                    ctx->max_chunks);
+    if ((st = check_scale(scale)) != HCMS_OK) return st;
+    if (mode == HCMS_MODE_PIPELINED &&
+        (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
+        return fail(HCMS_ERR_ARG, "pipelined mode needs three distinct streams");
+    const void *all[8] = {q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm};
+    for (const void *p : all)
+        if (!aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
+    for (int i = 0; i < 8; ++i)
+        for (int j = i + 1; j < 8; ++j) {
+            // Inputs may alias each other (read-only); everything else must not.
+            const bool both_inputs = i < 3 && j < 3;
+            if (!both_inputs && overlaps(all[i], bytes, all[j], bytes))
+                return fail(HCMS_ERR_ALIAS, "tensor %d overlaps tensor %d", i, j);
+        }
+    int cur_dev = -1;
+    hipError_t e = hipGetDevice(&cur_dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur_dev != ctx->device)
+        return fail(HCMS_ERR_ARG, "context is bound to device %d, current device is %d", ctx->device,
+                    cur_dev);
+    if (S == 0) return ok();
+
+    PlanWriter w{ctx->plan.data(), static_cast<int>(ctx->plan.size())};
+    const int n_ops = build_plan(n_chunks, mode, w);
+
+    hipStream_t streams[3] = {static_cast<hipStream_t>(main_stream),
+                              static_cast<hipStream_t>(copy_stream),
+                              static_cast<hipStream_t>(compute_stream)};
+    const int C = n_chunks;
+    int h0[64 + 1];
+    std::vector<int> h0_big;
+    int *offs = h0;
+    if (C + 1 > 65) {
+        h0_big.resize(C + 1);
+        offs = h0_big.data();
+    }
+    offs[0] = 0;
+    for (int c = 0; c < C; ++c) offs[c + 1] = offs[c] + chunk_sizes[c];
+
+    const int64_t head_bytes = static_cast<int64_t>(S) * d * elem_bytes(dtype);
+    const float c_log2e = scale_log2e(scale);
+    // Sync event id -> ctx event (ids: 0 E_main, 1..C E_pack, C+1..2C E_attn,
+    // 2C+1 E_done; the context keeps max_chunks of each kind).
+    auto event_of = [&](int id) -> hipEvent_t {
+        if (id == 0) return ctx->events[0];
+        if (id <= C) return ctx->events[id];
+        if (id <= 2 * C) return ctx->events[1 + ctx->max_chunks + (id - 1 - C)];
+        return ctx->events[1 + 2 * ctx->max_chunks];
+    };
+
+    const bool timed = static_cast<int>(ctx->timed_chunks.size()) < ctx->timing_calls;
+    const size_t call = ctx->timed_chunks.size();
+    for (int i = 0; i < n_ops; ++i) {
+        const hcms_op &op = ctx->plan[i];
+        hipStream_t s = streams[op.stream];
+        if (op.kind == HCMS_OP_RECORD) {
+            e = hipEventRecord(event_of(op.event), s);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+            continue;
+        }
+        if (op.kind == HCMS_OP_WAIT) {
+            e = hipStreamWaitEvent(s, event_of(op.event), 0);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+            continue;
+        }
+        const int c = op.chunk;
+        const size_t slot = (call * 3 + (op.kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
+        if (timed) {
+            e = hipEventRecord(ctx->t_begin[slot], s);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+        }
+        const int64_t off = head_bytes * offs[c];
+        const int hc = chunk_sizes[c];
+        if (op.kind == HCMS_OP_PACK) {
+            const void *src[3] = {q_seq, k_seq, v_seq};
+            void *dst[3] = {static_cast<char *>(q_hm) + off, static_cast<char *>(k_hm) + off,
+                            static_cast<char *>(v_hm) + off};
+            e = hcms::launch_pack(src, dst, 3, S, H, offs[c], hc, log2u, s);
+        } else if (op.kind == HCMS_OP_ATTENTION) {
+            e = hcms::launch_attention(static_cast<char *>(q_hm) + off, static_cast<char *>(k_hm) + off,
+                                       static_cast<char *>(v_hm) + off, static_cast<char *>(o_hm) + off,
+                                       S, hc, d, c_log2e, dtype, s);
+        } else {
+            e = hcms::launch_unpack(static_cast<char *>(o_hm) + off, o_seq, S, H, offs[c], hc, log2u, s);
+        }
+        if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        if (timed) {
+            e = hipEventRecord(ctx->t_end[slot], s);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+        }
+    }
+    if (timed) ctx->timed_chunks.push_back(C);
+    return ok();
+}
+
+}  // extern "C"

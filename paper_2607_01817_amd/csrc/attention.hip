@@ -1,0 +1,387 @@
+// Flash-style non-causal softmax attention for gfx950 (MI355X), bf16 MFMA.
+//
+// Computes, per head h and query i (Sec. 3.3 Property of computational
+// independence; the attention step of Alg. 1):
+//   O[h][i] = sum_j softmax_j(scale * <Q[h][i], K[h][j]>) V[h][j],  j < S.
+// The S x S score matrix is never stored: keys are visited in blocks of
+// kBC = 64 with a running maximum and running sum per query (online softmax),
+// so memory is O(S d) per head.
+//
+// Work decomposition
+//   * one workgroup = 4 waves = one tile of kBR = 128 queries of one head;
+//     each wave owns 32 queries for the whole key loop; about 200 VGPRs per
+//     wave, so two workgroups share a CU and the SIMDs interleave the MFMA work
+//     of one wave with the softmax of the other;
+//   * K and V blocks are staged in LDS (double-buffered) by all 256 threads;
+//   * scores are computed transposed, S^T = K Q^T, with
+//     v_mfma_f32_32x32x16_bf16: keys are the M dimension and queries the N
+//     dimension.  In the accumulator layout each lane then holds one query
+//     (column) and 16 keys (rows) per 32 x 32 tile, so the row max and row sum
+//     of the softmax are in-lane reductions plus one swap between the two
+//     32-lane halves of the wave;
+//   * the same layout is exactly the B operand that O^T += V^T P^T needs, so P
+//     never leaves registers.  V is stored transposed in LDS ([d][key]) with the
+//     keys of every 16-key group permuted (bits 2 and 3 of the key index
+//     swapped) to match the order in which the accumulator rows arrive;
+//   * lazy rescaling: the running maximum used for the exponentials is only
+//     raised when a block's maximum exceeds it by more than 2^8 in the exp2
+//     domain.  Exponentials are then at most 2^8, which bf16 and fp32 hold
+//     exactly in range; the final O / l is unchanged.  The decision is taken per
+//     query (per lane); a wave only skips the multiply when no lane needs it,
+//     and a lane that does not need it multiplies by exactly 1.  So the
+//     arithmetic of every query depends only on its own row, never on which
+//     other queries share the wave, tile, chunk or launch: any head chunking
+//     gives bit-identical results;
+//   * exp2 is the hardware v_exp_f32 on the argument s * c - m * c (one FMA),
+//     c = scale * log2(e);
+//   * P is rounded to bf16 (nearest-even, v_cvt_pk_bf16_f32) for the PV MFMA;
+//     all accumulation (scores, O, l) is fp32;
+//   * the grid is remapped so that the 8 XCDs each take a contiguous range of
+//     (head, query tile) pairs, so concurrent workgroups of an XCD stream the
+//     same K/V blocks through that XCD's L2.
+//
+// Tails: loads go through buffer resources bounded by the head's tensor, so
+// query and key rows >= S read as zeros; such queries are not stored and such
+// keys get score -inf in the last block only.
+#include "hcms_internal.h"
+
+namespace hcms {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kQW = 32;              // queries per wave
+constexpr int NT = kQW / 32;         // 32-query MFMA tiles per wave
+constexpr int kBR = kQW * kWaves;    // queries per workgroup
+constexpr int kBC = 64;              // keys per block
+constexpr float kRescaleThreshold = 8.0f;  // log2 of the largest tolerated exp
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource over one head's [S][D] tensor: loads past its end return 0,
+// which is how the query and key tails are read without branches.
+__device__ inline __amdgpu_buffer_rsrc_t head_rsrc(const void *base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0,
+                                             static_cast<int>(bytes), 0x00020000);
+}
+
+// 8 consecutive elements at byte offset `off` as bf16 (fp32 storage is rounded
+// to nearest-even), returned as raw 32-bit words.
+template <typename T>
+__device__ inline u32x4 load8(__amdgpu_buffer_rsrc_t r, int off);
+
+template <>
+__device__ inline u32x4 load8<__bf16>(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+template <>
+__device__ inline u32x4 load8<float>(__amdgpu_buffer_rsrc_t r, int off) {
+    const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
+    const f32x8 x = {__builtin_bit_cast(float, a[0]), __builtin_bit_cast(float, a[1]),
+                     __builtin_bit_cast(float, a[2]), __builtin_bit_cast(float, a[3]),
+                     __builtin_bit_cast(float, b[0]), __builtin_bit_cast(float, b[1]),
+                     __builtin_bit_cast(float, b[2]), __builtin_bit_cast(float, b[3])};
+    return __builtin_bit_cast(u32x4, __builtin_convertvector(x, bf16x8));
+}
+
+__device__ inline void store4(__bf16 *p, f32x4 x) {
+    *reinterpret_cast<bf16x4 *>(p) = __builtin_convertvector(x, bf16x4);
+}
+__device__ inline void store4(float *p, f32x4 x) { *reinterpret_cast<f32x4 *>(p) = x; }
+
+// Position of key `k` (0..63) inside a transposed V row: bits 2 and 3 swapped.
+__device__ inline int vt_pos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
+
+// LDS tiles are padded by 16 bytes per row: K is [kBC][D + 8] and V^T is
+// [D][kBC + 8] (bf16 elements).  With rows of 272 (K, D = 128) or 144 bytes the
+// 16-byte operand reads of 16 consecutive rows land on 16 disjoint groups of 4
+// banks, and every LDS address is one per-lane base plus an immediate offset.
+template <int D>
+struct Lds {
+    static constexpr int KS = D + 8;      // K row stride (elements)
+    static constexpr int VS = kBC + 8;    // V^T row stride (elements)
+    static constexpr int KT = kBC * KS;   // K tile size (elements)
+    static constexpr int VT = D * VS;     // V^T tile size (elements)
+    static constexpr int BUF = KT + VT;   // one stage buffer
+};
+
+// Global -> register -> LDS staging of one key block (K rows and V^T).
+template <int D, typename T>
+struct Stage {
+    static constexpr int CH = D / 8;                        // 16-byte bf16 chunks per row
+    static constexpr int ROWB = D * static_cast<int>(sizeof(T));  // bytes per stored row
+    static constexpr int CHB = 8 * static_cast<int>(sizeof(T));   // bytes per stored chunk
+    static constexpr int KPASS = kBC * CH / kThreads;       // K chunks per thread
+    static constexpr int VTASK = (kBC / 2) * CH / kThreads; // V (key pair, chunk) tasks
+    static_assert(KPASS >= 1 && VTASK >= 1, "tile too small for the workgroup");
+
+    u32x4 kreg[KPASS];
+    u32x4 vreg[VTASK][2];
+
+    // K: thread -> (row, chunk), 16 threads cover a 256-byte row.
+    __device__ static int k_row(int p, int tid) { return p * (kThreads / CH) + tid / CH; }
+    __device__ static int k_chunk(int tid) { return tid % CH; }
+    // V: a wave covers 16 key pairs x 4 chunks; key pair kp = 2 keys.
+    __device__ static int v_pair(int task) { return ((task >> 6) & 1) * 16 + (task & 15); }
+    __device__ static int v_chunk(int task) { return (task >> 7) * 4 + ((task >> 4) & 3); }
+
+    __device__ void load(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kb, int tid) {
+        const int key0 = kb * kBC;
+#pragma unroll
+        for (int p = 0; p < KPASS; ++p)
+            kreg[p] = load8<T>(kr, (key0 + k_row(p, tid)) * ROWB + k_chunk(tid) * CHB);
+#pragma unroll
+        for (int i = 0; i < VTASK; ++i) {
+            const int task = tid + i * kThreads;
+            const int off = (key0 + 2 * v_pair(task)) * ROWB + v_chunk(task) * CHB;
+            vreg[i][0] = load8<T>(vr, off);
+            vreg[i][1] = load8<T>(vr, off + ROWB);
+        }
+    }
+
+    __device__ void store(__bf16 *ks, __bf16 *vts, int tid) const {
+#pragma unroll
+        for (int p = 0; p < KPASS; ++p)
+            *reinterpret_cast<u32x4 *>(ks + k_row(p, tid) * Lds<D>::KS + k_chunk(tid) * 8) = kreg[p];
+#pragma unroll
+        for (int i = 0; i < VTASK; ++i) {
+            const int task = tid + i * kThreads;
+            __bf16 *dst = vts + v_chunk(task) * 8 * Lds<D>::VS + vt_pos(2 * v_pair(task));
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                // (V[2kp][e], V[2kp+1][e]) as one 32-bit word of V^T row 8 chunk + e.
+                const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
+                *reinterpret_cast<unsigned *>(dst + e * Lds<D>::VS) =
+                    __builtin_amdgcn_perm(vreg[i][1][e >> 1], vreg[i][0][e >> 1], sel);
+            }
+        }
+    }
+};
+
+// O^T[dt][nt] += V^T[dt] P^T[nt] over the 64 keys of a block (4 k-steps).
+template <int DT>
+__device__ inline void pv_mfma(f32x16 (&oacc)[DT][NT], const bf16x8 (&pb)[NT][4],
+                               const __bf16 *vts, int li, int g) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(vts + (dt * 32 + li) * (kBC + 8) +
+                                                                (ks * 2 + g) * 8);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                oacc[dt][nt] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[nt][ks], oacc[dt][nt], 0, 0, 0);
+        }
+    }
+}
+
+template <int D, typename T>
+__global__ __launch_bounds__(kThreads, 2) void attention_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v, T *__restrict__ o,
+    int S, int n_qtiles, float c) {
+    constexpr int KK = D / 16;  // MFMA k-steps over the head dimension
+    constexpr int DT = D / 32;  // 32-row tiles of O^T
+    __shared__ __attribute__((aligned(16))) __bf16 smem[2][Lds<D>::BUF];
+
+    // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
+    // contiguous range of (head, query tile) pairs.
+    const int nb = gridDim.x, b = blockIdx.x;
+    const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
+    const int logical = xcd * per + min(xcd, rem) + (b >> 3);
+    const int head = logical / n_qtiles;
+    const int qtile = logical - head * n_qtiles;
+
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * sizeof(T);
+    const __amdgpu_buffer_rsrc_t qr = head_rsrc(q + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t vr = head_rsrc(v + hoff, hbytes);
+    T *oh = o + hoff;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 31;   // row / column index inside a 32-wide MFMA tile
+    const int g = lane >> 5;    // which half of the wave
+    const int q0 = qtile * kBR + wave * kQW;
+
+    // Q^T as the B operand: lane (g, n) holds query n, head dims 16 kk + 8 g + [0, 8).
+    // Rows past S read as zeros and are never stored.
+    bf16x8 qreg[NT][KK];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int qi = q0 + nt * 32 + li;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            qreg[nt][kk] = __builtin_bit_cast(
+                bf16x8, load8<T>(qr, (qi * D + kk * 16 + g * 8) * static_cast<int>(sizeof(T))));
+    }
+
+    f32x16 oacc[DT][NT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) oacc[dt][nt] = f32x16{};
+    float m_used[NT], lsum[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        m_used[nt] = -INFINITY;
+        lsum[nt] = 0.f;
+    }
+
+    const int nkb = (S + kBC - 1) / kBC;
+    Stage<D, T> st;
+    st.load(kr, vr, 0, tid);
+    st.store(&smem[0][0], &smem[0][Lds<D>::KT], tid);
+    __syncthreads();
+
+    for (int kb = 0; kb < nkb; ++kb) {
+        const __bf16 *ks = &smem[kb & 1][0];
+        const __bf16 *vts = &smem[kb & 1][Lds<D>::KT];
+        if (kb + 1 < nkb) st.load(kr, vr, kb + 1, tid);
+
+        // ---- S^T = K Q^T for 64 keys x 64 queries ----
+        f32x16 sacc[2][NT];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) sacc[mt][nt] = f32x16{};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                    ks + (mt * 32 + li) * Lds<D>::KS + (kk * 2 + g) * 8);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    sacc[mt][nt] =
+                        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[nt][kk], sacc[mt][nt], 0, 0, 0);
+            }
+        }
+
+        // ---- mask keys beyond S (last block only) ----
+        if (kb == nkb - 1 && (S % kBC) != 0) {
+            const int kvalid = S - kb * kBC;
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+                    if (key >= kvalid) {
+#pragma unroll
+                        for (int nt = 0; nt < NT; ++nt) sacc[mt][nt][r] = -INFINITY;
+                    }
+                }
+        }
+
+        // ---- online softmax with lazy rescaling ----
+        float alpha[NT];
+        bool raise_any = false;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            float mx = sacc[0][nt][0];
+#pragma unroll
+            for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[0][nt][r]);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[1][nt][r]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            // First block: m_used = -inf, so the test is true and alpha = 0.
+            const bool raise = (mx - m_used[nt]) * c > kRescaleThreshold;
+            alpha[nt] = raise ? __builtin_amdgcn_exp2f((m_used[nt] - mx) * c) : 1.0f;
+            m_used[nt] = raise ? mx : m_used[nt];
+            lsum[nt] *= alpha[nt];
+            raise_any |= raise;
+        }
+        // ---- P = exp2(s c - m c), row sums, bf16 B operands ----
+        bf16x8 pb[NT][4];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const float mc = m_used[nt] * c;
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) {
+                f32x16 p;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][nt][r], c, -mc));
+                    lsum[nt] += p[r];
+                }
+                const f32x8 lo = {p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]};
+                const f32x8 hi = {p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]};
+                pb[nt][mt * 2 + 0] = __builtin_convertvector(lo, bf16x8);
+                pb[nt][mt * 2 + 1] = __builtin_convertvector(hi, bf16x8);
+            }
+        }
+
+        // ---- O^T = alpha O^T + V^T P^T (the rescale is rare after block 0) ----
+        if (__any(raise_any)) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) oacc[dt][nt][r] *= alpha[nt];
+        }
+        pv_mfma<DT>(oacc, pb, vts, li, g);
+
+        if (kb + 1 < nkb) st.store(&smem[(kb + 1) & 1][0], &smem[(kb + 1) & 1][Lds<D>::KT], tid);
+        __syncthreads();
+    }
+
+    // ---- O = O^T / l, rounded to the storage type ----
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const float l = lsum[nt] + __shfl_xor(lsum[nt], 32);
+        const float inv = 1.0f / l;
+        const int qi = q0 + nt * 32 + li;
+        if (qi < S) {
+            T *orow = oh + static_cast<int64_t>(qi) * D;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const f32x4 x = {oacc[dt][nt][rb * 4 + 0] * inv, oacc[dt][nt][rb * 4 + 1] * inv,
+                                     oacc[dt][nt][rb * 4 + 2] * inv, oacc[dt][nt][rb * 4 + 3] * inv};
+                    store4(orow + dt * 32 + rb * 8 + g * 4, x);
+                }
+        }
+    }
+}
+
+template <int D, typename T>
+hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, int S, int n_heads,
+                        float c, hipStream_t stream) {
+    const int n_qtiles = (S + kBR - 1) / kBR;
+    const int64_t blocks = static_cast<int64_t>(n_qtiles) * n_heads;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    attention_kernel<D, T><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+        static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
+        static_cast<T *>(o), S, n_qtiles, c);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, int S,
+                            int n_heads, int d, float scale_log2e, int dtype, hipStream_t stream) {
+    if (S == 0 || n_heads == 0) return hipSuccess;
+    if (d == 128 && dtype == 0)
+        return launch_typed<128, __bf16>(q, k, v, o, S, n_heads, scale_log2e, stream);
+    if (d == 64 && dtype == 0)
+        return launch_typed<64, __bf16>(q, k, v, o, S, n_heads, scale_log2e, stream);
+    if (d == 128 && dtype == 1)
+        return launch_typed<128, float>(q, k, v, o, S, n_heads, scale_log2e, stream);
+    if (d == 64 && dtype == 1)
+        return launch_typed<64, float>(q, k, v, o, S, n_heads, scale_log2e, stream);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace hcms

@@ -1,0 +1,28 @@
+// Internal launchers of the HCMS HIP library (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace hcms {
+
+// Copy `n_tensors` (1..3) head chunks at once.  Each tensor z moves
+//   dst[z][j][t][:] = src[z][t][h0 + j][:]   (pack)
+// for t < S, j < hc, where a row ([:]) is 16 << log2_units bytes.
+hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors,
+                       int64_t S, int64_t H, int64_t h0, int64_t hc, int log2_units,
+                       hipStream_t stream);
+
+//   dst[t][h0 + j][:] = src[j][t][:]   (unpack)
+hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64_t h0,
+                         int64_t hc, int log2_units, hipStream_t stream);
+
+// Attention of `n_heads` consecutive heads, head-major [n_heads][S][d]
+// buffers starting at the chunk's first head.  scale_log2e = scale * log2(e).
+// dtype: 0 = bf16 storage, 1 = fp32 storage.  d in {64, 128}.
+hipError_t launch_attention(const void *q, const void *k, const void *v, void *o,
+                            int S, int n_heads, int d, float scale_log2e, int dtype,
+                            hipStream_t stream);
+
+}  // namespace hcms
