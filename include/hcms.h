@@ -25,7 +25,8 @@
  *     crosses this boundary.
  *   - Input and output buffers of one call must not overlap (checked; returns
  *     HCMS_ERR_ALIAS).
- *   - S = 0 (an empty sequence) is valid and enqueues nothing.
+ *   - S = 0 (an empty sequence) is valid and enqueues nothing; the tensor
+ *     pointers may then be NULL.
  *   - Supported: d in {64, 128} for attention; for pack/unpack any d whose row
  *     (d * element size) is a power of two from 16 to 1024 bytes; dtype bf16 or
  *     fp32 storage.

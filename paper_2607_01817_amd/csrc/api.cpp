@@ -102,7 +102,7 @@ int check_scale(float scale) {
 int check_pack_args(const void *a, const void *b, int P, int S, int H, int d, int h_begin,
                     int h_count, int dtype, int *log2_units) {
     int st;
-    if (!a || !b) return fail(HCMS_ERR_NULL, "source or destination is NULL");
+    if (S > 0 && (!a || !b)) return fail(HCMS_ERR_NULL, "source or destination is NULL");
     if ((st = check_dtype(dtype)) != HCMS_OK) return st;
     if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
     if ((st = row_log2_units(d, dtype, log2_units)) != HCMS_OK) return st;
@@ -256,7 +256,7 @@ int hcms_unpack(const void *src_hm, void *dst_seq, int P, int S, int H, int d, i
 static int check_attention_args(const void *q, const void *k, const void *v, const void *out, int S,
                                 int H, int d, float scale, const int *sizes, int n, int dtype) {
     int st;
-    if (!q || !k || !v || !out) return fail(HCMS_ERR_NULL, "q, k, v or out is NULL");
+    if (S > 0 && (!q || !k || !v || !out)) return fail(HCMS_ERR_NULL, "q, k, v or out is NULL");
     if ((st = check_dtype(dtype)) != HCMS_OK) return st;
     if ((st = check_dims(1, S, H, d, dtype)) != HCMS_OK) return st;
     if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
@@ -404,7 +404,7 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
                  void *main_stream, void *copy_stream, void *compute_stream) {
     int st;
     if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
-    if (!q_seq || !k_seq || !v_seq || !o_seq || !q_hm || !k_hm || !v_hm || !o_hm)
+    if (S > 0 && (!q_seq || !k_seq || !v_seq || !o_seq || !q_hm || !k_hm || !v_hm || !o_hm))
         return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
     if (mode != HCMS_MODE_SERIAL && mode != HCMS_MODE_PIPELINED)
         return fail(HCMS_ERR_ARG, "mode %d is neither serial (0) nor pipelined (1)", mode);

@@ -81,14 +81,14 @@ __device__ inline u32x4 load8<__bf16>(__amdgpu_buffer_rsrc_t r, int off) {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
+// The two loads are reinterpreted as whole float vectors before the
+// conversion: converting lane-wise bit casts of u32 vector elements to bf16
+// miscompiles with this toolchain (elements are dropped).
 template <>
 __device__ inline u32x4 load8<float>(__amdgpu_buffer_rsrc_t r, int off) {
-    const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-    const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
-    const f32x8 x = {__builtin_bit_cast(float, a[0]), __builtin_bit_cast(float, a[1]),
-                     __builtin_bit_cast(float, a[2]), __builtin_bit_cast(float, a[3]),
-                     __builtin_bit_cast(float, b[0]), __builtin_bit_cast(float, b[1]),
-                     __builtin_bit_cast(float, b[2]), __builtin_bit_cast(float, b[3])};
+    const f32x4 a = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+    const f32x4 b = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0));
+    const f32x8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(u32x4, __builtin_convertvector(x, bf16x8));
 }
 

@@ -182,9 +182,10 @@ def test_pack_validation(lib, fn):
         got = f(*args, None)
         assert got == want, (fn, args, got, _err(lib))
         assert _err(lib)
-    # An empty sequence is valid and enqueues nothing.
+    # An empty sequence is valid and enqueues nothing (buffers may be NULL).
     assert f(A, B, 4, 0, 4, 64, 0, 2, 1, None) == OK
     assert _err(lib) == ""
+    assert f(None, None, 4, 0, 4, 64, 0, 2, 1, None) == OK
 
 
 def test_attention_validation(lib):
@@ -214,6 +215,7 @@ def test_attention_validation(lib):
     assert call(o=A) == EALIAS
     assert call(o=B + 4096) == EALIAS
     assert call(S=0) == OK  # empty sequence: nothing enqueued
+    assert call(S=0, q=None, k=None, v=None, o=None) == OK
 
 
 def test_forward_and_ctx_validation(lib):
