@@ -8,11 +8,14 @@
 // so memory is O(S d) per head.
 //
 // Work decomposition
-//   * one workgroup = 4 waves = one tile of kBR = 128 queries of one head;
-//     each wave owns 32 queries for the whole key loop; about 200 VGPRs per
-//     wave, so two workgroups share a CU and the SIMDs interleave the MFMA work
-//     of one wave with the softmax of the other;
-//   * K and V blocks are staged in LDS (double-buffered) by all 256 threads;
+//   * one workgroup = WAVES waves (8 for d = 128, 4 for d = 64) = one tile of
+//     32 * WAVES queries of one head; each wave owns 32 queries for the whole
+//     key loop.  Two waves per SIMD.  With 8 waves the register file holds
+//     exactly one workgroup per CU, so a workgroup dispatched while other
+//     kernels occupy part of the GPU can never be queued behind two running
+//     ones on the same CU, and every staged K/V block feeds 256 queries;
+//   * K and V blocks are staged in LDS by all threads (global -> registers ->
+//     LDS), K one block ahead of V, each double-buffered;
 //   * scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: keys are the M dimension and queries the N
 //     dimension.  In the accumulator layout each lane then holds one query
@@ -23,6 +26,9 @@
 //     never leaves registers.  V is stored transposed in LDS ([d][key]) with the
 //     keys of every 16-key group permuted (bits 2 and 3 of the key index
 //     swapped) to match the order in which the accumulator rows arrive;
+//   * software pipeline: while the VALU computes the softmax of block j, the
+//     MFMA unit already computes the scores of block j + 1 (no dependency
+//     between the two), then O^T += V_j^T P_j^T;
 //   * lazy rescaling: the running maximum used for the exponentials is only
 //     raised when a block's maximum exceeds it by more than 2^8 in the exp2
 //     domain.  Exponentials are then at most 2^8, which bf16 and fp32 hold
@@ -35,7 +41,9 @@
 //   * exp2 is the hardware v_exp_f32 on the argument s * c - m * c (one FMA),
 //     c = scale * log2(e);
 //   * P is rounded to bf16 (nearest-even, v_cvt_pk_bf16_f32) for the PV MFMA;
-//     all accumulation (scores, O, l) is fp32;
+//     the row sum l adds exactly these rounded values (v_dot2c_f32_bf16 with a
+//     (1, 1) pair), so the weights that multiply V are normalised exactly; all
+//     accumulation (scores, O, l) is fp32;
 //   * the grid is remapped so that the 8 XCDs each take a contiguous range of
 //     (head, query tile) pairs, so concurrent workgroups of an XCD stream the
 //     same K/V blocks through that XCD's L2.
@@ -50,19 +58,15 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
-constexpr int kQW = 32;              // queries per wave
-constexpr int NT = kQW / 32;         // 32-query MFMA tiles per wave
-constexpr int kBR = kQW * kWaves;    // queries per workgroup
+constexpr int kQW = 32;              // queries per wave (one 32-wide MFMA tile)
 constexpr int kBC = 64;              // keys per block
 constexpr float kRescaleThreshold = 8.0f;  // log2 of the largest tolerated exp
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Buffer resource over one head's [S][D] tensor: loads past its end return 0,
 // which is how the query and key tails are read without branches.
@@ -74,10 +78,10 @@ __device__ inline __amdgpu_buffer_rsrc_t head_rsrc(const void *base, int64_t byt
 // 8 consecutive elements at byte offset `off` as bf16 (fp32 storage is rounded
 // to nearest-even), returned as raw 32-bit words.
 template <typename T>
-__device__ inline u32x4 load8(__amdgpu_buffer_rsrc_t r, int off);
+__device__ inline u32x4 load8(__amdgpu_buffer_rsrc_t r, unsigned off);
 
 template <>
-__device__ inline u32x4 load8<__bf16>(__amdgpu_buffer_rsrc_t r, int off) {
+__device__ inline u32x4 load8<__bf16>(__amdgpu_buffer_rsrc_t r, unsigned off) {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
@@ -85,7 +89,7 @@ __device__ inline u32x4 load8<__bf16>(__amdgpu_buffer_rsrc_t r, int off) {
 // conversion: converting lane-wise bit casts of u32 vector elements to bf16
 // miscompiles with this toolchain (elements are dropped).
 template <>
-__device__ inline u32x4 load8<float>(__amdgpu_buffer_rsrc_t r, int off) {
+__device__ inline u32x4 load8<float>(__amdgpu_buffer_rsrc_t r, unsigned off) {
     const f32x4 a = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
     const f32x4 b = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0));
     const f32x8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
@@ -110,15 +114,15 @@ struct Lds {
     static constexpr int VS = kBC + 8;    // V^T row stride (elements)
     static constexpr int KT = kBC * KS;   // K tile size (elements)
     static constexpr int VT = D * VS;     // V^T tile size (elements)
-    static constexpr int BUF = KT + VT;   // one stage buffer
 };
 
-// Global -> register -> LDS staging of one key block (K rows and V^T).
-template <int D, typename T>
+// Global -> register -> LDS staging of one K block and one V block.
+template <int D, typename T, int WAVES>
 struct Stage {
+    static constexpr int kThreads = 64 * WAVES;
     static constexpr int CH = D / 8;                        // 16-byte bf16 chunks per row
-    static constexpr int ROWB = D * static_cast<int>(sizeof(T));  // bytes per stored row
-    static constexpr int CHB = 8 * static_cast<int>(sizeof(T));   // bytes per stored chunk
+    static constexpr unsigned ROWB = D * sizeof(T);          // bytes per stored row
+    static constexpr unsigned CHB = 8 * sizeof(T);           // bytes per stored chunk
     static constexpr int KPASS = kBC * CH / kThreads;       // K chunks per thread
     static constexpr int VTASK = (kBC / 2) * CH / kThreads; // V (key pair, chunk) tasks
     static_assert(KPASS >= 1 && VTASK >= 1, "tile too small for the workgroup");
@@ -126,31 +130,38 @@ struct Stage {
     u32x4 kreg[KPASS];
     u32x4 vreg[VTASK][2];
 
-    // K: thread -> (row, chunk), 16 threads cover a 256-byte row.
+    // K: thread -> (row, chunk), CH threads cover a row.
     __device__ static int k_row(int p, int tid) { return p * (kThreads / CH) + tid / CH; }
     __device__ static int k_chunk(int tid) { return tid % CH; }
-    // V: a wave covers 16 key pairs x 4 chunks; key pair kp = 2 keys.
+    // V: a wave covers 16 key pairs x 4 chunks; key pair kp = keys 2kp, 2kp + 1.
     __device__ static int v_pair(int task) { return ((task >> 6) & 1) * 16 + (task & 15); }
     __device__ static int v_chunk(int task) { return (task >> 7) * 4 + ((task >> 4) & 3); }
 
-    __device__ void load(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kb, int tid) {
-        const int key0 = kb * kBC;
+    // Offsets stay below 2^32: a head is at most 2^31 - 1 bytes and blocks past
+    // its end are at most three blocks away.
+    __device__ void load(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kblk, int vblk,
+                         int tid) {
+        const unsigned key0 = static_cast<unsigned>(kblk) * kBC;
 #pragma unroll
         for (int p = 0; p < KPASS; ++p)
             kreg[p] = load8<T>(kr, (key0 + k_row(p, tid)) * ROWB + k_chunk(tid) * CHB);
+        const unsigned vkey0 = static_cast<unsigned>(vblk) * kBC;
 #pragma unroll
         for (int i = 0; i < VTASK; ++i) {
             const int task = tid + i * kThreads;
-            const int off = (key0 + 2 * v_pair(task)) * ROWB + v_chunk(task) * CHB;
+            const unsigned off = (vkey0 + 2 * v_pair(task)) * ROWB + v_chunk(task) * CHB;
             vreg[i][0] = load8<T>(vr, off);
             vreg[i][1] = load8<T>(vr, off + ROWB);
         }
     }
 
-    __device__ void store(__bf16 *ks, __bf16 *vts, int tid) const {
+    __device__ void store_k(__bf16 *ks, int tid) const {
 #pragma unroll
         for (int p = 0; p < KPASS; ++p)
             *reinterpret_cast<u32x4 *>(ks + k_row(p, tid) * Lds<D>::KS + k_chunk(tid) * 8) = kreg[p];
+    }
+
+    __device__ void store_v(__bf16 *vts, int tid) const {
 #pragma unroll
         for (int i = 0; i < VTASK; ++i) {
             const int task = tid + i * kThreads;
@@ -166,31 +177,95 @@ struct Stage {
     }
 };
 
-// O^T[dt][nt] += V^T[dt] P^T[nt] over the 64 keys of a block (4 k-steps).
-template <int DT>
-__device__ inline void pv_mfma(f32x16 (&oacc)[DT][NT], const bf16x8 (&pb)[NT][4],
-                               const __bf16 *vts, int li, int g) {
+// S^T[mt] = K[mt] Q^T for the 64 keys of a block (2 tiles of 32 keys).
+template <int D>
+__device__ inline void qk_mfma(f32x16 (&sacc)[2], const __bf16 *ks, const bf16x8 (&qreg)[D / 16],
+                               int li, int g) {
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
+    for (int mt = 0; mt < 2; ++mt) sacc[mt] = f32x16{};
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(vts + (dt * 32 + li) * (kBC + 8) +
-                                                                (ks * 2 + g) * 8);
+    for (int kk = 0; kk < D / 16; ++kk) {
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                oacc[dt][nt] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[nt][ks], oacc[dt][nt], 0, 0, 0);
+        for (int mt = 0; mt < 2; ++mt) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ks + (mt * 32 + li) * Lds<D>::KS +
+                                                                (kk * 2 + g) * 8);
+            sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[mt], 0, 0, 0);
         }
     }
 }
 
-template <int D, typename T>
-__global__ __launch_bounds__(kThreads, 2) void attention_kernel(
+// O^T[dt] += V^T[dt] P^T over the 64 keys of a block (4 k-steps of 16 keys).
+template <int D>
+__device__ inline void pv_mfma(f32x16 (&oacc)[D / 32], const bf16x8 (&pb)[4], const __bf16 *vts,
+                               int li, int g) {
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(vts + (dt * 32 + li) * Lds<D>::VS +
+                                                                (ks * 2 + g) * 8);
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[dt], 0, 0, 0);
+        }
+    }
+}
+
+// Online softmax of one block for this lane's query: updates the running
+// maximum m_used (lazily) and the row sum, returns the rescale factor of O and
+// the bf16 B operands P^T.  With MASK, keys at or past `kvalid` inside the
+// block get score -inf.
+template <bool MASK>
+__device__ inline float softmax_block(f32x16 (&sacc)[2], float &m_used, float &lsum,
+                                      bf16x8 (&pb)[4], float c, int g, int kvalid, bool &raise) {
+    if (MASK) {
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+                if (key >= kvalid) sacc[mt][r] = -INFINITY;
+            }
+    }
+    float mx = sacc[0][0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[1][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    // First block: m_used = -inf, so the test is true and alpha = 0.
+    raise = (mx - m_used) * c > kRescaleThreshold;
+    const float alpha = raise ? __builtin_amdgcn_exp2f((m_used - mx) * c) : 1.0f;
+    m_used = raise ? mx : m_used;
+    lsum *= alpha;
+    const float mc = m_used * c;
+    const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            f32x8 p;
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+                p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][h * 8 + r], c, -mc));
+            const bf16x8 pbf = __builtin_convertvector(p, bf16x8);
+            pb[mt * 2 + h] = pbf;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bf16x2 pair = {pbf[2 * r], pbf[2 * r + 1]};
+                lsum = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, lsum, false);
+            }
+        }
+    }
+    return alpha;
+}
+
+template <int D, typename T, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v, T *__restrict__ o,
     int S, int n_qtiles, float c) {
     constexpr int KK = D / 16;  // MFMA k-steps over the head dimension
     constexpr int DT = D / 32;  // 32-row tiles of O^T
-    __shared__ __attribute__((aligned(16))) __bf16 smem[2][Lds<D>::BUF];
+    __shared__ __attribute__((aligned(16))) __bf16 kbuf[2][Lds<D>::KT];
+    __shared__ __attribute__((aligned(16))) __bf16 vbuf[2][Lds<D>::VT];
 
     // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
     // contiguous range of (head, query tile) pairs.
@@ -212,157 +287,100 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(
     const int wave = tid >> 6;
     const int li = lane & 31;   // row / column index inside a 32-wide MFMA tile
     const int g = lane >> 5;    // which half of the wave
-    const int q0 = qtile * kBR + wave * kQW;
+    const int q0 = qtile * (kQW * WAVES) + wave * kQW;
+    const int qi = q0 + li;     // this lane's query
 
     // Q^T as the B operand: lane (g, n) holds query n, head dims 16 kk + 8 g + [0, 8).
     // Rows past S read as zeros and are never stored.
-    bf16x8 qreg[NT][KK];
+    bf16x8 qreg[KK];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        const int qi = q0 + nt * 32 + li;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-            qreg[nt][kk] = __builtin_bit_cast(
-                bf16x8, load8<T>(qr, (qi * D + kk * 16 + g * 8) * static_cast<int>(sizeof(T))));
-    }
+    for (int kk = 0; kk < KK; ++kk)
+        qreg[kk] = __builtin_bit_cast(
+            bf16x8, load8<T>(qr, static_cast<unsigned>(qi * D + kk * 16 + g * 8) * sizeof(T)));
 
-    f32x16 oacc[DT][NT];
+    f32x16 oacc[DT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) oacc[dt][nt] = f32x16{};
-    float m_used[NT], lsum[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        m_used[nt] = -INFINITY;
-        lsum[nt] = 0.f;
-    }
-
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+    float m_used = -INFINITY, lsum = 0.f;
     const int nkb = (S + kBC - 1) / kBC;
-    Stage<D, T> st;
-    st.load(kr, vr, 0, tid);
-    st.store(&smem[0][0], &smem[0][Lds<D>::KT], tid);
+
+    // Prologue: K_0, V_0 and K_1 in LDS, scores of block 0.
+    Stage<D, T, WAVES> st;
+    st.load(kr, vr, 0, 0, tid);
+    st.store_k(kbuf[0], tid);
+    st.store_v(vbuf[0], tid);
+    st.load(kr, vr, 1, 1, tid);
+    st.store_k(kbuf[1], tid);
     __syncthreads();
+    f32x16 scur[2];
+    qk_mfma<D>(scur, kbuf[0], qreg, li, g);
+    __syncthreads();  // kbuf[0] is overwritten in the first iteration
 
-    for (int kb = 0; kb < nkb; ++kb) {
-        const __bf16 *ks = &smem[kb & 1][0];
-        const __bf16 *vts = &smem[kb & 1][Lds<D>::KT];
-        if (kb + 1 < nkb) st.load(kr, vr, kb + 1, tid);
-
-        // ---- S^T = K Q^T for 64 keys x 64 queries ----
-        f32x16 sacc[2][NT];
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) sacc[mt][nt] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
-                    ks + (mt * 32 + li) * Lds<D>::KS + (kk * 2 + g) * 8);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-                    sacc[mt][nt] =
-                        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[nt][kk], sacc[mt][nt], 0, 0, 0);
-            }
-        }
-
-        // ---- mask keys beyond S (last block only) ----
-        if (kb == nkb - 1 && (S % kBC) != 0) {
-            const int kvalid = S - kb * kBC;
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-                    if (key >= kvalid) {
-#pragma unroll
-                        for (int nt = 0; nt < NT; ++nt) sacc[mt][nt][r] = -INFINITY;
-                    }
-                }
-        }
-
-        // ---- online softmax with lazy rescaling ----
-        float alpha[NT];
-        bool raise_any = false;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            float mx = sacc[0][nt][0];
-#pragma unroll
-            for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[0][nt][r]);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[1][nt][r]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            // First block: m_used = -inf, so the test is true and alpha = 0.
-            const bool raise = (mx - m_used[nt]) * c > kRescaleThreshold;
-            alpha[nt] = raise ? __builtin_amdgcn_exp2f((m_used[nt] - mx) * c) : 1.0f;
-            m_used[nt] = raise ? mx : m_used[nt];
-            lsum[nt] *= alpha[nt];
-            raise_any |= raise;
-        }
-        // ---- P = exp2(s c - m c), row sums, bf16 B operands ----
-        bf16x8 pb[NT][4];
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            const float mc = m_used[nt] * c;
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt) {
-                f32x16 p;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][nt][r], c, -mc));
-                    lsum[nt] += p[r];
-                }
-                const f32x8 lo = {p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]};
-                const f32x8 hi = {p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]};
-                pb[nt][mt * 2 + 0] = __builtin_convertvector(lo, bf16x8);
-                pb[nt][mt * 2 + 1] = __builtin_convertvector(hi, bf16x8);
-            }
-        }
-
-        // ---- O^T = alpha O^T + V^T P^T (the rescale is rare after block 0) ----
-        if (__any(raise_any)) {
+    // Steady state: block j's softmax and PV overlap block j + 1's scores.
+    // LDS holds K_{j+1} in kbuf[(j+1)&1] and V_j in vbuf[j&1]; K_{j+2} and
+    // V_{j+1} travel through registers and land in the buffers freed by K_j
+    // and V_{j-1}.
+    for (int j = 0; j + 1 < nkb; ++j) {
+        st.load(kr, vr, j + 2, j + 1, tid);
+        f32x16 snext[2];
+        qk_mfma<D>(snext, kbuf[(j + 1) & 1], qreg, li, g);
+        bf16x8 pb[4];
+        bool raise;
+        const float alpha = softmax_block<false>(scur, m_used, lsum, pb, c, g, kBC, raise);
+        if (__any(raise)) {
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) oacc[dt][nt][r] *= alpha[nt];
+                for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
         }
-        pv_mfma<DT>(oacc, pb, vts, li, g);
-
-        if (kb + 1 < nkb) st.store(&smem[(kb + 1) & 1][0], &smem[(kb + 1) & 1][Lds<D>::KT], tid);
+        pv_mfma<D>(oacc, pb, vbuf[j & 1], li, g);
+        st.store_k(kbuf[j & 1], tid);
+        st.store_v(vbuf[(j + 1) & 1], tid);
         __syncthreads();
+        scur[0] = snext[0];
+        scur[1] = snext[1];
+    }
+
+    // Last block: mask the keys past S.
+    {
+        const int j = nkb - 1;
+        bf16x8 pb[4];
+        bool raise;
+        const float alpha = softmax_block<true>(scur, m_used, lsum, pb, c, g, S - j * kBC, raise);
+        if (__any(raise)) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+        }
+        pv_mfma<D>(oacc, pb, vbuf[j & 1], li, g);
     }
 
     // ---- O = O^T / l, rounded to the storage type ----
+    const float l = lsum + __shfl_xor(lsum, 32);
+    const float inv = 1.0f / l;
+    if (qi < S) {
+        T *orow = oh + static_cast<int64_t>(qi) * D;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        const float l = lsum[nt] + __shfl_xor(lsum[nt], 32);
-        const float inv = 1.0f / l;
-        const int qi = q0 + nt * 32 + li;
-        if (qi < S) {
-            T *orow = oh + static_cast<int64_t>(qi) * D;
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    const f32x4 x = {oacc[dt][nt][rb * 4 + 0] * inv, oacc[dt][nt][rb * 4 + 1] * inv,
-                                     oacc[dt][nt][rb * 4 + 2] * inv, oacc[dt][nt][rb * 4 + 3] * inv};
-                    store4(orow + dt * 32 + rb * 8 + g * 4, x);
-                }
-        }
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 x = {oacc[dt][rb * 4 + 0] * inv, oacc[dt][rb * 4 + 1] * inv,
+                                 oacc[dt][rb * 4 + 2] * inv, oacc[dt][rb * 4 + 3] * inv};
+                store4(orow + dt * 32 + rb * 8 + g * 4, x);
+            }
     }
 }
 
 template <int D, typename T>
 hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, int S, int n_heads,
                         float c, hipStream_t stream) {
-    const int n_qtiles = (S + kBR - 1) / kBR;
+    constexpr int WAVES = D == 128 ? 8 : 4;
+    constexpr int BR = kQW * WAVES;
+    const int n_qtiles = (S + BR - 1) / BR;
     const int64_t blocks = static_cast<int64_t>(n_qtiles) * n_heads;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    attention_kernel<D, T><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+    attention_kernel<D, T, WAVES><<<static_cast<unsigned>(blocks), 64 * WAVES, 0, stream>>>(
         static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
         static_cast<T *>(o), S, n_qtiles, c);
     return hipGetLastError();
