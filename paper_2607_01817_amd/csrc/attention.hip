@@ -21,14 +21,16 @@
 //     dimension.  In the accumulator layout each lane then holds one query
 //     (column) and 16 keys (rows) per 32 x 32 tile, so the row max and row sum
 //     of the softmax are in-lane reductions plus one swap between the two
-//     32-lane halves of the wave;
+//     32-lane halves of the wave (v_permlane32_swap, registers only);
 //   * the same layout is exactly the B operand that O^T += V^T P^T needs, so P
 //     never leaves registers.  V is stored transposed in LDS ([d][key]) with the
 //     keys of every 16-key group permuted (bits 2 and 3 of the key index
 //     swapped) to match the order in which the accumulator rows arrive;
 //   * software pipeline: while the VALU computes the softmax of block j, the
 //     MFMA unit already computes the scores of block j + 1 (no dependency
-//     between the two), then O^T += V_j^T P_j^T;
+//     between the two), then O^T += V_j^T P_j^T.  The K operands of the score
+//     MFMAs are read from LDS four MFMAs ahead; the loop is unrolled by two so
+//     the score registers alternate roles instead of being copied;
 //   * lazy rescaling: the running maximum used for the exponentials is only
 //     raised when a block's maximum exceeds it by more than 2^8 in the exp2
 //     domain.  Exponentials are then at most 2^8, which bf16 and fp32 hold
@@ -177,20 +179,26 @@ struct Stage {
     }
 };
 
-// S^T[mt] = K[mt] Q^T for the 64 keys of a block (2 tiles of 32 keys).
+// S^T[mt] = K[mt] Q^T for the 64 keys of a block (2 tiles of 32 keys); the
+// K operands are read from LDS four MFMAs ahead of their use.
 template <int D>
 __device__ inline void qk_mfma(f32x16 (&sacc)[2], const __bf16 *ks, const bf16x8 (&qreg)[D / 16],
                                int li, int g) {
+    constexpr int N = 2 * (D / 16);
+    constexpr int AHEAD = 4;
+    bf16x8 a[N];
+#pragma unroll
+    for (int i = 0; i < AHEAD; ++i)
+        a[i] = *reinterpret_cast<const bf16x8 *>(ks + ((i & 1) * 32 + li) * Lds<D>::KS + ((i >> 1) * 2 + g) * 8);
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) sacc[mt] = f32x16{};
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ks + (mt * 32 + li) * Lds<D>::KS +
-                                                                (kk * 2 + g) * 8);
-            sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[mt], 0, 0, 0);
+    for (int i = 0; i < N; ++i) {
+        if (i + AHEAD < N) {
+            const int n = i + AHEAD;
+            a[n] = *reinterpret_cast<const bf16x8 *>(ks + ((n & 1) * 32 + li) * Lds<D>::KS + ((n >> 1) * 2 + g) * 8);
         }
+        sacc[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], qreg[i >> 1], sacc[i & 1], 0, 0, 0);
     }
 }
 
@@ -230,7 +238,12 @@ __device__ inline float softmax_block(f32x16 (&sacc)[2], float &m_used, float &l
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[0][r]);
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[1][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    {
+        const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
+                                                        __builtin_bit_cast(unsigned, mx), false, false);
+        mx = fmaxf(__builtin_bit_cast(float, static_cast<unsigned>(r[0])),
+                   __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
+    }
     // First block: m_used = -inf, so the test is true and alpha = 0.
     raise = (mx - m_used) * c > kRescaleThreshold;
     const float alpha = raise ? __builtin_amdgcn_exp2f((m_used - mx) * c) : 1.0f;
@@ -320,9 +333,8 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
     // LDS holds K_{j+1} in kbuf[(j+1)&1] and V_j in vbuf[j&1]; K_{j+2} and
     // V_{j+1} travel through registers and land in the buffers freed by K_j
     // and V_{j-1}.
-    for (int j = 0; j + 1 < nkb; ++j) {
+    auto step = [&](int j, f32x16(&scur)[2], f32x16(&snext)[2]) {
         st.load(kr, vr, j + 2, j + 1, tid);
-        f32x16 snext[2];
         qk_mfma<D>(snext, kbuf[(j + 1) & 1], qreg, li, g);
         bf16x8 pb[4];
         bool raise;
@@ -337,8 +349,17 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
         st.store_k(kbuf[j & 1], tid);
         st.store_v(vbuf[(j + 1) & 1], tid);
         __syncthreads();
-        scur[0] = snext[0];
-        scur[1] = snext[1];
+    };
+    f32x16 salt[2];
+    int j0 = 0;
+    for (; j0 + 2 < nkb; j0 += 2) {
+        step(j0, scur, salt);
+        step(j0 + 1, salt, scur);
+    }
+    if (j0 + 1 < nkb) {
+        step(j0, scur, salt);
+        scur[0] = salt[0];
+        scur[1] = salt[1];
     }
 
     // Last block: mask the keys past S.
@@ -357,7 +378,13 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
     }
 
     // ---- O = O^T / l, rounded to the storage type ----
-    const float l = lsum + __shfl_xor(lsum, 32);
+    float l;
+    {
+        const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, lsum),
+                                                        __builtin_bit_cast(unsigned, lsum), false, false);
+        l = __builtin_bit_cast(float, static_cast<unsigned>(r[0])) +
+            __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
+    }
     const float inv = 1.0f / l;
     if (qi < S) {
         T *orow = oh + static_cast<int64_t>(qi) * D;
