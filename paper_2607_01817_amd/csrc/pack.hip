@@ -12,19 +12,22 @@
 // complete, aligned 128-byte cache lines.  Consecutive lanes move consecutive
 // 16-byte units of the dense side; the strided side is still read or written in
 // full rows.  No LDS stage is needed for coalescing.  Each thread issues all of
-// its loads before any store to keep several 16-byte requests in flight.
+// its loads before any store to keep several 16-byte requests in flight.  The
+// source is read once, so its loads carry the non-temporal hint.
 #include "hcms_internal.h"
 
 namespace hcms {
 namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 constexpr int kUnitsPerBlock = kThreads * kUnroll;
 
 struct PackPtrs {
-    const uint4 *src[3];
-    uint4 *dst[3];
+    const u32x4 *src[3];
+    u32x4 *dst[3];
 };
 
 // grid: x = ceil(S * units_per_row / kUnitsPerBlock), y = hc, z = tensor.
@@ -32,18 +35,18 @@ template <int LOG2U>
 __global__ __launch_bounds__(kThreads) void pack_kernel(PackPtrs p, int64_t S, int64_t H,
                                                         int64_t h0) {
     const int64_t j = blockIdx.y;
-    const uint4 *__restrict__ src = p.src[blockIdx.z];
-    uint4 *__restrict__ dst = p.dst[blockIdx.z] + ((j * S) << LOG2U);
+    const u32x4 *__restrict__ src = p.src[blockIdx.z];
+    u32x4 *__restrict__ dst = p.dst[blockIdx.z] + ((j * S) << LOG2U);
     const int64_t n = S << LOG2U;
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kUnitsPerBlock + threadIdx.x;
-    uint4 buf[kUnroll];
+    u32x4 buf[kUnroll];
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i) {
         const int64_t u = base + i * kThreads;
         if (u < n) {
             const int64_t t = u >> LOG2U;
             const int64_t w = u & ((1 << LOG2U) - 1);
-            buf[i] = src[((t * H + h0 + j) << LOG2U) + w];
+            buf[i] = __builtin_nontemporal_load(src + ((t * H + h0 + j) << LOG2U) + w);
         }
     }
 #pragma unroll
@@ -55,18 +58,18 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(PackPtrs p, int64_t S, i
 
 // grid: x = ceil(S * units_per_row / kUnitsPerBlock), y = hc.
 template <int LOG2U>
-__global__ __launch_bounds__(kThreads) void unpack_kernel(const uint4 *__restrict__ src_all,
-                                                          uint4 *__restrict__ dst, int64_t S,
+__global__ __launch_bounds__(kThreads) void unpack_kernel(const u32x4 *__restrict__ src_all,
+                                                          u32x4 *__restrict__ dst, int64_t S,
                                                           int64_t H, int64_t h0) {
     const int64_t j = blockIdx.y;
-    const uint4 *__restrict__ src = src_all + ((j * S) << LOG2U);
+    const u32x4 *__restrict__ src = src_all + ((j * S) << LOG2U);
     const int64_t n = S << LOG2U;
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kUnitsPerBlock + threadIdx.x;
-    uint4 buf[kUnroll];
+    u32x4 buf[kUnroll];
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i) {
         const int64_t u = base + i * kThreads;
-        if (u < n) buf[i] = src[u];
+        if (u < n) buf[i] = __builtin_nontemporal_load(src + u);
     }
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i) {
@@ -92,7 +95,7 @@ void pack_dispatch(const PackPtrs &p, int n_tensors, int64_t S, int64_t H, int64
 }
 
 template <int LOG2U>
-void unpack_dispatch(const uint4 *src, uint4 *dst, int64_t S, int64_t H, int64_t h0,
+void unpack_dispatch(const u32x4 *src, u32x4 *dst, int64_t S, int64_t H, int64_t h0,
                      int64_t hc, hipStream_t stream) {
     unpack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, 1), kThreads, 0, stream>>>(src, dst, S, H, h0);
 }
@@ -104,8 +107,8 @@ hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, 
     if (S == 0 || hc == 0) return hipSuccess;
     PackPtrs p{};
     for (int z = 0; z < n_tensors; ++z) {
-        p.src[z] = static_cast<const uint4 *>(src[z]);
-        p.dst[z] = static_cast<uint4 *>(dst[z]);
+        p.src[z] = static_cast<const u32x4 *>(src[z]);
+        p.dst[z] = static_cast<u32x4 *>(dst[z]);
     }
     switch (log2_units) {
         case 0: pack_dispatch<0>(p, n_tensors, S, H, h0, hc, stream); break;
@@ -123,8 +126,8 @@ hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, 
 hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64_t h0,
                          int64_t hc, int log2_units, hipStream_t stream) {
     if (S == 0 || hc == 0) return hipSuccess;
-    const uint4 *s = static_cast<const uint4 *>(src);
-    uint4 *d = static_cast<uint4 *>(dst);
+    const u32x4 *s = static_cast<const u32x4 *>(src);
+    u32x4 *d = static_cast<u32x4 *>(dst);
     switch (log2_units) {
         case 0: unpack_dispatch<0>(s, d, S, H, h0, hc, stream); break;
         case 1: unpack_dispatch<1>(s, d, S, H, h0, hc, stream); break;
