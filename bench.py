@@ -3,15 +3,16 @@
 
 A step is one pass of the whole hot path over one batch of synthetic input:
 pack Q/K/V of every head chunk, attention of every chunk, unpack of every
-chunk, scheduled on the copy and compute streams (``hcms_forward``, pipelined
-mode).  The workload is the Wan2.2-14B-shaped rank share at P = 8: S = 56160
+chunk, scheduled across streams by ``hcms_forward`` (auto mode: the one-GPU
+schedule the round rule picks).  The workload is the Wan2.2-14B-shaped rank share at P = 8: S = 56160
 tokens (36 latent frames x 1560), H = 5 local heads, d = 128, bf16, chunks
 2 + 2 + 1 (the paper's uneven rule for C = 3).
 
 Printed: one JSON line with the metric (attention TFLOP/s, 4 S^2 H d per step
-over the pipelined step time), the roofline of the dominant kernel (attention,
-bf16 MFMA), the layout kernels' HBM rates, serial versus pipelined times, and
-the oracle timed on the host cores on a bounded sample of the same workload.
+over the step time), the roofline of the dominant kernel (attention, bf16
+MFMA), the layout kernels' HBM rates, the serial, Alg. 1, inline and lanes
+schedules side by side, and the oracle timed on the host cores on a bounded
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -102,7 +103,8 @@ def copy_calibration(dev):
 def cpu_baseline(w, q, k, v, seconds: float):
     """Time the oracle on sampled query rows of the same workload."""
     import oracle
-    rows_all = inputs.sample_rows(w, 4096, seed=w.seed + 77)
+    per_head = min(w.S, 16384)
+    rows_all = inputs.sample_rows(w, per_head, seed=w.seed + 77)
     heads = [(x[:, h, :].to(torch.float64).numpy() for x in (q, k, v)) for h in range(w.H)]
     heads = [tuple(t) for t in heads]
     done_rows = 0
@@ -110,7 +112,7 @@ def cpu_baseline(w, q, k, v, seconds: float):
     batch = 128
     h = 0
     pos = [0] * w.H
-    while t_cpu < seconds and done_rows < w.H * 4096:
+    while t_cpu < seconds and done_rows < w.H * per_head:
         qh, kh, vh = heads[h]
         rows = rows_all[h][pos[h]:pos[h] + batch]
         pos[h] += batch
@@ -131,13 +133,53 @@ def cpu_baseline(w, q, k, v, seconds: float):
     }
 
 
+MODES = {"serial": hcms.MODE_SERIAL, "pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE,
+         "lanes": hcms.MODE_LANES, "auto": hcms.MODE_AUTO}
+MODE_NAMES = {v: k for k, v in MODES.items()}
+
+
+def quartiles(xs):
+    q = np.percentile(xs, [25, 50, 75])
+    return {"median": round(float(q[1]), 4), "iqr": [round(float(q[0]), 4), round(float(q[2]), 4)]}
+
+
+def compare_modes(ctx, w, chunks, reps: int, dev):
+    """Serial, Alg. 1, inline and lanes schedules of one workload, interleaved
+    (order reversed every other rep to cancel clock drift), step time from
+    events on the main stream."""
+    q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
+    out = torch.empty_like(q)
+    ws = ctx.workspaces(w.S, w.H, w.d, q.dtype)
+    modes = ["serial", "pipelined", "inline", "lanes"]
+    times = {m: [] for m in modes}
+    for r in range(reps + 1):
+        for m in (modes if r % 2 == 0 else modes[::-1]):
+            t = time_region(lambda: ctx.forward(q, k, v, w.P, w.scale, chunks, mode=MODES[m],
+                                                out=out, workspaces=ws), 1)
+            if r > 0:
+                times[m] += t
+    ctx.forward(q, k, v, w.P, w.scale, chunks, mode=hcms.MODE_AUTO, out=out, workspaces=ws)
+    res = {"workload": w.name, "chunks": list(chunks), "auto_runs": MODE_NAMES[ctx.last_mode]}
+    ser = quartiles(times["serial"])
+    res["serial_ms"] = ser
+    for m in modes[1:]:
+        qm = quartiles(times[m])
+        qm["gain_vs_serial_ms"] = round(ser["median"] - qm["median"], 4)
+        qm["below_serial"] = bool(qm["iqr"][1] < ser["iqr"][0])
+        res[m + "_ms"] = qm
+    del q, k, v, out
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=150,
+                    help="untimed steps; about a second of them lets the clock settle")
     ap.add_argument("--workload", default="wan_p8", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--chunks", default="2,2,1")
+    ap.add_argument("--mode", default="auto", choices=sorted(MODES))
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--no-extras", action="store_true",
@@ -158,26 +200,28 @@ def main():
     w = inputs.WORKLOADS[args.workload]
     sizes = parse_chunks(args.chunks)
     assert sum(sizes) == w.H, f"chunks {sizes} do not sum to H={w.H}"
+    mode = MODES[args.mode]
     hcms.load()
     dev = torch.device("cuda:0")
     if args.copy_calibration:
         copy_calibration(dev)
-    log(f"workload {w.name}: S={w.S} H={w.H} d={w.d} {w.dtype} P={w.P} chunks={sizes}")
+    log(f"workload {w.name}: S={w.S} H={w.H} d={w.d} {w.dtype} P={w.P} chunks={sizes} "
+        f"mode={args.mode}")
     q, k, v = inputs.make_qkv(w)
     qd, kd, vd = (x.to(dev) for x in (q, k, v))
     ctx = hcms.Context(max_chunks=max(16, len(sizes)))
     out = torch.empty_like(qd)
     ws = ctx.workspaces(w.S, w.H, w.d, qd.dtype)
 
-    def step(mode=hcms.MODE_PIPELINED, chunks=sizes):
-        ctx.forward(qd, kd, vd, w.P, w.scale, chunks, mode=mode, out=out, workspaces=ws)
+    def step(m=mode, chunks=sizes):
+        ctx.forward(qd, kd, vd, w.P, w.scale, chunks, mode=m, out=out, workspaces=ws)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    plan = MODE_NAMES[ctx.last_mode]
 
-    # ---- timed region: K pipelined steps, kernels bracketed by events ----
-    ctx.set_timing(args.steps)
+    # ---- timed region: K steps, nothing but the steps between the events ----
     main_stream = torch.cuda.current_stream()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
@@ -188,13 +232,22 @@ def main():
     t1.record(main_stream)
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
+
+    # ---- the same K steps again with every kernel bracketed by events on
+    # the stream that runs it: per-launch durations for the roofline ----
+    ctx.set_timing(args.steps)
+    t0.record(main_stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(main_stream)
+    torch.cuda.synchronize()
+    ms_per_step_events = t0.elapsed_time(t1) / args.steps
     attn_ms = ctx.kernel_ms(hcms.OP_ATTENTION)
     pack_ms = ctx.kernel_ms(hcms.OP_PACK)
     unpack_ms = ctx.kernel_ms(hcms.OP_UNPACK)
     ctx.set_timing(0)
 
     tflops = w.flops / (ms_per_step * 1e-3) / 1e12
-    # Attention roofline: algorithmic FLOPs of each launch / its duration.
     C = len(sizes)
     launch_flops = [4.0 * w.S * w.S * sizes[i % C] * w.d for i in range(len(attn_ms))]
     avg_attn_ms = statistics.mean(attn_ms)
@@ -215,9 +268,9 @@ def main():
         "config": {
             "workload": f"{w.name}: S={w.S} (36 frames x 1560 tokens), H={w.H} local heads, "
                         f"d={w.d}, {w.dtype}, P={w.P} shards, chunks {'+'.join(map(str, sizes))}, "
-                        "pipelined pack+attention+unpack",
+                        f"pack+attention+unpack, {plan} schedule",
             "S": w.S, "H": w.H, "d": w.d, "P": w.P, "chunks": list(sizes),
-            "mode": "pipelined",
+            "mode": args.mode, "plan": plan,
         },
         "roofline": {
             "bound": "mfma",
@@ -228,7 +281,9 @@ def main():
             "traffic": measured_traffic(w.name, sizes),
             "kernel": "attention_kernel<128, bf16>",
             "per_launch": f"4*S^2*H_c*d FLOP per chunk launch; avg launch {avg_attn_ms:.4f} ms "
-                          f"over {len(attn_ms)} launches in the timed region",
+                          f"over {len(attn_ms)} launches, events on the launching stream, in "
+                          f"a second pass of the {args.steps} steps "
+                          f"({ms_per_step_events:.4f} ms per step with the events)",
         },
     }
 
@@ -236,8 +291,8 @@ def main():
         es = w.elem_bytes
         pk_bytes = [3 * 2 * w.S * sizes[i % C] * w.d * es for i in range(len(pack_ms))]
         up_bytes = [2 * w.S * sizes[i % C] * w.d * es for i in range(len(unpack_ms))]
-        pipe = {"pack_in_pipeline_GBps": round(sum(pk_bytes) / (sum(pack_ms) * 1e-3) / 1e9, 1),
-                "unpack_in_pipeline_GBps": round(sum(up_bytes) / (sum(unpack_ms) * 1e-3) / 1e9, 1)}
+        pipe = {"pack_in_step_GBps": round(sum(pk_bytes) / (sum(pack_ms) * 1e-3) / 1e9, 1),
+                "unpack_in_step_GBps": round(sum(up_bytes) / (sum(unpack_ms) * 1e-3) / 1e9, 1)}
 
         # ---- layout kernels alone on the Wan-P4, Wan-P8 and Stress shapes:
         # cold (MALL flushed) and warm.  A byte move does not depend on the
@@ -273,21 +328,14 @@ def main():
         res.update(pipe)
         result["layout"] = res
 
-        # ---- serial vs pipelined, interleaved (ABAB) ----
+        # ---- the schedules side by side: serial, Alg. 1, inline, lanes ----
         torch.cuda.synchronize()
-        reps = max(10, args.steps)
-        cmp = {}
-        for label, chunks in (("chunked", sizes), ("unchunked", (w.H,))):
-            a, b = [], []
-            for _ in range(reps):
-                a += time_region(lambda: step(hcms.MODE_SERIAL, chunks), 1)
-                b += time_region(lambda: step(hcms.MODE_PIPELINED, chunks), 1)
-            qa, qb = np.percentile(a, [25, 50, 75]), np.percentile(b, [25, 50, 75])
-            cmp[label] = {"chunks": list(chunks),
-                          "serial_ms": {"median": round(qa[1], 4), "iqr": [round(qa[0], 4), round(qa[2], 4)]},
-                          "pipelined_ms": {"median": round(qb[1], 4), "iqr": [round(qb[0], 4), round(qb[2], 4)]},
-                          "pipelined_below_serial": bool(qb[2] < qa[0])}
-        result["pipeline"] = cmp
+        reps = max(20, args.steps // 2)
+        cmp = [compare_modes(ctx, w, sizes, reps, dev), compare_modes(ctx, w, (w.H,), reps, dev)]
+        wp4 = inputs.WORKLOADS["wan_p4"]
+        for ch in ((5, 5), (10,)):
+            cmp.append(compare_modes(ctx, wp4, ch, reps, dev))
+        result["schedules"] = cmp
 
     if not args.no_cpu:
         log("timing the oracle on the host ...")

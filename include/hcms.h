@@ -140,6 +140,9 @@ HCMS_API int hcms_attention(const void *q, const void *k, const void *v, void *o
 /* Modes of hcms_forward / hcms_plan. */
 #define HCMS_MODE_SERIAL 0     /* every op on the main stream, chunk by chunk */
 #define HCMS_MODE_PIPELINED 1  /* Alg. 1: copy stream + compute stream + events */
+#define HCMS_MODE_INLINE 2     /* one lane, four synchronisations (see hcms_plan) */
+#define HCMS_MODE_LANES 3      /* chunks alternate between two streams (see hcms_plan) */
+#define HCMS_MODE_AUTO 4       /* hcms_forward only: inline or lanes, per hcms_auto_mode */
 
 /* Op kinds, streams and event ids of a plan (hcms_plan). */
 #define HCMS_OP_RECORD 0     /* record event `event` on `stream` */
@@ -170,11 +173,44 @@ typedef struct hcms_op {
  * E_c^attn and unpacks c; finally E_done is recorded on the copy stream and the
  * main stream waits it (the join of Alg. 1 as a stream wait, not a host sync).
  * Serial mode is pack c, attention c, unpack c on the main stream for every c.
+ * Inline and lanes modes are schedules for one GPU, where a pack or unpack
+ * costs a few hundred times less than a chunk's attention and each event
+ * record or wait on the critical path costs about as much as a copy.
+ * Inline mode keeps one lane on the main stream with four synchronisations:
+ * the main stream packs chunk 0 and records E_0^pack; the copy stream waits
+ * it, packs chunks 1..C-1 and records E_{C-1}^pack; the main stream runs
+ * every attention, waiting E_{C-1}^pack before attention 1 and recording
+ * E_{C-2}^attn before attention C-1; the copy stream waits E_{C-2}^attn,
+ * unpacks chunks 0..C-2 and records E_done; the main stream unpacks chunk
+ * C-1 and waits E_done.  The compute stream is not used.
+ * Lanes mode alternates chunks between the main stream (even c) and the
+ * compute stream (odd c), each running pack c, attention c, unpack c in
+ * order: the main stream records E_0^pack after chunk 0's pack, the compute
+ * stream waits it before its first chunk and records E_done after its last,
+ * and the main stream waits E_done after its own last chunk.  Besides the
+ * copies, the attention launches of the two lanes overlap, so that the
+ * workgroups of one fill the CUs the last round of the other leaves idle.
+ * The copy stream is not used.
+ * With one chunk the inline and lanes plans are the serial plan.
  *   ops : host array of `cap` entries, or NULL to query the count.
  * Returns the number of ops (>= 0), HCMS_ERR_CHUNKS (n_chunks < 1),
- * HCMS_ERR_ARG (mode) or HCMS_ERR_CAPACITY (cap too small; nothing written).
+ * HCMS_ERR_ARG (mode, or HCMS_MODE_AUTO, which has no fixed plan) or
+ * HCMS_ERR_CAPACITY (cap too small; nothing written).
  */
 HCMS_API int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap);
+
+/*
+ * The plan HCMS_MODE_AUTO runs: attention of chunk c launches
+ * W_c = ceil(S / Br) * H_c workgroups, of which n_cu * B run at once (Br and
+ * B the attention tiling for head dimension d: 256 queries and one workgroup
+ * per CU for d = 128, 128 and two for d = 64).  One lane takes
+ * sum_c ceil(W_c / (n_cu * B)) rounds of workgroups; two lanes pool them,
+ * ceil(sum_c W_c / (n_cu * B)).  Returns HCMS_MODE_LANES when pooling saves a
+ * round, HCMS_MODE_INLINE otherwise, HCMS_MODE_SERIAL for one chunk; or
+ * HCMS_ERR_SHAPE (S < 0, d), HCMS_ERR_ARG (n_cu < 1), HCMS_ERR_NULL or
+ * HCMS_ERR_CHUNKS.  Host only.
+ */
+HCMS_API int hcms_auto_mode(int S, int d, const int *chunk_sizes, int n_chunks, int n_cu);
 
 typedef struct hcms_ctx hcms_ctx;
 
@@ -186,6 +222,11 @@ typedef struct hcms_ctx hcms_ctx;
  * HIP.
  */
 HCMS_API int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out);
+
+/* The plan mode the context's last hcms_forward ran (HCMS_MODE_AUTO resolved;
+   -1 before the first call), and the device's compute-unit count. */
+HCMS_API int hcms_ctx_last_mode(const hcms_ctx *ctx);
+HCMS_API int hcms_ctx_num_cu(const hcms_ctx *ctx);
 
 /* Destroy a context (its events).  The caller must not destroy it while work
    that waits on its events is still pending.  NULL is accepted. */
@@ -212,14 +253,16 @@ HCMS_API int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap)
  *   pack Q, K, V of the chunk into heads [h0_c, h0_c + H_c) of the head-major
  *   workspaces, run attention on them into o_hm, and unpack o_hm's chunk into
  *   the head slots [h0_c, h0_c + H_c) of o_seq,
- * scheduled as hcms_plan(n_chunks, mode) describes.  Returns when everything
+ * scheduled as hcms_plan(n_chunks, mode) describes (HCMS_MODE_AUTO: the mode
+ * hcms_auto_mode picks for the device's CU count).  Returns when everything
  * is enqueued; `main_stream` is ordered after all of it on return (no host
- * synchronisation).  Serial and pipelined modes, and all chunkings, give
- * bit-identical o_seq.
+ * synchronisation).  All modes and all chunkings give bit-identical o_seq.
  *   q_seq, k_seq, v_seq, o_seq : device, [P][S/P][H][d]
  *   q_hm, k_hm, v_hm, o_hm     : device workspaces, [H][S][d] each
  *   copy_stream, compute_stream: used in pipelined mode; must be distinct from
- *                                each other and from main_stream
+ *                                each other and from main_stream.  Inline mode
+ *                                uses copy_stream only, lanes mode
+ *                                compute_stream only (distinct from main).
  * Errors: as hcms_pack and hcms_attention, plus ARG (mode, stream reuse,
  * context of another device) and CHUNKS (n_chunks > the context's max_chunks).
  */

@@ -22,7 +22,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhcms.so")
 
 BF16, FP32 = 0, 1
-MODE_SERIAL, MODE_PIPELINED = 0, 1
+MODE_SERIAL, MODE_PIPELINED, MODE_INLINE, MODE_LANES, MODE_AUTO = 0, 1, 2, 3, 4
 OP_RECORD, OP_WAIT, OP_PACK, OP_ATTENTION, OP_UNPACK = 0, 1, 2, 3, 4
 STREAM_MAIN, STREAM_COPY, STREAM_COMPUTE = 0, 1, 2
 
@@ -65,6 +65,9 @@ def load():
         "hcms_unpack": ([vp, vp, i, i, i, i, i, i, i, vp], i),
         "hcms_attention": ([vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
         "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
+        "hcms_auto_mode": ([i, i, ip, i, i], i),
+        "hcms_ctx_last_mode": ([vp], i),
+        "hcms_ctx_num_cu": ([vp], i),
         "hcms_ctx_create": ([i, i, ctypes.POINTER(vp)], i),
         "hcms_ctx_destroy": ([vp], i),
         "hcms_ctx_set_timing": ([vp, i], i),
@@ -132,6 +135,12 @@ def plan(n_chunks: int, mode: int = MODE_PIPELINED) -> list[tuple[int, int, int,
     return [(o.kind, o.stream, o.chunk, o.event) for o in ops]
 
 
+def auto_mode(S: int, d: int, chunk_sizes, n_cu: int) -> int:
+    """The plan mode MODE_AUTO runs for these chunks on n_cu compute units."""
+    sizes, n = _ints(chunk_sizes)
+    return _check(load().hcms_auto_mode(S, d, sizes, n, n_cu))
+
+
 def pack(src_seq: torch.Tensor, P: int, h_begin: int, h_count: int,
          out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """[S][H][d] (= [P][S/P][H][d]) -> [h_count][S][d] chunk of heads."""
@@ -185,7 +194,7 @@ def attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float,
 
 
 class Context:
-    """The dual-stream chunk scheduler (Alg. 1) bound to one device.
+    """The chunk scheduler (Alg. 1 and its one-GPU schedules) on one device.
 
     Owns the library context (cached events), a copy stream and a compute
     stream (default priority), and head-major workspaces that are reallocated
@@ -204,6 +213,15 @@ class Context:
         self._h = h
         self._ws = None
         self._ws_key = None
+
+    @property
+    def num_cu(self) -> int:
+        return _check(load().hcms_ctx_num_cu(self._h))
+
+    @property
+    def last_mode(self) -> int:
+        """Plan mode of the last forward (MODE_AUTO resolved), -1 before any."""
+        return load().hcms_ctx_last_mode(self._h)
 
     def close(self):
         if self._h:
@@ -240,7 +258,7 @@ class Context:
         return list(buf[:n])
 
     def forward(self, q_seq: torch.Tensor, k_seq: torch.Tensor, v_seq: torch.Tensor, P: int,
-                scale: float, chunk_sizes, mode: int = MODE_PIPELINED,
+                scale: float, chunk_sizes, mode: int = MODE_AUTO,
                 out: torch.Tensor | None = None, workspaces=None,
                 main_stream=None) -> torch.Tensor:
         """One GPU's share of an HCMS forward: [S][H][d] in, [S][H][d] out.

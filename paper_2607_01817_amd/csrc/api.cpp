@@ -131,18 +131,19 @@ struct PlanWriter {
     }
 };
 
-int build_plan(int C, int mode, PlanWriter &w) {
+void serial_plan(int C, PlanWriter &w) {
+    for (int c = 0; c < C; ++c) {
+        w.put(HCMS_OP_PACK, HCMS_STREAM_MAIN, c, -1);
+        w.put(HCMS_OP_ATTENTION, HCMS_STREAM_MAIN, c, -1);
+        w.put(HCMS_OP_UNPACK, HCMS_STREAM_MAIN, c, -1);
+    }
+}
+
+// Alg. 1 in its printed issue order.
+void alg1_plan(int C, PlanWriter &w) {
     const int e_main = 0, e_done = 1 + 2 * C;
     auto e_pack = [](int c) { return 1 + c; };
     auto e_attn = [C](int c) { return 1 + C + c; };
-    if (mode == HCMS_MODE_SERIAL) {
-        for (int c = 0; c < C; ++c) {
-            w.put(HCMS_OP_PACK, HCMS_STREAM_MAIN, c, -1);
-            w.put(HCMS_OP_ATTENTION, HCMS_STREAM_MAIN, c, -1);
-            w.put(HCMS_OP_UNPACK, HCMS_STREAM_MAIN, c, -1);
-        }
-        return w.n;
-    }
     // Main stream: fork.
     w.put(HCMS_OP_RECORD, HCMS_STREAM_MAIN, -1, e_main);
     // Copy stream: input layout of every chunk.
@@ -167,10 +168,108 @@ int build_plan(int C, int mode, PlanWriter &w) {
     // ordered after the last attention.
     w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_done);
     w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
+}
+
+// One lane with the fewest stream synchronisations, for one GPU.  On one GPU
+// a pack or unpack costs a few hundred times less than a chunk's attention,
+// and every event record or wait on the critical path costs a few
+// microseconds, about as much as the copies it hides.  So:
+//  - attention runs on the main stream (no fork or join of a third stream);
+//  - chunk 0's pack, which nothing can hide, runs in front of its attention,
+//    and the last chunk's unpack after its attention, on the same stream;
+//  - the copy stream starts after chunk 0's pack and packs chunks 1..C-1 while
+//    attention 0 runs; attention 1 waits once for all of them (E_{C-1}^pack;
+//    the copy stream runs them in order);
+//  - unpacks 0..C-2 wait once for attention C-2 (E_{C-2}^attn) and run while
+//    attention C-1 does; the main stream waits E_done after the last unpack.
+// Every pack c -> attention c -> unpack c dependency of Alg. 1 holds, with
+// four synchronisations on the main stream whatever C is.
+void inline_plan(int C, PlanWriter &w) {
+    if (C == 1) return serial_plan(C, w);
+    const int e_done = 1 + 2 * C;
+    auto e_pack = [](int c) { return 1 + c; };
+    auto e_attn = [C](int c) { return 1 + C + c; };
+    w.put(HCMS_OP_PACK, HCMS_STREAM_MAIN, 0, -1);
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_MAIN, -1, e_pack(0));
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COPY, -1, e_pack(0));
+    for (int c = 1; c < C; ++c) w.put(HCMS_OP_PACK, HCMS_STREAM_COPY, c, -1);
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_pack(C - 1));
+    for (int c = 0; c < C; ++c) {
+        if (c == C - 1) w.put(HCMS_OP_RECORD, HCMS_STREAM_MAIN, -1, e_attn(C - 2));
+        if (c == 1) w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_pack(C - 1));
+        w.put(HCMS_OP_ATTENTION, HCMS_STREAM_MAIN, c, -1);
+    }
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COPY, -1, e_attn(C - 2));
+    for (int c = 0; c < C - 1; ++c) w.put(HCMS_OP_UNPACK, HCMS_STREAM_COPY, c, -1);
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_done);
+    w.put(HCMS_OP_UNPACK, HCMS_STREAM_MAIN, C - 1, -1);
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
+}
+
+// Two lanes, for one GPU.  Chunks alternate between the main stream (even c)
+// and the compute stream (odd c); each lane runs pack c, attention c, unpack c
+// in order.  No chunk depends on another (the lemma of no inter-chunk
+// dependency), so the lanes only meet at the fork and the join.  One lane's
+// copies run beside the other lane's attention, and, which matters more on
+// one GPU, a chunk's attention launch leaves CUs idle in its last round of
+// workgroups that the other lane's attention fills.  The second lane starts
+// after chunk 0's pack (E_0^pack) so that its first pack does not take
+// bandwidth from the pack attention 0 waits for; the main stream waits E_done,
+// recorded at the end of the second lane.  Four synchronisations in all,
+// whatever C is.  One chunk has nothing to overlap: its plan is the serial one.
+void lanes_plan(int C, PlanWriter &w) {
+    if (C == 1) return serial_plan(C, w);
+    const int e_pack0 = 1, e_done = 1 + 2 * C;
+    auto chunk = [&](int c) {
+        const int s = (c & 1) ? HCMS_STREAM_COMPUTE : HCMS_STREAM_MAIN;
+        w.put(HCMS_OP_PACK, s, c, -1);
+        if (c == 0) w.put(HCMS_OP_RECORD, s, -1, e_pack0);
+        w.put(HCMS_OP_ATTENTION, s, c, -1);
+        w.put(HCMS_OP_UNPACK, s, c, -1);
+    };
+    chunk(0);
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COMPUTE, -1, e_pack0);
+    for (int c = 1; c < C; ++c) chunk(c);
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_COMPUTE, -1, e_done);
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
+}
+
+// Modes with a fixed plan (hcms_plan); HCMS_MODE_AUTO resolves to one of
+// them per call.
+bool plan_mode(int mode) {
+    return mode == HCMS_MODE_SERIAL || mode == HCMS_MODE_PIPELINED ||
+           mode == HCMS_MODE_INLINE || mode == HCMS_MODE_LANES;
+}
+
+int build_plan(int C, int mode, PlanWriter &w) {
+    if (mode == HCMS_MODE_SERIAL) serial_plan(C, w);
+    else if (mode == HCMS_MODE_PIPELINED) alg1_plan(C, w);
+    else if (mode == HCMS_MODE_INLINE) inline_plan(C, w);
+    else lanes_plan(C, w);
     return w.n;
 }
 
-int plan_size(int C, int mode) { return mode == HCMS_MODE_SERIAL ? 3 * C : 7 * C + 5; }
+int plan_size(int C, int mode) {
+    if (mode == HCMS_MODE_SERIAL || (C == 1 && mode != HCMS_MODE_PIPELINED)) return 3 * C;
+    if (mode == HCMS_MODE_PIPELINED) return 7 * C + 5;
+    return mode == HCMS_MODE_INLINE ? 3 * C + 8 : 3 * C + 4;
+}
+
+// Rounds of attention workgroups: a launch of W workgroups on `slots`
+// concurrent slots takes ceil(W / slots) rounds; two lanes pool the chunks.
+int auto_mode(int S, int d, const int *sizes, int C, int n_cu) {
+    if (C == 1) return HCMS_MODE_SERIAL;
+    const int64_t br = hcms::attention_queries_per_block(d);
+    const int64_t slots = static_cast<int64_t>(n_cu) * hcms::attention_blocks_per_cu(d);
+    const int64_t tiles = (S + br - 1) / br;
+    int64_t rounds = 0, total = 0;
+    for (int c = 0; c < C; ++c) {
+        const int64_t wc = tiles * sizes[c];
+        rounds += (wc + slots - 1) / slots;
+        total += wc;
+    }
+    return rounds > (total + slots - 1) / slots ? HCMS_MODE_LANES : HCMS_MODE_INLINE;
+}
 
 // Saves the current device, switches to `dev`, restores on scope exit.
 struct DeviceGuard {
@@ -191,6 +290,8 @@ struct DeviceGuard {
 struct hcms_ctx {
     int device = 0;
     int max_chunks = 0;
+    int n_cu = 0;                        // compute units of the device
+    int last_mode = -1;                  // plan mode of the last hcms_forward
     std::vector<hipEvent_t> events;      // 2 * max_chunks + 2 sync events
     std::vector<hcms_op> plan;           // scratch for the op list
     int timing_calls = 0;                // calls to time (0 = off)
@@ -295,8 +396,9 @@ int hcms_attention(const void *q, const void *k, const void *v, void *out, int S
 
 int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
     if (n_chunks < 1) return fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be >= 1", n_chunks);
-    if (mode != HCMS_MODE_SERIAL && mode != HCMS_MODE_PIPELINED)
-        return fail(HCMS_ERR_ARG, "mode %d is neither serial (0) nor pipelined (1)", mode);
+    if (!plan_mode(mode))
+        return fail(HCMS_ERR_ARG, "mode %d has no fixed plan (serial 0, pipelined 1, inline 2, "
+                    "lanes 3)", mode);
     const int need = plan_size(n_chunks, mode);
     if (ops == nullptr) {
         ok();
@@ -307,6 +409,35 @@ int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
     const int n = build_plan(n_chunks, mode, w);
     ok();
     return n;
+}
+
+int hcms_auto_mode(int S, int d, const int *chunk_sizes, int n_chunks, int n_cu) {
+    if (S < 0) return fail(HCMS_ERR_SHAPE, "S=%d must be >= 0", S);
+    if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
+    if (n_cu < 1) return fail(HCMS_ERR_ARG, "n_cu=%d must be >= 1", n_cu);
+    if (!chunk_sizes) return fail(HCMS_ERR_NULL, "chunk_sizes is NULL");
+    if (n_chunks < 1) return fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be >= 1", n_chunks);
+    int H = 0;
+    for (int c = 0; c < n_chunks; ++c) {
+        if (chunk_sizes[c] < 1) return fail(HCMS_ERR_CHUNKS, "chunk %d is empty", c);
+        H += chunk_sizes[c];
+    }
+    int st = check_chunks(H, chunk_sizes, n_chunks);
+    if (st != HCMS_OK) return st;
+    ok();
+    return auto_mode(S, d, chunk_sizes, n_chunks, n_cu);
+}
+
+int hcms_ctx_last_mode(const hcms_ctx *ctx) {
+    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    ok();
+    return ctx->last_mode;
+}
+
+int hcms_ctx_num_cu(const hcms_ctx *ctx) {
+    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    ok();
+    return ctx->n_cu;
 }
 
 int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out) {
@@ -324,6 +455,11 @@ int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out) {
     if (!ctx) return fail(HCMS_ERR_ARG, "out of host memory");
     ctx->device = device;
     ctx->max_chunks = max_chunks;
+    e = hipDeviceGetAttribute(&ctx->n_cu, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess || ctx->n_cu < 1) {
+        delete ctx;
+        return hip_fail(e != hipSuccess ? e : hipErrorInvalidValue, "hipDeviceGetAttribute");
+    }
     ctx->plan.resize(plan_size(max_chunks, HCMS_MODE_PIPELINED));
     const int n_sync = 2 * max_chunks + 2;
     for (int i = 0; i < n_sync; ++i) {
@@ -406,8 +542,9 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
     if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
     if (S > 0 && (!q_seq || !k_seq || !v_seq || !o_seq || !q_hm || !k_hm || !v_hm || !o_hm))
         return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
-    if (mode != HCMS_MODE_SERIAL && mode != HCMS_MODE_PIPELINED)
-        return fail(HCMS_ERR_ARG, "mode %d is neither serial (0) nor pipelined (1)", mode);
+    if (!plan_mode(mode) && mode != HCMS_MODE_AUTO)
+        return fail(HCMS_ERR_ARG, "mode %d is not serial (0), pipelined (1), inline (2), lanes (3) "
+                    "or auto (4)", mode);
     if ((st = check_dtype(dtype)) != HCMS_OK) return st;
     if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
     int log2u = 0;
@@ -421,6 +558,11 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
     if (mode == HCMS_MODE_PIPELINED &&
         (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
         return fail(HCMS_ERR_ARG, "pipelined mode needs three distinct streams");
+    if (mode == HCMS_MODE_AUTO) mode = auto_mode(S, d, chunk_sizes, n_chunks, ctx->n_cu);
+    if (mode == HCMS_MODE_INLINE && copy_stream == main_stream)
+        return fail(HCMS_ERR_ARG, "inline mode needs a copy stream distinct from the main stream");
+    if (mode == HCMS_MODE_LANES && compute_stream == main_stream)
+        return fail(HCMS_ERR_ARG, "lanes mode needs a compute stream distinct from the main stream");
     const void *all[8] = {q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm};
     for (const void *p : all)
         if (!aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
@@ -442,6 +584,7 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
 
     PlanWriter w{ctx->plan.data(), static_cast<int>(ctx->plan.size())};
     const int n_ops = build_plan(n_chunks, mode, w);
+    ctx->last_mode = mode;
 
     hipStream_t streams[3] = {static_cast<hipStream_t>(main_stream),
                               static_cast<hipStream_t>(copy_stream),

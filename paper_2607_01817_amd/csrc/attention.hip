@@ -399,10 +399,17 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
     }
 }
 
+// Waves per workgroup: 8 for d = 128 (one workgroup per CU, two waves per
+// SIMD), 4 for d = 64 (two workgroups per CU).
+template <int D>
+struct Waves {
+    static constexpr int value = D == 128 ? 8 : 4;
+};
+
 template <int D, typename T>
 hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, int S, int n_heads,
                         float c, hipStream_t stream) {
-    constexpr int WAVES = D == 128 ? 8 : 4;
+    constexpr int WAVES = Waves<D>::value;
     constexpr int BR = kQW * WAVES;
     const int n_qtiles = (S + BR - 1) / BR;
     const int64_t blocks = static_cast<int64_t>(n_qtiles) * n_heads;
@@ -414,6 +421,9 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, in
 }
 
 }  // namespace
+
+int attention_queries_per_block(int d) { return kQW * (d == 128 ? Waves<128>::value : Waves<64>::value); }
+int attention_blocks_per_cu(int d) { return 8 / (d == 128 ? Waves<128>::value : Waves<64>::value); }
 
 hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, int S,
                             int n_heads, int d, float scale_log2e, int dtype, hipStream_t stream) {

@@ -21,6 +21,11 @@ hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64
 // Attention of `n_heads` consecutive heads, head-major [n_heads][S][d]
 // buffers starting at the chunk's first head.  scale_log2e = scale * log2(e).
 // dtype: 0 = bf16 storage, 1 = fp32 storage.  d in {64, 128}.
+// Tiling of the attention launch: queries per workgroup, and workgroups one
+// CU holds at once, for head dimension d (64 or 128).
+int attention_queries_per_block(int d);
+int attention_blocks_per_cu(int d);
+
 hipError_t launch_attention(const void *q, const void *k, const void *v, void *o,
                             int S, int n_heads, int d, float scale_log2e, int dtype,
                             hipStream_t stream);

@@ -14,6 +14,16 @@
 // full rows.  No LDS stage is needed for coalescing.  Each thread issues all of
 // its loads before any store to keep several 16-byte requests in flight.  The
 // source is read once, so its loads carry the non-temporal hint.
+//
+// Register budget.  In the pipelined schedule these kernels run while an
+// attention workgroup holds its CU; that workgroup leaves 32 VGPRs per SIMD
+// lane free (two waves of at most 240).  A copy wave that fits in those 32
+// registers is placed beside the attention waves instead of waiting for the CU
+// to drain, so the copy never delays an attention workgroup's start.  The
+// kernels therefore address memory through buffer resources built per
+// workgroup (64-bit bases in scalar registers, 32-bit lane offsets), and the
+// hardware range check of the resource replaces per-lane tail branches:
+// out-of-range loads return zero and out-of-range stores are dropped.
 #include "hcms_internal.h"
 
 namespace hcms {
@@ -23,63 +33,87 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
-constexpr int kUnitsPerBlock = kThreads * kUnroll;
+constexpr int kUnitsPerBlock = kThreads * kUnroll;  // 16-byte units per workgroup
+constexpr int kNonTemporal = 2;                     // cache-policy bit of a streaming load
 
 struct PackPtrs {
-    const u32x4 *src[3];
-    u32x4 *dst[3];
+    const char *src[3];
+    char *dst[3];
 };
 
-// grid: x = ceil(S * units_per_row / kUnitsPerBlock), y = hc, z = tensor.
+// Resource over [base, base + min(bytes, 2^32 - 1)).
+__device__ inline __amdgpu_buffer_rsrc_t span_rsrc(const char *base, int64_t bytes) {
+    const int64_t n = bytes < 0 ? 0 : (bytes > 0xFFFFFFFFll ? 0xFFFFFFFFll : bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(base), 0,
+                                             static_cast<int>(static_cast<uint32_t>(n)),
+                                             0x00020000);
+}
+
+// Workgroup (x, j, z) moves dense units [u0, u0 + kUnitsPerBlock) of chunk
+// head j of tensor z; those are rows t0 .. t0 + kUnitsPerBlock / U - 1 of the
+// strided side, which lie within 4096 * H * kUnroll bytes of the row of t0.
+struct BlockSpans {
+    int64_t dense_off, dense_left, strided_off, strided_left;
+};
+
+template <int LOG2U>
+__device__ inline BlockSpans block_spans(int64_t S, int64_t H, int64_t h0) {
+    const int64_t j = blockIdx.y;
+    const int64_t u0 = static_cast<int64_t>(blockIdx.x) * kUnitsPerBlock;
+    const int64_t t0 = u0 >> LOG2U;
+    BlockSpans b;
+    b.dense_off = ((j * S) << (LOG2U + 4)) + (u0 << 4);
+    b.dense_left = ((S << LOG2U) - u0) << 4;
+    b.strided_off = ((t0 * H + h0 + j) << (LOG2U + 4));
+    b.strided_left = ((S * H) << (LOG2U + 4)) - b.strided_off;
+    return b;
+}
+
+// Byte offset of local unit lu = tid + i * kThreads on the strided side,
+// relative to the row of t0: (lu / U) rows of H heads, then the unit in row.
+template <int LOG2U>
+__device__ inline uint32_t strided_lane_off(uint32_t tid, uint32_t H) {
+    return (((tid >> LOG2U) * H) << (LOG2U + 4)) + ((tid & ((1u << LOG2U) - 1)) << 4);
+}
+
+// grid: x = ceil(S * U / kUnitsPerBlock), y = hc, z = tensor.
 template <int LOG2U>
 __global__ __launch_bounds__(kThreads) void pack_kernel(PackPtrs p, int64_t S, int64_t H,
                                                         int64_t h0) {
-    const int64_t j = blockIdx.y;
-    const u32x4 *__restrict__ src = p.src[blockIdx.z];
-    u32x4 *__restrict__ dst = p.dst[blockIdx.z] + ((j * S) << LOG2U);
-    const int64_t n = S << LOG2U;
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kUnitsPerBlock + threadIdx.x;
+    const BlockSpans b = block_spans<LOG2U>(S, H, h0);
+    const __amdgpu_buffer_rsrc_t src =
+        span_rsrc(p.src[blockIdx.z] + b.strided_off, b.strided_left);
+    const __amdgpu_buffer_rsrc_t dst = span_rsrc(p.dst[blockIdx.z] + b.dense_off, b.dense_left);
+    const uint32_t tid = threadIdx.x;
+    const uint32_t so = strided_lane_off<LOG2U>(tid, static_cast<uint32_t>(H));
+    const uint32_t step = static_cast<uint32_t>(H) * (kThreads << 4);  // kThreads units down
     u32x4 buf[kUnroll];
 #pragma unroll
-    for (int i = 0; i < kUnroll; ++i) {
-        const int64_t u = base + i * kThreads;
-        if (u < n) {
-            const int64_t t = u >> LOG2U;
-            const int64_t w = u & ((1 << LOG2U) - 1);
-            buf[i] = __builtin_nontemporal_load(src + ((t * H + h0 + j) << LOG2U) + w);
-        }
-    }
+    for (int i = 0; i < kUnroll; ++i)
+        buf[i] = __builtin_amdgcn_raw_buffer_load_b128(src, so + i * step, 0, kNonTemporal);
 #pragma unroll
-    for (int i = 0; i < kUnroll; ++i) {
-        const int64_t u = base + i * kThreads;
-        if (u < n) dst[u] = buf[i];
-    }
+    for (int i = 0; i < kUnroll; ++i)
+        __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, (tid << 4) + i * (kThreads << 4), 0, 0);
 }
 
-// grid: x = ceil(S * units_per_row / kUnitsPerBlock), y = hc.
+// grid: x = ceil(S * U / kUnitsPerBlock), y = hc.
 template <int LOG2U>
-__global__ __launch_bounds__(kThreads) void unpack_kernel(const u32x4 *__restrict__ src_all,
-                                                          u32x4 *__restrict__ dst, int64_t S,
-                                                          int64_t H, int64_t h0) {
-    const int64_t j = blockIdx.y;
-    const u32x4 *__restrict__ src = src_all + ((j * S) << LOG2U);
-    const int64_t n = S << LOG2U;
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kUnitsPerBlock + threadIdx.x;
+__global__ __launch_bounds__(kThreads) void unpack_kernel(const char *src_all, char *dst_all,
+                                                          int64_t S, int64_t H, int64_t h0) {
+    const BlockSpans b = block_spans<LOG2U>(S, H, h0);
+    const __amdgpu_buffer_rsrc_t src = span_rsrc(src_all + b.dense_off, b.dense_left);
+    const __amdgpu_buffer_rsrc_t dst = span_rsrc(dst_all + b.strided_off, b.strided_left);
+    const uint32_t tid = threadIdx.x;
+    const uint32_t so = strided_lane_off<LOG2U>(tid, static_cast<uint32_t>(H));
+    const uint32_t step = static_cast<uint32_t>(H) * (kThreads << 4);
     u32x4 buf[kUnroll];
 #pragma unroll
-    for (int i = 0; i < kUnroll; ++i) {
-        const int64_t u = base + i * kThreads;
-        if (u < n) buf[i] = __builtin_nontemporal_load(src + u);
-    }
+    for (int i = 0; i < kUnroll; ++i)
+        buf[i] = __builtin_amdgcn_raw_buffer_load_b128(src, (tid << 4) + i * (kThreads << 4), 0,
+                                                       kNonTemporal);
 #pragma unroll
-    for (int i = 0; i < kUnroll; ++i) {
-        const int64_t u = base + i * kThreads;
-        if (u < n) {
-            const int64_t t = u >> LOG2U;
-            const int64_t w = u & ((1 << LOG2U) - 1);
-            dst[((t * H + h0 + j) << LOG2U) + w] = buf[i];
-        }
-    }
+    for (int i = 0; i < kUnroll; ++i)
+        __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, so + i * step, 0, 0);
 }
 
 dim3 grid_for(int64_t S, int64_t hc, int log2_units, int n_tensors) {
@@ -95,20 +129,25 @@ void pack_dispatch(const PackPtrs &p, int n_tensors, int64_t S, int64_t H, int64
 }
 
 template <int LOG2U>
-void unpack_dispatch(const u32x4 *src, u32x4 *dst, int64_t S, int64_t H, int64_t h0,
-                     int64_t hc, hipStream_t stream) {
+void unpack_dispatch(const char *src, char *dst, int64_t S, int64_t H, int64_t h0, int64_t hc,
+                     hipStream_t stream) {
     unpack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, 1), kThreads, 0, stream>>>(src, dst, S, H, h0);
 }
+
+// Lane offsets on the strided side are 32-bit: a workgroup spans at most
+// kUnitsPerBlock rows of H heads, 16 KiB * H bytes.
+bool strided_span_fits(int64_t H) { return H > 0 && H * (int64_t{kUnitsPerBlock} << 4) < (int64_t{1} << 32); }
 
 }  // namespace
 
 hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, int64_t S,
                        int64_t H, int64_t h0, int64_t hc, int log2_units, hipStream_t stream) {
     if (S == 0 || hc == 0) return hipSuccess;
+    if (!strided_span_fits(H) || n_tensors < 1 || n_tensors > 3) return hipErrorInvalidValue;
     PackPtrs p{};
     for (int z = 0; z < n_tensors; ++z) {
-        p.src[z] = static_cast<const u32x4 *>(src[z]);
-        p.dst[z] = static_cast<u32x4 *>(dst[z]);
+        p.src[z] = static_cast<const char *>(src[z]);
+        p.dst[z] = static_cast<char *>(dst[z]);
     }
     switch (log2_units) {
         case 0: pack_dispatch<0>(p, n_tensors, S, H, h0, hc, stream); break;
@@ -126,8 +165,9 @@ hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, 
 hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64_t h0,
                          int64_t hc, int log2_units, hipStream_t stream) {
     if (S == 0 || hc == 0) return hipSuccess;
-    const u32x4 *s = static_cast<const u32x4 *>(src);
-    u32x4 *d = static_cast<u32x4 *>(dst);
+    if (!strided_span_fits(H)) return hipErrorInvalidValue;
+    const char *s = static_cast<const char *>(src);
+    char *d = static_cast<char *>(dst);
     switch (log2_units) {
         case 0: unpack_dispatch<0>(s, d, S, H, h0, hc, stream); break;
         case 1: unpack_dispatch<1>(s, d, S, H, h0, hc, stream); break;

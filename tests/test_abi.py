@@ -97,36 +97,132 @@ def kernel_ops(ops, kind):
     return {op[2]: i for i, op in enumerate(ops) if op[0] == kind}
 
 
-@pytest.mark.parametrize("C", [1, 2, 3, 5, 10])
-def test_pipelined_plan_orders_every_dependency(lib, C):
-    ops = hcms.plan(C, hcms.MODE_PIPELINED)
-    assert len(ops) == 7 * C + 5
+def check_pipelined_dependencies(ops, C, attention_stream):
+    """The dependencies of Alg. 1 hold in a plan, whatever streams run what:
+    pack c -> attention c -> unpack c, every kernel ordered after the main
+    stream's position at the call and before its position at the return,
+    and nothing else forced between neighbouring chunks (lemma of no
+    inter-chunk dependency)."""
     reach = happens_before(ops)
     pk, at, up = (kernel_ops(ops, k) for k in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK))
     assert sorted(pk) == sorted(at) == sorted(up) == list(range(C))
     for c in range(C):
-        assert ops[pk[c]][1] == hcms.STREAM_COPY
-        assert ops[at[c]][1] == hcms.STREAM_COMPUTE
-        assert ops[up[c]][1] == hcms.STREAM_COPY
+        assert attention_stream is None or ops[at[c]][1] == attention_stream
         assert at[c] in reach[pk[c]], "attention must wait for its pack"
         assert up[c] in reach[at[c]], "unpack must wait for its attention"
-    # The fork: every kernel is after E_main's record on the main stream.
-    assert ops[0] == (hcms.OP_RECORD, hcms.STREAM_MAIN, -1, 0)
-    for i, op in enumerate(ops):
-        if op[0] in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK):
-            assert i in reach[0]
-    # The join: the main stream's last op is after every kernel.
-    last_main = max(i for i, op in enumerate(ops) if op[1] == hcms.STREAM_MAIN)
-    for i, op in enumerate(ops):
-        if op[0] in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK):
-            assert last_main in reach[i]
-    # Overlap is allowed: pack c+1 is not ordered after attention c (Lemma of
-    # no inter-chunk dependency), and attention c+1 not after unpack c.
+    kernels = [i for i, op in enumerate(ops)
+               if op[0] in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK)]
+    main = [i for i, op in enumerate(ops) if op[1] == hcms.STREAM_MAIN]
+    first_main, last_main = main[0], main[-1]
+    for i in kernels:   # fork: after the main stream's first op (or it)
+        assert i == first_main or i in reach[first_main]
+    for i in kernels:   # join: the main stream's last op is after every kernel
+        assert i == last_main or last_main in reach[i]
     for c in range(C - 1):
         assert pk[c + 1] not in reach[at[c]]
         assert at[c + 1] not in reach[up[c]]
+    # Every wait names an event recorded before it in issue order (checked by
+    # happens_before) and every event is recorded at most once per call.
+    recorded = [op[3] for op in ops if op[0] == hcms.OP_RECORD]
+    assert len(recorded) == len(set(recorded))
+    return pk, at, up
+
+
+@pytest.mark.parametrize("C", [1, 2, 3, 5, 10])
+def test_pipelined_plan_orders_every_dependency(lib, C):
+    ops = hcms.plan(C, hcms.MODE_PIPELINED)
+    assert len(ops) == 7 * C + 5
+    assert ops[0] == (hcms.OP_RECORD, hcms.STREAM_MAIN, -1, 0)
+    pk, at, up = check_pipelined_dependencies(ops, C, hcms.STREAM_COMPUTE)
+    for c in range(C):
+        assert ops[pk[c]][1] == hcms.STREAM_COPY
+        assert ops[up[c]][1] == hcms.STREAM_COPY
     # Alg. 1 issue order on the copy stream: all packs before any unpack.
     assert max(pk.values()) < min(up.values())
+
+
+@pytest.mark.parametrize("C", [2, 3, 5, 10])
+def test_inline_plan_orders_every_dependency(lib, C):
+    ops = hcms.plan(C, hcms.MODE_INLINE)
+    assert len(ops) == 3 * C + 8
+    pk, at, up = check_pipelined_dependencies(ops, C, hcms.STREAM_MAIN)
+    assert ops[pk[0]][1] == hcms.STREAM_MAIN and ops[up[C - 1]][1] == hcms.STREAM_MAIN
+    for c in range(1, C):
+        assert ops[pk[c]][1] == hcms.STREAM_COPY
+        assert ops[up[c - 1]][1] == hcms.STREAM_COPY
+    assert all(op[1] != hcms.STREAM_COMPUTE for op in ops)
+    reach = happens_before(ops)
+    # Packs 1..C-1 start after chunk 0's and overlap attention 0; unpacks
+    # 0..C-2 overlap the last attention.
+    for c in range(1, C):
+        assert pk[c] in reach[pk[0]] and pk[c] not in reach[at[0]]
+        assert up[c - 1] not in reach[at[C - 1]] and at[C - 1] not in reach[up[c - 1]]
+    # Four synchronisations on the main stream, whatever C is.
+    syncs = [op for op in ops if op[1] == hcms.STREAM_MAIN and op[0] in (hcms.OP_RECORD, hcms.OP_WAIT)]
+    assert len(syncs) == 4
+
+
+@pytest.mark.parametrize("C", [2, 3, 5, 10])
+def test_lanes_plan_orders_every_dependency(lib, C):
+    ops = hcms.plan(C, hcms.MODE_LANES)
+    assert len(ops) == 3 * C + 4
+    pk, at, up = check_pipelined_dependencies(ops, C, None)
+    for c in range(C):
+        lane = hcms.STREAM_COMPUTE if c % 2 else hcms.STREAM_MAIN
+        assert ops[pk[c]][1] == ops[at[c]][1] == ops[up[c]][1] == lane
+    assert all(op[1] != hcms.STREAM_COPY for op in ops)
+    reach = happens_before(ops)
+    # Chunks of different lanes are unordered: their kernels may overlap.
+    for c in range(C):
+        for c2 in range(c + 1, C):
+            if (c2 - c) % 2 and c > 0:
+                for a in (pk[c], at[c], up[c]):
+                    for b in (pk[c2], at[c2], up[c2]):
+                        assert b not in reach[a] and a not in reach[b], (c, c2)
+    # The second lane starts after chunk 0's pack only.
+    assert pk[1] in reach[pk[0]] and pk[1] not in reach[at[0]]
+    # Four synchronisations, whatever C is.
+    assert sum(op[0] in (hcms.OP_RECORD, hcms.OP_WAIT) for op in ops) == 4
+
+
+def test_one_gpu_plans_with_one_chunk_are_serial(lib):
+    assert hcms.plan(1, hcms.MODE_LANES) == hcms.plan(1, hcms.MODE_SERIAL)
+    assert hcms.plan(1, hcms.MODE_INLINE) == hcms.plan(1, hcms.MODE_SERIAL)
+
+
+# Rounds of attention workgroups, worked by hand for 256 CUs.  d = 128: 256
+# queries per workgroup, one per CU; d = 64: 128 queries, two per CU.
+@pytest.mark.parametrize("S,d,sizes,want", [
+    (56160, 128, (2, 2, 1), "inline"),        # 220 tiles: 2+2+1 rounds = ceil(1100/256) = 5
+    (56160, 128, (1, 1, 1, 1, 1), "inline"),  # 5 x 1 = ceil(1100/256) = 5
+    (32760, 128, (5, 5), "lanes"),            # 128 tiles: 3+3 = 6 > ceil(1280/256) = 5
+    (32760, 128, (4, 3, 3), "lanes"),         # 2+2+2 = 6 > 5
+    (100000, 128, (10, 10, 10, 10), "lanes"),  # 391 tiles: 4 x 16 = 64 > ceil(15640/256) = 62
+    (100000, 128, (14, 13, 13), "inline"),    # 22+20+20 = 62 = ceil(15640/256)
+    (65536, 128, (2, 2), "inline"),           # 256 tiles: 2+2 = 4 = ceil(1024/256)
+    (4096, 128, (3, 3, 2), "lanes"),          # 16 tiles: 1+1+1 = 3 > ceil(128/256) = 1
+    (4096, 64, (3, 3, 2), "lanes"),           # 32 tiles, 512 slots: 3 > 1
+    (32768, 64, (4, 4), "inline"),            # 256 tiles, 512 slots: 2+2 = 4 = ceil(2048/512)
+    (32768, 64, (3, 5), "lanes"),             # 2+3 = 5 > ceil(2048/512) = 4
+    (56160, 128, (5,), "serial"),             # one chunk
+    (0, 128, (2, 2), "inline"),               # nothing to launch: 0 rounds either way
+])
+def test_auto_mode_by_rounds(lib, S, d, sizes, want):
+    modes = {"serial": hcms.MODE_SERIAL, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES}
+    assert hcms.auto_mode(S, d, sizes, 256) == modes[want]
+
+
+def test_auto_mode_validation(lib):
+    sizes = (ctypes.c_int * 2)(2, 2)
+    assert lib.hcms_auto_mode(-1, 128, sizes, 2, 256) == ESHAPE
+    assert lib.hcms_auto_mode(100, 96, sizes, 2, 256) == ESHAPE
+    assert lib.hcms_auto_mode(100, 128, sizes, 2, 0) == EARG
+    assert lib.hcms_auto_mode(100, 128, None, 2, 256) == ENULL
+    assert lib.hcms_auto_mode(100, 128, sizes, 0, 256) == ECHUNKS
+    bad = (ctypes.c_int * 2)(2, 0)
+    assert lib.hcms_auto_mode(100, 128, bad, 2, 256) == ECHUNKS
+    assert lib.hcms_ctx_last_mode(None) == ENULL
+    assert lib.hcms_ctx_num_cu(None) == ENULL
 
 
 @pytest.mark.parametrize("C", [1, 4])
@@ -142,6 +238,10 @@ def test_serial_plan(lib, C):
 def test_plan_errors(lib):
     assert lib.hcms_plan(0, 1, None, 0) == ECHUNKS
     assert lib.hcms_plan(2, 7, None, 0) == EARG
+    assert lib.hcms_plan(2, hcms.MODE_AUTO, None, 0) == EARG   # no fixed plan
+    assert lib.hcms_plan(2, 5, None, 0) == EARG
+    assert lib.hcms_plan(2, hcms.MODE_INLINE, None, 0) == 14
+    assert lib.hcms_plan(2, hcms.MODE_LANES, None, 0) == 10
     ops = (hcms.Op * 3)()
     assert lib.hcms_plan(2, 1, ops, 3) == ECAP
     assert lib.hcms_plan(2, 1, None, 0) == 19

@@ -65,6 +65,30 @@ def test_pack_unpack_bit_exact(hcms, oracle_mod, name):
         del out
 
 
+@pytest.mark.parametrize("d,dtype", [(8, torch.bfloat16), (16, torch.bfloat16),
+                                     (16, torch.float32), (64, torch.bfloat16),
+                                     (128, torch.float32), (256, torch.float32)])
+def test_pack_unpack_every_row_size(hcms, oracle_mod, d, dtype):
+    """Rows of 16 .. 1024 bytes (every unit count the kernels specialise on),
+    an odd head count, a middle chunk and a token count that leaves a ragged
+    last workgroup for every row size."""
+    S, H, P, h0, hc = 8 * 131, 7, 8, 2, 3
+    log(f"[pack/unpack rows] d={d} {dtype} S={S} H={H} chunk {h0}+{hc}")
+    g = torch.Generator().manual_seed(d)
+    x = torch.randn(S, H, d, generator=g).to(dtype)
+    xb = bits(x).numpy()
+    chunk = hcms.pack(x.cuda(), P, h0, hc)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(chunk.cpu()).numpy(), oracle_mod.pack(xb, P, h0, hc))
+    dst = torch.empty(S, H, d, dtype=dtype, device="cuda")
+    _fill_bits(dst)
+    before = bits(dst.cpu()).numpy()
+    hcms.unpack(chunk, dst, P, h0)
+    torch.cuda.synchronize()
+    want = oracle_mod.unpack(bits(chunk.cpu()).numpy(), before, P, h0)
+    assert np.array_equal(bits(dst.cpu()).numpy(), want)
+
+
 def test_unpack_leaves_other_heads(hcms):
     S, H, d, P = 1024, 6, 128, 8
     g = torch.Generator().manual_seed(11)
@@ -195,7 +219,8 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
     ref = hcms.attention(_cuda_hm(q), _cuda_hm(k), _cuda_hm(v), w.scale).permute(1, 0, 2).contiguous()
     ctx = hcms.Context(max_chunks=16)
     for sizes in _chunkings(w):
-        for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED):
+        for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED, hcms.MODE_INLINE, hcms.MODE_LANES,
+                     hcms.MODE_AUTO):
             out = ctx.forward(qd, kd, vd, w.P, w.scale, sizes, mode=mode)
             assert torch.equal(bits(out), bits(ref)), (name, sizes, mode)
     out = ctx.forward(qd, kd, vd, w.P, w.scale, w.chunkings[-1]).float().cpu()
@@ -205,6 +230,22 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
                                          head_major_np(v, h), w.scale, rows[h])
         got = out[torch.from_numpy(rows[h]), h].double().numpy()
         check_attention_rows(got, want, f"forward {name} head {h}")
+    ctx.close()
+
+
+@pytest.mark.parametrize("name,sizes", [("wan_p8", (2, 2, 1)), ("wan_p4", (5, 5)),
+                                        ("small", (3, 3, 2)), ("small", (8,))])
+def test_auto_mode_runs_the_predicted_plan(hcms, name, sizes):
+    w = inputs.WORKLOADS[name]
+    q, k, v = (x.cuda() for x in workload_inputs(name))
+    ctx = hcms.Context()
+    assert ctx.num_cu == torch.cuda.get_device_properties(0).multi_processor_count
+    assert ctx.last_mode == -1
+    ctx.forward(q, k, v, w.P, w.scale, sizes, mode=hcms.MODE_AUTO)
+    assert ctx.last_mode == hcms.auto_mode(w.S, w.d, sizes, ctx.num_cu)
+    ctx.forward(q, k, v, w.P, w.scale, sizes, mode=hcms.MODE_PIPELINED)
+    assert ctx.last_mode == hcms.MODE_PIPELINED
+    torch.cuda.synchronize()
     ctx.close()
 
 
@@ -226,8 +267,9 @@ def _delay(stream, cycles=40_000_000):
         torch.cuda._sleep(cycles)
 
 
+@pytest.mark.parametrize("mode", ["pipelined", "inline", "lanes"])
 @pytest.mark.parametrize("late", ["copy", "compute", "main"])
-def test_pipelined_respects_events_under_delay(hcms, late):
+def test_pipelined_respects_events_under_delay(hcms, late, mode):
     """Poison the workspaces and the output, delay one stream with a bounded
     spin kernel, and read the output on the main stream right after the call
     returns.  A missing wait (fork, E_c^pack, E_c^attn or the join) would let
@@ -254,10 +296,11 @@ def test_pipelined_respects_events_under_delay(hcms, late):
     else:
         torch.cuda.synchronize()
         _delay(ctx.copy_stream if late == "copy" else ctx.compute_stream)
-    ctx.forward(q_in, k, v, w.P, w.scale, sizes, mode=hcms.MODE_PIPELINED, out=out)
+    m = {"pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES}[mode]
+    ctx.forward(q_in, k, v, w.P, w.scale, sizes, mode=m, out=out)
     seen = out.clone()            # on the main stream, no host sync in between
     torch.cuda.synchronize()
-    assert torch.equal(bits(seen), bits(ref)), late
+    assert torch.equal(bits(seen), bits(ref)), (late, mode)
     ctx.close()
 
 
