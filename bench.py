@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import statistics
 import sys
@@ -167,6 +168,60 @@ def compare_modes(ctx, w, chunks, reps: int, dev):
         qm["gain_vs_serial_ms"] = round(ser["median"] - qm["median"], 4)
         qm["below_serial"] = bool(qm["iqr"][1] < ser["iqr"][0])
         res[m + "_ms"] = qm
+    del q, k, v, out
+    return res
+
+
+def time_model_sweep(ctx, w, reps: int, dev):
+    """The paper's chunk-count study on one GPU: for C = 1..H (the default
+    partition), the serial, Alg. 1 and auto schedules interleaved, the layout
+    and attention kernel times of the serial run, and the time model
+    T(C) = a + T_comm / C + beta C fitted to the scheduled times."""
+    q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
+    out = torch.empty_like(q)
+    ws = ctx.workspaces(w.S, w.H, w.d, q.dtype)
+    counts = list(range(1, w.H + 1))
+    modes = ["serial", "pipelined", "auto"]
+    med = {m: [] for m in modes}
+    t_comm, t_attn = [], []
+    for C in counts:
+        sizes = hcms.default_chunks(w.H, C)
+
+        def run(m):
+            ctx.forward(q, k, v, w.P, w.scale, sizes, mode=MODES[m], out=out, workspaces=ws)
+
+        times = {m: [] for m in modes}
+        for r in range(reps + 1):
+            for m in (modes if r % 2 == 0 else modes[::-1]):
+                t = time_region(lambda: run(m), 1)
+                if r > 0:
+                    times[m] += t
+        for m in modes:
+            med[m].append(float(np.median(times[m])))
+        ctx.set_timing(1)
+        run("serial")
+        torch.cuda.synchronize()
+        t_comm.append(sum(ctx.kernel_ms(hcms.OP_PACK)) + sum(ctx.kernel_ms(hcms.OP_UNPACK)))
+        t_attn.append(sum(ctx.kernel_ms(hcms.OP_ATTENTION)))
+        ctx.set_timing(0)
+    res = {"workload": w.name, "chunk_counts": counts,
+           "serial_ms": [round(x, 4) for x in med["serial"]],
+           "pipelined_ms": [round(x, 4) for x in med["pipelined"]],
+           "auto_ms": [round(x, 4) for x in med["auto"]],
+           "layout_kernels_ms": [round(x, 4) for x in t_comm],
+           "attention_kernels_ms": [round(x, 4) for x in t_attn]}
+    for m in ("pipelined", "auto"):
+        a, tc, beta = hcms.model_fit(counts, med[m])
+        pred = [a + tc / c + beta * c for c in counts]
+        err = max(abs(p_ - t) / t for p_, t in zip(pred, med[m]))
+        best_model, c_star = (hcms.model_optimal_chunks(tc, beta, w.H)
+                              if tc >= 0 and beta >= 0 else (None, None))
+        res["fit_" + m] = {
+            "a_ms": round(a, 4), "t_comm_ms": round(tc, 4), "beta_ms": round(beta, 4),
+            "c_star": None if c_star is None or not math.isfinite(c_star) else round(c_star, 3),
+            "best_c_model": best_model,
+            "best_c_measured": counts[int(np.argmin(med[m]))],
+            "max_rel_error": round(err, 5)}
     del q, k, v, out
     return res
 
@@ -336,6 +391,10 @@ def main():
         for ch in ((5, 5), (10,)):
             cmp.append(compare_modes(ctx, wp4, ch, reps, dev))
         result["schedules"] = cmp
+
+        # ---- the time model over the chunk count (Wan-P8, Wan-P4) ----
+        result["time_model"] = [time_model_sweep(ctx, tw, reps, dev)
+                                for tw in dict.fromkeys((w, wp4))]
 
     if not args.no_cpu:
         log("timing the oracle on the host ...")

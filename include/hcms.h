@@ -212,6 +212,34 @@ HCMS_API int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap);
  */
 HCMS_API int hcms_auto_mode(int S, int d, const int *chunk_sizes, int n_chunks, int n_cu);
 
+/*
+ * Time model of HCMS (Sec. 3.7, Theorem of the optimal chunk count; appendix
+ * equations of the HCMS time, the optimal chunk count and the speedup).
+ * Host only; times in any one unit.
+ *
+ * hcms_model_time: T_hcms(C) = t0 + t_comm / C + t_attn + C * beta, the time
+ *   of C chunks with fixed overhead t0 (projections), communication t_comm
+ *   (here: the layout kernels), attention t_attn and per-chunk overhead beta.
+ *   Errors: NULL, CHUNKS (C < 1), ARG (a time negative or not finite).
+ * hcms_model_optimal_chunks: returns the integer C in [1, H] that minimises
+ *   T_hcms (one of the two integers around C* = sqrt(t_comm / beta); ties go to
+ *   fewer chunks; beta = 0 gives H) and writes C* itself to *c_real_out unless
+ *   it is NULL.  Errors: SHAPE (H < 1), ARG.
+ * hcms_model_speedup: S(C) = 1 / (1 - rho (C - 1) / C + C beta / T_total)
+ *   with rho = t_comm / T_total in [0, 1].  Errors: NULL, CHUNKS, ARG (rho out
+ *   of range, beta / T_total < 0, or a non-positive model time).
+ * hcms_model_fit: least-squares fit of T(C) = a + t_comm / C + beta C to n >= 3
+ *   measured (chunk count, time) pairs, giving a = t0 + t_attn.  Errors: NULL,
+ *   CHUNKS (a count < 1), ARG (n < 3, a time not finite, or fewer than three
+ *   distinct counts).
+ */
+HCMS_API int hcms_model_time(double t0, double t_comm, double t_attn, double beta, int n_chunks,
+                             double *t_out);
+HCMS_API int hcms_model_optimal_chunks(double t_comm, double beta, int H, double *c_real_out);
+HCMS_API int hcms_model_speedup(double rho, double beta_over_total, int n_chunks, double *s_out);
+HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n, double *a_out,
+                            double *t_comm_out, double *beta_out);
+
 typedef struct hcms_ctx hcms_ctx;
 
 /*

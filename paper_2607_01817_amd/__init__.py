@@ -54,8 +54,9 @@ def load():
         raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                            "`python -m paper_2607_01817_amd.build` (no CPU fallback exists)")
     lib = ctypes.CDLL(LIB_PATH)
-    i, vp, f = ctypes.c_int, ctypes.c_void_p, ctypes.c_float
+    i, vp, f, d = ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_double
     ip = ctypes.POINTER(ctypes.c_int)
+    dp = ctypes.POINTER(ctypes.c_double)
     sig = {
         "hcms_abi_version": ([], i),
         "hcms_status_string": ([i], ctypes.c_char_p),
@@ -67,6 +68,10 @@ def load():
         "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
         "hcms_auto_mode": ([i, i, ip, i, i], i),
         "hcms_ctx_last_mode": ([vp], i),
+        "hcms_model_time": ([d, d, d, d, i, dp], i),
+        "hcms_model_optimal_chunks": ([d, d, i, dp], i),
+        "hcms_model_speedup": ([d, d, i, dp], i),
+        "hcms_model_fit": ([ip, dp, i, dp, dp, dp], i),
         "hcms_ctx_num_cu": ([vp], i),
         "hcms_ctx_create": ([i, i, ctypes.POINTER(vp)], i),
         "hcms_ctx_destroy": ([vp], i),
@@ -139,6 +144,35 @@ def auto_mode(S: int, d: int, chunk_sizes, n_cu: int) -> int:
     """The plan mode MODE_AUTO runs for these chunks on n_cu compute units."""
     sizes, n = _ints(chunk_sizes)
     return _check(load().hcms_auto_mode(S, d, sizes, n, n_cu))
+
+
+def model_time(t0: float, t_comm: float, t_attn: float, beta: float, n_chunks: int) -> float:
+    """T_hcms(C) of the paper's time model."""
+    out = ctypes.c_double()
+    _check(load().hcms_model_time(t0, t_comm, t_attn, beta, n_chunks, ctypes.byref(out)))
+    return out.value
+
+
+def model_optimal_chunks(t_comm: float, beta: float, H: int) -> tuple[int, float]:
+    """(best integer chunk count in [1, H], C* = sqrt(t_comm / beta))."""
+    c_real = ctypes.c_double()
+    best = _check(load().hcms_model_optimal_chunks(t_comm, beta, H, ctypes.byref(c_real)))
+    return best, c_real.value
+
+
+def model_speedup(rho: float, beta_over_total: float, n_chunks: int) -> float:
+    out = ctypes.c_double()
+    _check(load().hcms_model_speedup(rho, beta_over_total, n_chunks, ctypes.byref(out)))
+    return out.value
+
+
+def model_fit(chunk_counts, times) -> tuple[float, float, float]:
+    """(a = t0 + t_attn, t_comm, beta) fitted to measured (C, time) pairs."""
+    cs, n = _ints(chunk_counts)
+    ts = (ctypes.c_double * max(1, len(times)))(*[float(t) for t in times])
+    a, tc, b = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(load().hcms_model_fit(cs, ts, n, ctypes.byref(a), ctypes.byref(tc), ctypes.byref(b)))
+    return a.value, tc.value, b.value
 
 
 def pack(src_seq: torch.Tensor, P: int, h_begin: int, h_count: int,

@@ -14,9 +14,11 @@
 
 #include "hcms_internal.h"
 
-namespace {
+namespace hcms {
 
+namespace {
 thread_local char g_last_error[512] = "";
+}  // namespace
 
 int fail(int status, const char *fmt, ...) {
     va_list ap;
@@ -30,6 +32,15 @@ int ok() {
     g_last_error[0] = '\0';
     return HCMS_OK;
 }
+
+const char *last_error() { return g_last_error; }
+
+}  // namespace hcms
+
+namespace {
+
+using hcms::fail;
+using hcms::ok;
 
 int hip_fail(hipError_t e, const char *what) {
     return fail(HCMS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -320,7 +331,7 @@ const char *hcms_status_string(int status) {
     }
 }
 
-const char *hcms_last_error(void) { return g_last_error; }
+const char *hcms_last_error(void) { return hcms::last_error(); }
 
 int hcms_default_chunks(int H, int C, int *sizes_out) {
     if (!sizes_out) return fail(HCMS_ERR_NULL, "sizes_out is NULL");

@@ -7,6 +7,12 @@
 
 namespace hcms {
 
+// Thread-local error detail behind hcms_last_error: fail() records a message
+// and returns `status`, ok() clears it and returns HCMS_OK.
+int fail(int status, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int ok();
+const char *last_error();
+
 // Copy `n_tensors` (1..3) head chunks at once.  Each tensor z moves
 //   dst[z][j][t][:] = src[z][t][h0 + j][:]   (pack)
 // for t < S, j < hc, where a row ([:]) is 16 << log2_units bytes.
