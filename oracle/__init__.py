@@ -17,6 +17,9 @@ Contents, each a plain statement of what the paper defines:
   share of the input/output all-to-all (Sec. 3.1, Sec. 3.3 split equation,
   Alg. 1 SplitByHeads / Concat), as explicit index loops in C.
 * :func:`forward`          unpack o attention o pack over every chunk.
+* :func:`attention_backward_head`  the gradient of one head's attention with
+  respect to Q, K and V for a given output gradient, by the chain rule through
+  the row softmax, in C (``hcms_oracle.c``).
 
 Every function here is pinned by tests in ``tests/test_oracle.py`` against
 values the paper prints (the uneven-partition table), closed forms, invariants
@@ -60,6 +63,9 @@ def _load():
     for fn in (lib.oracle_pack, lib.oracle_unpack):
         fn.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, i64]
         fn.restype = ctypes.c_int
+    lib.oracle_attention_backward.argtypes = [vp, vp, vp, vp, i64, i64, dp, vp, i64, vp, i64,
+                                              vp, vp, vp]
+    lib.oracle_attention_backward.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -137,6 +143,37 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
     if rows is None:
         return np.stack([attention_head(q[h], k[h], v[h], scale) for h in range(H)])
     return [attention_head(q[h], k[h], v[h], scale, rows[h]) for h in range(H)]
+
+
+def attention_backward_head(q: np.ndarray, k: np.ndarray, v: np.ndarray, g: np.ndarray,
+                            scale: float, q_rows=None, k_rows=None):
+    """Gradients of one head's attention for output gradient ``g``.
+
+    ``q``, ``k``, ``v``, ``g`` are ``[S][d]``.  Returns ``(dq, dk, dv)``:
+    ``dq`` for the query indices ``q_rows`` (default all), ``dk`` and ``dv``
+    for the key indices ``k_rows`` (default all), each ``[n][d]`` fp64.
+    """
+    q, k, v, g = (np.ascontiguousarray(x, dtype=np.float64) for x in (q, k, v, g))
+    if not (q.shape == k.shape == v.shape == g.shape) or q.ndim != 2:
+        raise ValueError("q, k, v, g must all be [S][d]")
+    S, d = q.shape
+    qr = np.arange(S, dtype=np.int64) if q_rows is None else np.ascontiguousarray(q_rows, np.int64)
+    kr = np.arange(S, dtype=np.int64) if k_rows is None else np.ascontiguousarray(k_rows, np.int64)
+    for r in (qr, kr):
+        if r.size and (r.min() < 0 or r.max() >= S):
+            raise ValueError("row index out of range")
+    if np.unique(qr).size != qr.size:
+        raise ValueError("q_rows must be distinct")
+    dq = np.zeros((qr.size, d))
+    dk = np.zeros((kr.size, d))
+    dv = np.zeros((kr.size, d))
+    rc = _load().oracle_attention_backward(
+        q.ctypes.data, k.ctypes.data, v.ctypes.data, g.ctypes.data, S, d, float(scale),
+        qr.ctypes.data, qr.size, kr.ctypes.data, kr.size,
+        dq.ctypes.data, dk.ctypes.data, dv.ctypes.data)
+    if rc != 0:
+        raise MemoryError("oracle scratch allocation failed")
+    return dq, dk, dv
 
 
 # ---------------------------------------------------------------------------

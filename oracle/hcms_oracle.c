@@ -26,6 +26,12 @@
  *   oracle_unpack          The inverse (output all-to-all + concatenation along
  *                          heads, Alg. 1): dst[p][s][h0+j][e] = src[j][p*(S/P)+s][e];
  *                          heads outside the chunk are left untouched.
+ *   oracle_attention_backward
+ *                          The gradient of that attention with respect to Q, K
+ *                          and V for a given output gradient (the training use
+ *                          of Sec. 4, correctness and training validation in
+ *                          the appendix), written as the chain rule through the
+ *                          softmax with full rows, no recomputation tricks.
  */
 #include <math.h>
 #include <stdint.h>
@@ -133,6 +139,115 @@ int oracle_unpack(const void *src, void *dst, int64_t P, int64_t S, int64_t H,
                     memcpy(dp + to * elem_bytes, sp + from * elem_bytes, (size_t)elem_bytes);
                 }
     return 0;
+}
+
+/*
+ * Backward of one head.  With g = dL/dO (the output gradient):
+ *   s_ij  = scale * <q_i, k_j>
+ *   p_ij  = exp(s_ij - m_i) / l_i,  m_i = max_j s_ij,  l_i = sum_j exp(s_ij - m_i)
+ *   dv_j  = sum_i p_ij g_i                      (O = P V)
+ *   dp_ij = <g_i, v_j>
+ *   ds_ij = p_ij (dp_ij - sum_k p_ik dp_ik)     (Jacobian of the row softmax)
+ *   dq_i  = scale * sum_j ds_ij k_j
+ *   dk_j  = scale * sum_i ds_ij q_i
+ *   q, k, v, g : [S][d] row-major fp64
+ *   q_rows     : n_q query indices whose dq is written to dq [n_q][d]
+ *   k_rows     : n_k key indices whose dk, dv are written to dk, dv [n_k][d]
+ * Pass 1 visits every query that a requested output needs (all of them when
+ * n_k > 0) and keeps m_i, l_i and c_i = sum_k p_ik dp_ik; pass 2 sums over
+ * all queries for each requested key.  Returns 0, or -1 if an allocation
+ * fails.
+ */
+int oracle_attention_backward(const double *q, const double *k, const double *v, const double *g,
+                              int64_t S, int64_t d, double scale,
+                              const int64_t *q_rows, int64_t n_q,
+                              const int64_t *k_rows, int64_t n_k,
+                              double *dq, double *dk, double *dv)
+{
+    double *m = (double *)malloc((size_t)S * sizeof(double));
+    double *l = (double *)malloc((size_t)S * sizeof(double));
+    double *cdp = (double *)malloc((size_t)S * sizeof(double));
+    int64_t *qpos = (int64_t *)malloc((size_t)S * sizeof(int64_t));
+    if (!m || !l || !cdp || !qpos) {
+        free(m); free(l); free(cdp); free(qpos);
+        return -1;
+    }
+    /* qpos[i]: where query i's dq goes, or -1 */
+    for (int64_t i = 0; i < S; ++i) qpos[i] = -1;
+    for (int64_t r = 0; r < n_q; ++r) qpos[q_rows[r]] = r;
+    int failed = 0;
+
+    /* pass 1: per query row */
+#pragma omp parallel
+    {
+        double *s = (double *)malloc((size_t)S * sizeof(double));
+        double *dp = (double *)malloc((size_t)S * sizeof(double));
+        if (!s || !dp) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t i = 0; i < S; ++i) {
+            if (!s || !dp) continue;
+            if (n_k == 0 && qpos[i] < 0) continue;
+            const double *qi = q + i * d, *gi = g + i * d;
+            double mi = -INFINITY;
+            for (int64_t j = 0; j < S; ++j) {
+                double dot = 0.0, dg = 0.0;
+                for (int64_t t = 0; t < d; ++t) {
+                    dot += qi[t] * k[j * d + t];
+                    dg += gi[t] * v[j * d + t];
+                }
+                s[j] = scale * dot;
+                dp[j] = dg;
+                if (s[j] > mi) mi = s[j];
+            }
+            double li = 0.0;
+            for (int64_t j = 0; j < S; ++j) li += exp(s[j] - mi);
+            double ci = 0.0;
+            for (int64_t j = 0; j < S; ++j) ci += exp(s[j] - mi) / li * dp[j];
+            m[i] = mi;
+            l[i] = li;
+            cdp[i] = ci;
+            if (qpos[i] >= 0) {
+                double *o = dq + qpos[i] * d;
+                for (int64_t t = 0; t < d; ++t) o[t] = 0.0;
+                for (int64_t j = 0; j < S; ++j) {
+                    const double ds = exp(s[j] - mi) / li * (dp[j] - ci);
+                    for (int64_t t = 0; t < d; ++t) o[t] += scale * ds * k[j * d + t];
+                }
+            }
+        }
+        free(s);
+        free(dp);
+    }
+
+    /* pass 2: per requested key row, summing over every query */
+    if (!failed) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t r = 0; r < n_k; ++r) {
+            const int64_t j = k_rows[r];
+            const double *kj = k + j * d, *vj = v + j * d;
+            double *okk = dk + r * d, *ov = dv + r * d;
+            for (int64_t t = 0; t < d; ++t) okk[t] = ov[t] = 0.0;
+            for (int64_t i = 0; i < S; ++i) {
+                const double *qi = q + i * d, *gi = g + i * d;
+                double dot = 0.0, dg = 0.0;
+                for (int64_t t = 0; t < d; ++t) {
+                    dot += qi[t] * kj[t];
+                    dg += gi[t] * vj[t];
+                }
+                const double p = exp(scale * dot - m[i]) / l[i];
+                const double ds = p * (dg - cdp[i]);
+                for (int64_t t = 0; t < d; ++t) {
+                    ov[t] += p * gi[t];
+                    okk[t] += scale * ds * qi[t];
+                }
+            }
+        }
+    }
+    free(m); free(l); free(cdp); free(qpos);
+    return failed ? -1 : 0;
 }
 
 /* Number of OpenMP threads the attention oracle runs on (for reporting). */
