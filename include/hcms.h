@@ -133,6 +133,45 @@ HCMS_API int hcms_attention(const void *q, const void *k, const void *v, void *o
                    int S, int H, int d, float scale,
                    const int *chunk_sizes, int n_chunks, int dtype, void *stream);
 
+/*
+ * Training forward: hcms_attention plus, per head h and query i, the log2 of
+ * the softmax denominator,
+ *   lse[h][i] = log2 sum_j exp2(c <Q[h][i], K[h][j]>),  c = scale * log2(e),
+ * the statistic the backward pass recomputes the weights from:
+ * P_ij = exp2(c <Q[h][i], K[h][j]> - lse[h][i]).
+ *   lse : device, [H][S] fp32, 4-byte aligned, disjoint from q, k, v, out
+ * out is bit-identical to hcms_attention's.  Errors: as hcms_attention, plus
+ * NULL, ALIGN and ALIAS for lse.
+ */
+HCMS_API int hcms_attention_lse(const void *q, const void *k, const void *v, void *out, float *lse,
+                                int S, int H, int d, float scale, const int *chunk_sizes,
+                                int n_chunks, int dtype, void *stream);
+
+/*
+ * Backward of head-chunked attention, for training (the forward's gradient
+ * through the row softmax; the appendix validates HCMS for training).  With
+ * s_ij = <Q[h][i], K[h][j]>, P_ij = exp2(c s_ij - lse[h][i]) (the forward's
+ * weights), D_i = <dO[h][i], O[h][i]>:
+ *   dV[h][j] = sum_i P_ij dO[h][i]
+ *   dQ[h][i] = scale sum_j P_ij (<dO[h][i], V[h][j]> - D_i) K[h][j]
+ *   dK[h][j] = scale sum_i P_ij (<dO[h][i], V[h][j]> - D_i) Q[h][i]
+ * Per chunk, in order on `stream`: one query-parallel launch (D into delta,
+ * then dq) and one key-parallel launch (dk, dv).  No atomics: deterministic,
+ * and the result does not depend on the chunking.  Operands are rounded to
+ * bf16 for the MFMAs (fp32 storage included), accumulation is fp32, dq, dk,
+ * dv are rounded to the storage type.
+ *   q, k, v, out : the forward's inputs and output, [H][S][d]
+ *   dout         : dL/dO, [H][S][d]
+ *   lse          : [H][S] fp32 from hcms_attention_lse on the same q, k, v, scale
+ *   dq, dk, dv   : outputs, [H][S][d], disjoint from every input and each other
+ *   delta        : [H][S] fp32 workspace (receives D)
+ * Errors: as hcms_attention, plus NULL, ALIGN and ALIAS for the added buffers.
+ */
+HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v, const void *out,
+                                     const void *dout, const float *lse, void *dq, void *dk,
+                                     void *dv, float *delta, int S, int H, int d, float scale,
+                                     const int *chunk_sizes, int n_chunks, int dtype, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Scheduler                                                                 */
 /* ------------------------------------------------------------------------ */

@@ -17,6 +17,8 @@ Contents, each a plain statement of what the paper defines:
   share of the input/output all-to-all (Sec. 3.1, Sec. 3.3 split equation,
   Alg. 1 SplitByHeads / Concat), as explicit index loops in C.
 * :func:`forward`          unpack o attention o pack over every chunk.
+* :func:`lse_head`         log2 of each query row's softmax denominator, the
+  statistic a training forward keeps for its backward pass.
 * :func:`attention_backward_head`  the gradient of one head's attention with
   respect to Q, K and V for a given output gradient, by the chain rule through
   the row softmax, in C (``hcms_oracle.c``).
@@ -143,6 +145,19 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
     if rows is None:
         return np.stack([attention_head(q[h], k[h], v[h], scale) for h in range(H)])
     return [attention_head(q[h], k[h], v[h], scale, rows[h]) for h in range(H)]
+
+
+def lse_head(q: np.ndarray, k: np.ndarray, scale: float, rows=None) -> np.ndarray:
+    """log2 of the softmax denominator of each listed query row:
+    ``log2 sum_j exp(scale * <q_i, k_j>)`` (= ``log2 sum_j exp2(c <q_i, k_j>)``
+    with ``c = scale * log2(e)``), fp64, with the row maximum taken out before
+    the exponentials."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    rows = np.arange(q.shape[0]) if rows is None else np.asarray(rows, dtype=np.int64)
+    s = scale * (q[rows] @ k.T)
+    m = s.max(axis=1)
+    return (m + np.log(np.exp(s - m[:, None]).sum(axis=1))) / np.log(2.0)
 
 
 def attention_backward_head(q: np.ndarray, k: np.ndarray, v: np.ndarray, g: np.ndarray,

@@ -65,6 +65,9 @@ def load():
         "hcms_pack": ([vp, vp, i, i, i, i, i, i, i, vp], i),
         "hcms_unpack": ([vp, vp, i, i, i, i, i, i, i, vp], i),
         "hcms_attention": ([vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
+        "hcms_attention_lse": ([vp, vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
+        "hcms_attention_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, f, ip, i, i,
+                                     vp], i),
         "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
         "hcms_auto_mode": ([i, i, ip, i, i], i),
         "hcms_ctx_last_mode": ([vp], i),
@@ -226,6 +229,64 @@ def attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float,
                                  S, H, d, float(scale), sizes, n, _dtype(q), _stream(stream)))
     return out
 
+
+
+def _same_hm(ts, names, like):
+    _dev(like, "q")
+    if like.dim() != 3:
+        raise ValueError("q must be [H][S][d]")
+    for t, n in zip(ts, names):
+        _dev(t, n)
+        if t.shape != like.shape or t.dtype != like.dtype:
+            raise ValueError(f"{n} must match q ([H][S][d], same dtype)")
+
+
+def _stats(t, name, H, S, device):
+    if t is None:
+        return torch.empty((H, S), dtype=torch.float32, device=device)
+    _dev(t, name)
+    if t.dtype != torch.float32 or t.shape != (H, S):
+        raise ValueError(f"{name} must be float32 [H][S]")
+    return t
+
+
+def attention_lse(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float,
+                  chunk_sizes=None, out: torch.Tensor | None = None,
+                  lse: torch.Tensor | None = None, stream=None):
+    """Training forward: ``(out, lse)`` with ``lse[h][i]`` the log2 softmax
+    denominator of ``scale * log2(e) * <q_i, k_j>`` (see hcms.h)."""
+    _same_hm((k, v), ("k", "v"), q)
+    H, S, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _same_hm((out,), ("out",), q)
+    lse = _stats(lse, "lse", H, S, q.device)
+    sizes, n = _ints(chunk_sizes if chunk_sizes is not None else [H])
+    _check(load().hcms_attention_lse(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                     lse.data_ptr(), S, H, d, float(scale), sizes, n, _dtype(q),
+                                     _stream(stream)))
+    return out, lse
+
+
+def attention_backward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
+                       dout: torch.Tensor, lse: torch.Tensor, scale: float, chunk_sizes=None,
+                       dq=None, dk=None, dv=None, delta=None, stream=None):
+    """``(dq, dk, dv)`` of head-major attention for output gradient ``dout``;
+    ``lse`` comes from :func:`attention_lse` on the same inputs."""
+    _same_hm((k, v, out, dout), ("k", "v", "out", "dout"), q)
+    H, S, d = q.shape
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    _same_hm((dq, dk, dv), ("dq", "dk", "dv"), q)
+    lse = _stats(lse, "lse", H, S, q.device)
+    delta = _stats(delta, "delta", H, S, q.device)
+    sizes, n = _ints(chunk_sizes if chunk_sizes is not None else [H])
+    _check(load().hcms_attention_backward(
+        q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta.data_ptr(), S, H, d, float(scale),
+        sizes, n, _dtype(q), _stream(stream)))
+    return dq, dk, dv
 
 class Context:
     """The chunk scheduler (Alg. 1 and its one-GPU schedules) on one device.

@@ -298,6 +298,48 @@ struct DeviceGuard {
 
 }  // namespace
 
+namespace {
+
+float scale_log2e(float scale) {
+    return static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+}
+
+// One attention launch per chunk, in order, on `stream`; lse (optional) is
+// [H][S] fp32 and advances with the chunk's first head.
+int run_attention(const void *q, const void *k, const void *v, void *out, float *lse, int S, int d,
+                  float scale, const int *chunk_sizes, int n_chunks, int dtype, hipStream_t stream) {
+    const int64_t head = static_cast<int64_t>(S) * d * elem_bytes(dtype);
+    const float c = scale_log2e(scale);
+    int h0 = 0;
+    for (int i = 0; i < n_chunks; ++i) {
+        const int64_t off = head * h0;
+        const hipError_t e = hcms::launch_attention(
+            static_cast<const char *>(q) + off, static_cast<const char *>(k) + off,
+            static_cast<const char *>(v) + off, static_cast<char *>(out) + off,
+            lse ? lse + static_cast<int64_t>(h0) * S : nullptr, S, chunk_sizes[i], d, c, dtype, stream);
+        if (e != hipSuccess) return hip_fail(e, "attention launch");
+        h0 += chunk_sizes[i];
+    }
+    return ok();
+}
+
+// A [H][S] fp32 statistics buffer: non-NULL unless S = 0, 4-byte aligned, and
+// disjoint from the four [H][S][d] tensors.
+int check_stats(const float *p, const char *name, int S, int H, const void *a, const void *b,
+                const void *c, const void *d_, int d, int dtype) {
+    if (S == 0) return HCMS_OK;
+    if (!p) return fail(HCMS_ERR_NULL, "%s is NULL", name);
+    if ((reinterpret_cast<uintptr_t>(p) & 3u) != 0)
+        return fail(HCMS_ERR_ALIGN, "%s must be 4-byte aligned", name);
+    const int64_t sb = static_cast<int64_t>(S) * H * 4;
+    const int64_t tb = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
+    for (const void *t : {a, b, c, d_})
+        if (overlaps(p, sb, t, tb)) return fail(HCMS_ERR_ALIAS, "%s overlaps a tensor", name);
+    return HCMS_OK;
+}
+
+}  // namespace
+
 struct hcms_ctx {
     int device = 0;
     int max_chunks = 0;
@@ -382,24 +424,63 @@ static int check_attention_args(const void *q, const void *k, const void *v, con
     return HCMS_OK;
 }
 
-static float scale_log2e(float scale) {
-    return static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
-}
-
 int hcms_attention(const void *q, const void *k, const void *v, void *out, int S, int H, int d,
                    float scale, const int *chunk_sizes, int n_chunks, int dtype, void *stream) {
     const int st = check_attention_args(q, k, v, out, S, H, d, scale, chunk_sizes, n_chunks, dtype);
     if (st != HCMS_OK) return st;
+    return run_attention(q, k, v, out, nullptr, S, d, scale, chunk_sizes, n_chunks, dtype,
+                         static_cast<hipStream_t>(stream));
+}
+
+int hcms_attention_lse(const void *q, const void *k, const void *v, void *out, float *lse, int S,
+                       int H, int d, float scale, const int *chunk_sizes, int n_chunks, int dtype,
+                       void *stream) {
+    int st = check_attention_args(q, k, v, out, S, H, d, scale, chunk_sizes, n_chunks, dtype);
+    if (st != HCMS_OK) return st;
+    if ((st = check_stats(lse, "lse", S, H, q, k, v, out, d, dtype)) != HCMS_OK) return st;
+    return run_attention(q, k, v, out, lse, S, d, scale, chunk_sizes, n_chunks, dtype,
+                         static_cast<hipStream_t>(stream));
+}
+
+int hcms_attention_backward(const void *q, const void *k, const void *v, const void *out,
+                            const void *dout, const float *lse, void *dq, void *dk, void *dv,
+                            float *delta, int S, int H, int d, float scale,
+                            const int *chunk_sizes, int n_chunks, int dtype, void *stream) {
+    int st = check_attention_args(q, k, v, out, S, H, d, scale, chunk_sizes, n_chunks, dtype);
+    if (st != HCMS_OK) return st;
+    if (S > 0 && (!dout || !dq || !dk || !dv)) return fail(HCMS_ERR_NULL, "a gradient tensor is NULL");
+    for (const void *p : {dout, static_cast<const void *>(dq), static_cast<const void *>(dk),
+                          static_cast<const void *>(dv)})
+        if (S > 0 && !aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
+    // Outputs are disjoint from every input and from each other.
+    const void *ins[5] = {q, k, v, out, dout};
+    void *outs[3] = {dq, dk, dv};
+    for (int i = 0; i < 3; ++i) {
+        for (const void *x : ins)
+            if (overlaps(outs[i], bytes, x, bytes))
+                return fail(HCMS_ERR_ALIAS, "gradient %d overlaps an input", i);
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i], bytes, outs[j], bytes))
+                return fail(HCMS_ERR_ALIAS, "gradients %d and %d overlap", i, j);
+    }
+    if ((st = check_stats(lse, "lse", S, H, dq, dk, dv, dout, d, dtype)) != HCMS_OK) return st;
+    if ((st = check_stats(delta, "delta", S, H, dq, dk, dv, dout, d, dtype)) != HCMS_OK) return st;
+    if ((st = check_stats(delta, "delta", S, H, q, k, v, out, d, dtype)) != HCMS_OK) return st;
+    if (S > 0 && overlaps(lse, int64_t{S} * H * 4, delta, int64_t{S} * H * 4))
+        return fail(HCMS_ERR_ALIAS, "lse and delta overlap");
+    if (S == 0) return ok();
     const int64_t head = static_cast<int64_t>(S) * d * elem_bytes(dtype);
-    const float c = scale_log2e(scale);
     int h0 = 0;
     for (int i = 0; i < n_chunks; ++i) {
         const int64_t off = head * h0;
-        const hipError_t e = hcms::launch_attention(
-            static_cast<const char *>(q) + off, static_cast<const char *>(k) + off,
-            static_cast<const char *>(v) + off, static_cast<char *>(out) + off, S, chunk_sizes[i], d,
-            c, dtype, static_cast<hipStream_t>(stream));
-        if (e != hipSuccess) return hip_fail(e, "attention launch");
+        const int64_t soff = static_cast<int64_t>(h0) * S;
+        auto at = [off](const void *p) { return static_cast<const char *>(p) + off; };
+        auto atw = [off](void *p) { return static_cast<char *>(p) + off; };
+        const hipError_t e = hcms::launch_attention_backward(
+            at(q), at(k), at(v), at(out), at(dout), lse + soff, atw(dq), atw(dk), atw(dv),
+            delta + soff, S, chunk_sizes[i], d, scale, dtype, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "attention backward launch");
         h0 += chunk_sizes[i];
     }
     return ok();
@@ -653,7 +734,7 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
         } else if (op.kind == HCMS_OP_ATTENTION) {
             e = hcms::launch_attention(static_cast<char *>(q_hm) + off, static_cast<char *>(k_hm) + off,
                                        static_cast<char *>(v_hm) + off, static_cast<char *>(o_hm) + off,
-                                       S, hc, d, c_log2e, dtype, s);
+                                       nullptr, S, hc, d, c_log2e, dtype, s);
         } else {
             e = hcms::launch_unpack(static_cast<char *>(o_hm) + off, o_seq, S, H, offs[c], hc, log2u, s);
         }

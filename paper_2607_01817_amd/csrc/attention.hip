@@ -53,131 +53,13 @@
 // Tails: loads go through buffer resources bounded by the head's tensor, so
 // query and key rows >= S read as zeros; such queries are not stored and such
 // keys get score -inf in the last block only.
+#include "attention_tiles.h"
 #include "hcms_internal.h"
 
 namespace hcms {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kQW = 32;              // queries per wave (one 32-wide MFMA tile)
-constexpr int kBC = 64;              // keys per block
-constexpr float kRescaleThreshold = 8.0f;  // log2 of the largest tolerated exp
-
-// Buffer resource over one head's [S][D] tensor: loads past its end return 0,
-// which is how the query and key tails are read without branches.
-__device__ inline __amdgpu_buffer_rsrc_t head_rsrc(const void *base, int64_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0,
-                                             static_cast<int>(bytes), 0x00020000);
-}
-
-// 8 consecutive elements at byte offset `off` as bf16 (fp32 storage is rounded
-// to nearest-even), returned as raw 32-bit words.
-template <typename T>
-__device__ inline u32x4 load8(__amdgpu_buffer_rsrc_t r, unsigned off);
-
-template <>
-__device__ inline u32x4 load8<__bf16>(__amdgpu_buffer_rsrc_t r, unsigned off) {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-}
-
-// The two loads are reinterpreted as whole float vectors before the
-// conversion: converting lane-wise bit casts of u32 vector elements to bf16
-// miscompiles with this toolchain (elements are dropped).
-template <>
-__device__ inline u32x4 load8<float>(__amdgpu_buffer_rsrc_t r, unsigned off) {
-    const f32x4 a = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-    const f32x4 b = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0));
-    const f32x8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-    return __builtin_bit_cast(u32x4, __builtin_convertvector(x, bf16x8));
-}
-
-__device__ inline void store4(__bf16 *p, f32x4 x) {
-    *reinterpret_cast<bf16x4 *>(p) = __builtin_convertvector(x, bf16x4);
-}
-__device__ inline void store4(float *p, f32x4 x) { *reinterpret_cast<f32x4 *>(p) = x; }
-
-// Position of key `k` (0..63) inside a transposed V row: bits 2 and 3 swapped.
-__device__ inline int vt_pos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
-
-// LDS tiles are padded by 16 bytes per row: K is [kBC][D + 8] and V^T is
-// [D][kBC + 8] (bf16 elements).  With rows of 272 (K, D = 128) or 144 bytes the
-// 16-byte operand reads of 16 consecutive rows land on 16 disjoint groups of 4
-// banks, and every LDS address is one per-lane base plus an immediate offset.
-template <int D>
-struct Lds {
-    static constexpr int KS = D + 8;      // K row stride (elements)
-    static constexpr int VS = kBC + 8;    // V^T row stride (elements)
-    static constexpr int KT = kBC * KS;   // K tile size (elements)
-    static constexpr int VT = D * VS;     // V^T tile size (elements)
-};
-
-// Global -> register -> LDS staging of one K block and one V block.
-template <int D, typename T, int WAVES>
-struct Stage {
-    static constexpr int kThreads = 64 * WAVES;
-    static constexpr int CH = D / 8;                        // 16-byte bf16 chunks per row
-    static constexpr unsigned ROWB = D * sizeof(T);          // bytes per stored row
-    static constexpr unsigned CHB = 8 * sizeof(T);           // bytes per stored chunk
-    static constexpr int KPASS = kBC * CH / kThreads;       // K chunks per thread
-    static constexpr int VTASK = (kBC / 2) * CH / kThreads; // V (key pair, chunk) tasks
-    static_assert(KPASS >= 1 && VTASK >= 1, "tile too small for the workgroup");
-
-    u32x4 kreg[KPASS];
-    u32x4 vreg[VTASK][2];
-
-    // K: thread -> (row, chunk), CH threads cover a row.
-    __device__ static int k_row(int p, int tid) { return p * (kThreads / CH) + tid / CH; }
-    __device__ static int k_chunk(int tid) { return tid % CH; }
-    // V: a wave covers 16 key pairs x 4 chunks; key pair kp = keys 2kp, 2kp + 1.
-    __device__ static int v_pair(int task) { return ((task >> 6) & 1) * 16 + (task & 15); }
-    __device__ static int v_chunk(int task) { return (task >> 7) * 4 + ((task >> 4) & 3); }
-
-    // Offsets stay below 2^32: a head is at most 2^31 - 1 bytes and blocks past
-    // its end are at most three blocks away.
-    __device__ void load(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int kblk, int vblk,
-                         int tid) {
-        const unsigned key0 = static_cast<unsigned>(kblk) * kBC;
-#pragma unroll
-        for (int p = 0; p < KPASS; ++p)
-            kreg[p] = load8<T>(kr, (key0 + k_row(p, tid)) * ROWB + k_chunk(tid) * CHB);
-        const unsigned vkey0 = static_cast<unsigned>(vblk) * kBC;
-#pragma unroll
-        for (int i = 0; i < VTASK; ++i) {
-            const int task = tid + i * kThreads;
-            const unsigned off = (vkey0 + 2 * v_pair(task)) * ROWB + v_chunk(task) * CHB;
-            vreg[i][0] = load8<T>(vr, off);
-            vreg[i][1] = load8<T>(vr, off + ROWB);
-        }
-    }
-
-    __device__ void store_k(__bf16 *ks, int tid) const {
-#pragma unroll
-        for (int p = 0; p < KPASS; ++p)
-            *reinterpret_cast<u32x4 *>(ks + k_row(p, tid) * Lds<D>::KS + k_chunk(tid) * 8) = kreg[p];
-    }
-
-    __device__ void store_v(__bf16 *vts, int tid) const {
-#pragma unroll
-        for (int i = 0; i < VTASK; ++i) {
-            const int task = tid + i * kThreads;
-            __bf16 *dst = vts + v_chunk(task) * 8 * Lds<D>::VS + vt_pos(2 * v_pair(task));
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                // (V[2kp][e], V[2kp+1][e]) as one 32-bit word of V^T row 8 chunk + e.
-                const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
-                *reinterpret_cast<unsigned *>(dst + e * Lds<D>::VS) =
-                    __builtin_amdgcn_perm(vreg[i][1][e >> 1], vreg[i][0][e >> 1], sel);
-            }
-        }
-    }
-};
+using namespace tiles;
 
 // S^T[mt] = K[mt] Q^T for the 64 keys of a block (2 tiles of 32 keys); the
 // K operands are read from LDS four MFMAs ahead of their use.
@@ -274,7 +156,7 @@ __device__ inline float softmax_block(f32x16 (&sacc)[2], float &m_used, float &l
 template <int D, typename T, int WAVES>
 __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v, T *__restrict__ o,
-    int S, int n_qtiles, float c) {
+    float *__restrict__ lse, int S, int n_qtiles, float c) {
     constexpr int KK = D / 16;  // MFMA k-steps over the head dimension
     constexpr int DT = D / 32;  // 32-row tiles of O^T
     __shared__ __attribute__((aligned(16))) __bf16 kbuf[2][Lds<D>::KT];
@@ -386,6 +268,10 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
             __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
     }
     const float inv = 1.0f / l;
+    // log2 of the softmax denominator of c * s: P_ij = exp2(c s_ij - L2_i)
+    // (the statistic the backward pass recomputes P from).
+    if (lse != nullptr && g == 0 && qi < S)
+        lse[static_cast<int64_t>(head) * S + qi] = m_used * c + __builtin_amdgcn_logf(l);
     if (qi < S) {
         T *orow = oh + static_cast<int64_t>(qi) * D;
 #pragma unroll
@@ -407,8 +293,8 @@ struct Waves {
 };
 
 template <int D, typename T>
-hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, int S, int n_heads,
-                        float c, hipStream_t stream) {
+hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, float *lse, int S,
+                        int n_heads, float c, hipStream_t stream) {
     constexpr int WAVES = Waves<D>::value;
     constexpr int BR = kQW * WAVES;
     const int n_qtiles = (S + BR - 1) / BR;
@@ -416,7 +302,7 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, in
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     attention_kernel<D, T, WAVES><<<static_cast<unsigned>(blocks), 64 * WAVES, 0, stream>>>(
         static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
-        static_cast<T *>(o), S, n_qtiles, c);
+        static_cast<T *>(o), lse, S, n_qtiles, c);
     return hipGetLastError();
 }
 
@@ -425,17 +311,17 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, in
 int attention_queries_per_block(int d) { return kQW * (d == 128 ? Waves<128>::value : Waves<64>::value); }
 int attention_blocks_per_cu(int d) { return 8 / (d == 128 ? Waves<128>::value : Waves<64>::value); }
 
-hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, int S,
+hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, float *lse, int S,
                             int n_heads, int d, float scale_log2e, int dtype, hipStream_t stream) {
     if (S == 0 || n_heads == 0) return hipSuccess;
     if (d == 128 && dtype == 0)
-        return launch_typed<128, __bf16>(q, k, v, o, S, n_heads, scale_log2e, stream);
+        return launch_typed<128, __bf16>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
     if (d == 64 && dtype == 0)
-        return launch_typed<64, __bf16>(q, k, v, o, S, n_heads, scale_log2e, stream);
+        return launch_typed<64, __bf16>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
     if (d == 128 && dtype == 1)
-        return launch_typed<128, float>(q, k, v, o, S, n_heads, scale_log2e, stream);
+        return launch_typed<128, float>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
     if (d == 64 && dtype == 1)
-        return launch_typed<64, float>(q, k, v, o, S, n_heads, scale_log2e, stream);
+        return launch_typed<64, float>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
     return hipErrorInvalidValue;
 }
 

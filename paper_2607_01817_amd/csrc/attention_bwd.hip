@@ -1,0 +1,429 @@
+// Backward of the non-causal softmax attention, for gfx950 (bf16 MFMA).
+//
+// For one head, with s_ij = <q_i, k_j>, c = scale * log2(e), the forward's
+// statistic L_i = log2 sum_j exp2(c s_ij) and the output gradient dO:
+//   P_ij  = exp2(c s_ij - L_i)                       (softmax weights)
+//   D_i   = <dO_i, O_i>          (= sum_j P_ij dP_ij, since O_i = sum_j P_ij v_j)
+//   dP_ij = <dO_i, v_j>
+//   dS_ij = P_ij (dP_ij - D_i)                       (gradient of scale * s_ij)
+//   dQ_i  = scale sum_j dS_ij k_j
+//   dK_j  = scale sum_i dS_ij q_i
+//   dV_j  = sum_i P_ij dO_i
+// the chain rule through the row softmax of the attention step of Alg. 1
+// (Sec. 3.3 Property), used for training (the appendix's correctness and
+// training validation).
+//
+// Two launches per head chunk, no atomics, so the result is deterministic and
+// does not depend on the chunking:
+//   * attention_dq_kernel, query-parallel (the forward's decomposition): a
+//     wave owns 32 queries, keeps Q and dO as MFMA B operands in registers and
+//     walks the key blocks.  Per block, S^T = K Q^T and dP^T = V dO^T (K and V
+//     row-major in LDS), then dS, then dQ^T += K^T dS^T with K^T stored
+//     transposed in LDS, keys permuted like V^T in the forward so that dS
+//     leaves the accumulator layout directly as the B operand.  Its prologue
+//     computes D_i from dO and O and stores it for the second launch.
+//   * attention_dkdv_kernel, key-parallel: a wave owns 32 keys, keeps K and V
+//     as B operands, and walks blocks of 32 queries.  Per block, S = Q K^T and
+//     dP = dO V^T put one key per lane (the column) and 16 queries per lane
+//     (rows), so P and dS are already B operands of dV^T += dO^T P and
+//     dK^T += Q^T dS, with dO^T and Q^T transposed in LDS, queries permuted.
+// Both hold four waves per workgroup, one per SIMD: the register sets
+// (Q, dO, dQ^T, S^T, dP^T; or K, V, dK^T, dV^T, S, dP, the per-row L and D)
+// need more than the 256 registers two waves per SIMD would leave.
+//
+// Tails: loads go through buffer resources bounded by the head's tensor (rows
+// >= S read as zeros); keys or queries past S get P = 0 and are not stored.
+#include "attention_tiles.h"
+#include "hcms_internal.h"
+
+namespace hcms {
+namespace {
+
+using namespace tiles;
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kQB = 32;  // queries per block of the key-parallel kernel
+
+// Transposed tiles of 32 queries: [D][kQB + 8], the same 16-byte padding as
+// the forward's V^T (rows of 80 bytes: 16 consecutive rows hit disjoint banks).
+template <int D>
+struct QLds {
+    static constexpr int RS = D + 8;        // row-major row stride (elements)
+    static constexpr int TS = kQB + 8;      // transposed row stride (elements)
+    static constexpr int R = kQB * RS;      // row-major tile (elements)
+    static constexpr int TT = D * TS;       // transposed tile (elements)
+};
+
+__device__ inline unsigned bits(float x) { return __builtin_bit_cast(unsigned, x); }
+__device__ inline float swap_halves_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(bits(x), bits(x), false, false);
+    return __builtin_bit_cast(float, static_cast<unsigned>(r[0])) +
+           __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
+}
+
+// XCD-aware order: workgroup b runs on XCD b % 8; each XCD takes a contiguous
+// range of (head, tile) pairs.
+__device__ inline int xcd_logical(int b, int nb) {
+    const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
+    return xcd * per + min(xcd, rem) + (b >> 3);
+}
+
+// A 32 x 32 product over the head dimension: acc = A B^T with A rows from an
+// LDS tile (row-major, stride RS) and B held as the D/16 register operands.
+template <int D>
+__device__ inline f32x16 rows_times_regs(const __bf16 *a, int rs, const bf16x8 (&b)[D / 16], int li,
+                                          int g) {
+    f32x16 acc = {};
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+        const bf16x8 x = *reinterpret_cast<const bf16x8 *>(a + li * rs + kk * 16 + g * 8);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, b[kk], acc, 0, 0, 0);
+    }
+    return acc;
+}
+
+// ---------------------------------------------------------------------------
+// dQ (and D): query-parallel
+// ---------------------------------------------------------------------------
+template <int D, typename T>
+__global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+    const T *__restrict__ o, const T *__restrict__ dout, const float *__restrict__ lse,
+    T *__restrict__ dq, float *__restrict__ delta, int S, int n_qtiles, float c, float scale) {
+    constexpr int KK = D / 16, DT = D / 32;
+    __shared__ __attribute__((aligned(16))) __bf16 kbuf[2][Lds<D>::KT];   // K, row-major
+    __shared__ __attribute__((aligned(16))) __bf16 vbuf[2][Lds<D>::KT];   // V, row-major
+    __shared__ __attribute__((aligned(16))) __bf16 ktbuf[2][Lds<D>::VT];  // K^T, keys permuted
+
+    const int logical = xcd_logical(blockIdx.x, gridDim.x);
+    const int head = logical / n_qtiles;
+    const int qtile = logical - head * n_qtiles;
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * sizeof(T);
+    const __amdgpu_buffer_rsrc_t qr = head_rsrc(q + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t vr = head_rsrc(v + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t or_ = head_rsrc(o + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t dr = head_rsrc(dout + hoff, hbytes);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 31, g = lane >> 5;
+    const int qi = qtile * (kQW * kWaves) + wave * kQW + li;
+
+    bf16x8 qreg[KK], doreg[KK];
+    float dpart = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        const unsigned off = static_cast<unsigned>(qi * D + kk * 16 + g * 8) * sizeof(T);
+        qreg[kk] = __builtin_bit_cast(bf16x8, load8<T>(qr, off));
+        doreg[kk] = __builtin_bit_cast(bf16x8, load8<T>(dr, off));
+        const bf16x8 ov = __builtin_bit_cast(bf16x8, load8<T>(or_, off));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bf16x2 a = {doreg[kk][2 * e], doreg[kk][2 * e + 1]};
+            const bf16x2 b = {ov[2 * e], ov[2 * e + 1]};
+            dpart = __builtin_amdgcn_fdot2_f32_bf16(a, b, dpart, false);
+        }
+    }
+    const float Di = swap_halves_sum(dpart);
+    const float Li = qi < S ? lse[static_cast<int64_t>(head) * S + qi] : 0.f;
+    if (g == 0 && qi < S) delta[static_cast<int64_t>(head) * S + qi] = Di;
+
+    f32x16 dqacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
+    const int nkb = (S + kBC - 1) / kBC;
+
+    // Staging: V in the row pattern, K in the key-pair pattern (written both
+    // row-major and transposed).
+    Stage<D, T, kWaves> st;
+    st.load(vr, kr, 0, 0, tid);
+    st.store_k(vbuf[0], tid);
+    st.store_v_rows(kbuf[0], tid);
+    st.store_v(ktbuf[0], tid);
+    __syncthreads();
+
+    for (int j = 0; j < nkb; ++j) {
+        const int b = j & 1;
+        if (j + 1 < nkb) st.load(vr, kr, j + 1, j + 1, tid);
+        f32x16 sacc[2], dpacc[2];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+            sacc[mt] = f32x16{};
+            dpacc[mt] = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int row = (mt * 32 + li) * Lds<D>::KS + kk * 16 + g * 8;
+                const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kbuf[b] + row);
+                const bf16x8 va = *reinterpret_cast<const bf16x8 *>(vbuf[b] + row);
+                sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc[mt], 0, 0, 0);
+                dpacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc[mt], 0, 0, 0);
+            }
+        }
+        // dS^T in the accumulator layout: lane (g, query li), keys
+        // 32 mt + 8 (r / 4) + 4 g + r % 4; packed as the B operands of the
+        // four 16-key steps (keys permuted as in the forward's P).
+        const int kvalid = S - j * kBC;
+        bf16x8 dsb[4];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                f32x8 x;
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const int rr = h * 8 + r;
+                    const int key = mt * 32 + (rr >> 2) * 8 + g * 4 + (rr & 3);
+                    const float p = key < kvalid
+                        ? __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][rr], c, -Li)) : 0.f;
+                    x[r] = p * (dpacc[mt][rr] - Di);
+                }
+                dsb[mt * 2 + h] = __builtin_convertvector(x, bf16x8);
+            }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                    ktbuf[b] + (dt * 32 + li) * Lds<D>::VS + (ks * 2 + g) * 8);
+                dqacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[ks], dqacc[dt], 0, 0, 0);
+            }
+        if (j + 1 < nkb) {
+            st.store_k(vbuf[b ^ 1], tid);
+            st.store_v_rows(kbuf[b ^ 1], tid);
+            st.store_v(ktbuf[b ^ 1], tid);
+        }
+        __syncthreads();
+    }
+
+    if (qi < S) {
+        T *row = dq + hoff + static_cast<int64_t>(qi) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 x = {dqacc[dt][rb * 4 + 0] * scale, dqacc[dt][rb * 4 + 1] * scale,
+                                 dqacc[dt][rb * 4 + 2] * scale, dqacc[dt][rb * 4 + 3] * scale};
+                store4(row + dt * 32 + rb * 8 + g * 4, x);
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV: key-parallel
+// ---------------------------------------------------------------------------
+// Staging of one block of 32 queries: Q and dO in query pairs (row-major and
+// transposed stores), L and D as 32 floats each.
+template <int D, typename T>
+struct QStage {
+    static constexpr int CH = D / 8;
+    static constexpr unsigned ROWB = D * sizeof(T), CHB = 8 * sizeof(T);
+    static constexpr int TASKS = (kQB / 2) * CH;  // (query pair, chunk) tasks
+    static_assert(TASKS <= kThreads, "one task per thread at most");
+    u32x4 qv[2], dv[2];
+    f32x4 stat;
+
+    __device__ static int pair(int t) { return t & 15; }
+    __device__ static int chunk(int t) { return t >> 4; }
+
+    __device__ void load(__amdgpu_buffer_rsrc_t qr, __amdgpu_buffer_rsrc_t dr,
+                         __amdgpu_buffer_rsrc_t lr, __amdgpu_buffer_rsrc_t er, int blk, int tid) {
+        const unsigned q0 = static_cast<unsigned>(blk) * kQB;
+        if (tid < TASKS) {
+            const unsigned off = (q0 + 2 * pair(tid)) * ROWB + chunk(tid) * CHB;
+            qv[0] = load8<T>(qr, off);
+            qv[1] = load8<T>(qr, off + ROWB);
+            dv[0] = load8<T>(dr, off);
+            dv[1] = load8<T>(dr, off + ROWB);
+        }
+        // Threads 0..7 fetch L, 8..15 fetch D, 4 floats each.
+        if (tid < 16) {
+            const unsigned off = (q0 + (tid & 7) * 4) * 4u;
+            stat = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                 tid < 8 ? lr : er, off, 0, 0));
+        }
+    }
+
+    __device__ void store(__bf16 *qrow, __bf16 *drow, __bf16 *qt, __bf16 *dt, float *ls, float *ds,
+                          int tid) const {
+        if (tid < TASKS) {
+            const int p = pair(tid), ch = chunk(tid);
+            __bf16 *a = qrow + 2 * p * QLds<D>::RS + ch * 8;
+            __bf16 *b = drow + 2 * p * QLds<D>::RS + ch * 8;
+            *reinterpret_cast<u32x4 *>(a) = qv[0];
+            *reinterpret_cast<u32x4 *>(a + QLds<D>::RS) = qv[1];
+            *reinterpret_cast<u32x4 *>(b) = dv[0];
+            *reinterpret_cast<u32x4 *>(b + QLds<D>::RS) = dv[1];
+            __bf16 *ta = qt + ch * 8 * QLds<D>::TS + vt_pos(2 * p);
+            __bf16 *tb = dt + ch * 8 * QLds<D>::TS + vt_pos(2 * p);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
+                *reinterpret_cast<unsigned *>(ta + e * QLds<D>::TS) =
+                    __builtin_amdgcn_perm(qv[1][e >> 1], qv[0][e >> 1], sel);
+                *reinterpret_cast<unsigned *>(tb + e * QLds<D>::TS) =
+                    __builtin_amdgcn_perm(dv[1][e >> 1], dv[0][e >> 1], sel);
+            }
+        }
+        if (tid < 16) *reinterpret_cast<f32x4 *>((tid < 8 ? ls : ds) + (tid & 7) * 4) = stat;
+    }
+};
+
+template <int D, typename T>
+__global__ __launch_bounds__(kThreads, 1) void attention_dkdv_kernel(
+    const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
+    const T *__restrict__ dout, const float *__restrict__ lse, const float *__restrict__ delta,
+    T *__restrict__ dk, T *__restrict__ dv, int S, int n_ktiles, float c, float scale) {
+    constexpr int KK = D / 16, DT = D / 32;
+    __shared__ __attribute__((aligned(16))) __bf16 qbuf[2][QLds<D>::R];
+    __shared__ __attribute__((aligned(16))) __bf16 dbuf[2][QLds<D>::R];
+    __shared__ __attribute__((aligned(16))) __bf16 qtbuf[2][QLds<D>::TT];
+    __shared__ __attribute__((aligned(16))) __bf16 dtbuf[2][QLds<D>::TT];
+    __shared__ __attribute__((aligned(16))) float lbuf[2][kQB];
+    __shared__ __attribute__((aligned(16))) float ebuf[2][kQB];
+
+    const int logical = xcd_logical(blockIdx.x, gridDim.x);
+    const int head = logical / n_ktiles;
+    const int ktile = logical - head * n_ktiles;
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * sizeof(T);
+    const __amdgpu_buffer_rsrc_t qr = head_rsrc(q + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t vr = head_rsrc(v + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t dr = head_rsrc(dout + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t lr = head_rsrc(lse + static_cast<int64_t>(head) * S, int64_t{S} * 4);
+    const __amdgpu_buffer_rsrc_t er = head_rsrc(delta + static_cast<int64_t>(head) * S, int64_t{S} * 4);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 31, g = lane >> 5;
+    const int kj = ktile * (kQW * kWaves) + wave * kQW + li;
+
+    // K^T and V^T as B operands: lane (g, key li) holds head dims 16 kk + 8 g + [0, 8).
+    bf16x8 kreg[KK], vreg[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        const unsigned off = static_cast<unsigned>(kj * D + kk * 16 + g * 8) * sizeof(T);
+        kreg[kk] = __builtin_bit_cast(bf16x8, load8<T>(kr, off));
+        vreg[kk] = __builtin_bit_cast(bf16x8, load8<T>(vr, off));
+    }
+    f32x16 dkacc[DT], dvacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        dkacc[dt] = f32x16{};
+        dvacc[dt] = f32x16{};
+    }
+    const int nqb = (S + kQB - 1) / kQB;
+
+    QStage<D, T> st;
+    st.load(qr, dr, lr, er, 0, tid);
+    st.store(qbuf[0], dbuf[0], qtbuf[0], dtbuf[0], lbuf[0], ebuf[0], tid);
+    __syncthreads();
+
+    for (int i = 0; i < nqb; ++i) {
+        const int b = i & 1;
+        if (i + 1 < nqb) st.load(qr, dr, lr, er, i + 1, tid);
+        // S and dP: lane (g, key li), rows = queries 8 (r / 4) + 4 g + r % 4.
+        const f32x16 s = rows_times_regs<D>(qbuf[b], QLds<D>::RS, kreg, li, g);
+        const f32x16 dp = rows_times_regs<D>(dbuf[b], QLds<D>::RS, vreg, li, g);
+        const int qvalid = S - i * kQB;
+        bf16x8 pb[2], dsb[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const f32x4 l0 = *reinterpret_cast<const f32x4 *>(&lbuf[b][h * 16 + g * 4]);
+            const f32x4 l1 = *reinterpret_cast<const f32x4 *>(&lbuf[b][h * 16 + 8 + g * 4]);
+            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&ebuf[b][h * 16 + g * 4]);
+            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&ebuf[b][h * 16 + 8 + g * 4]);
+            f32x8 p, ds;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int rr = h * 8 + r;
+                const int qrow = (rr >> 2) * 8 + g * 4 + (rr & 3);
+                const float Lr = (r < 4) ? l0[r & 3] : l1[r & 3];
+                const float Dr = (r < 4) ? e0[r & 3] : e1[r & 3];
+                p[r] = qrow < qvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[rr], c, -Lr)) : 0.f;
+                ds[r] = p[r] * (dp[rr] - Dr);
+            }
+            pb[h] = __builtin_convertvector(p, bf16x8);
+            dsb[h] = __builtin_convertvector(ds, bf16x8);
+        }
+        // dV^T += dO^T P and dK^T += Q^T dS over the block's 32 queries (two
+        // 16-query steps; transposed rows hold the queries permuted).
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int qs = 0; qs < 2; ++qs) {
+                const int off = (dt * 32 + li) * QLds<D>::TS + (qs * 2 + g) * 8;
+                const bf16x8 da = *reinterpret_cast<const bf16x8 *>(dtbuf[b] + off);
+                const bf16x8 qa = *reinterpret_cast<const bf16x8 *>(qtbuf[b] + off);
+                dvacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, pb[qs], dvacc[dt], 0, 0, 0);
+                dkacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, dsb[qs], dkacc[dt], 0, 0, 0);
+            }
+        if (i + 1 < nqb)
+            st.store(qbuf[b ^ 1], dbuf[b ^ 1], qtbuf[b ^ 1], dtbuf[b ^ 1], lbuf[b ^ 1], ebuf[b ^ 1], tid);
+        __syncthreads();
+    }
+
+    if (kj < S) {
+        T *krow = dk + hoff + static_cast<int64_t>(kj) * D;
+        T *vrow = dv + hoff + static_cast<int64_t>(kj) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 xk = {dkacc[dt][rb * 4 + 0] * scale, dkacc[dt][rb * 4 + 1] * scale,
+                                  dkacc[dt][rb * 4 + 2] * scale, dkacc[dt][rb * 4 + 3] * scale};
+                const f32x4 xv = {dvacc[dt][rb * 4 + 0], dvacc[dt][rb * 4 + 1], dvacc[dt][rb * 4 + 2],
+                                  dvacc[dt][rb * 4 + 3]};
+                store4(krow + dt * 32 + rb * 8 + g * 4, xk);
+                store4(vrow + dt * 32 + rb * 8 + g * 4, xv);
+            }
+    }
+}
+
+template <int D, typename T>
+hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const void *o,
+                            const void *dout, const float *lse, void *dq, void *dk, void *dv,
+                            float *delta, int S, int n_heads, float c, float scale,
+                            hipStream_t stream) {
+    constexpr int BR = kQW * kWaves;
+    const int n_tiles = (S + BR - 1) / BR;
+    const int64_t blocks = static_cast<int64_t>(n_tiles) * n_heads;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    attention_dq_kernel<D, T><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+        static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
+        static_cast<const T *>(o), static_cast<const T *>(dout), lse, static_cast<T *>(dq), delta, S,
+        n_tiles, c, scale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    attention_dkdv_kernel<D, T><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+        static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
+        static_cast<const T *>(dout), lse, delta, static_cast<T *>(dk), static_cast<T *>(dv), S,
+        n_tiles, c, scale);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention_backward(const void *q, const void *k, const void *v, const void *o,
+                                     const void *dout, const float *lse, void *dq, void *dk,
+                                     void *dv, float *delta, int S, int n_heads, int d,
+                                     float scale, int dtype, hipStream_t stream) {
+    if (S == 0 || n_heads == 0) return hipSuccess;
+    const float c = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+    if (d == 128 && dtype == 0)
+        return launch_bwd_typed<128, __bf16>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
+                                             scale, stream);
+    if (d == 64 && dtype == 0)
+        return launch_bwd_typed<64, __bf16>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
+                                            scale, stream);
+    if (d == 128 && dtype == 1)
+        return launch_bwd_typed<128, float>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
+                                            scale, stream);
+    if (d == 64 && dtype == 1)
+        return launch_bwd_typed<64, float>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
+                                           scale, stream);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace hcms

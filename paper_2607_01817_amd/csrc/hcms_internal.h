@@ -32,8 +32,19 @@ hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64
 int attention_queries_per_block(int d);
 int attention_blocks_per_cu(int d);
 
-hipError_t launch_attention(const void *q, const void *k, const void *v, void *o,
+// lse, if not NULL, receives [n_heads][S] fp32 log2 softmax denominators:
+// P_ij = exp2(scale_log2e * <q_i, k_j> - lse_i).
+hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, float *lse,
                             int S, int n_heads, int d, float scale_log2e, int dtype,
                             hipStream_t stream);
+
+// Backward of attention for `n_heads` consecutive heads (head-major buffers
+// starting at the chunk's first head; lse and delta [n_heads][S] fp32): one
+// query-parallel launch writing delta = <dO, O> and dq, then one key-parallel
+// launch writing dk and dv.
+hipError_t launch_attention_backward(const void *q, const void *k, const void *v, const void *o,
+                                     const void *dout, const float *lse, void *dq, void *dk,
+                                     void *dv, float *delta, int S, int n_heads, int d,
+                                     float scale, int dtype, hipStream_t stream);
 
 }  // namespace hcms

@@ -99,6 +99,15 @@ def make_qkv(w: Workload, planted: bool = False, seed: int | None = None):
     return q, k, v
 
 
+def make_dout(w: Workload, seed: int | None = None):
+    """The output gradient dL/dO of a training step as a host tensor [S][H][d]:
+    fp32 ``randn`` from a CPU generator seeded with ``seed + 2000`` (default
+    ``w.seed + 2000``), unit scale, rounded to the storage dtype."""
+    seed = (w.seed if seed is None else seed) + 2000
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    return torch.randn((w.S, w.H, w.d), generator=g, dtype=torch.float32).to(torch_dtype(w))
+
+
 def planted_permutation(w: Workload, h: int, seed: int | None = None) -> np.ndarray:
     """The key index each query of head ``h`` is planted on (a permutation)."""
     seed = w.seed if seed is None else seed

@@ -338,3 +338,34 @@ def test_binding_rejects_cpu_tensors(lib):
         hcms.pack(x, 2, 0, 1)
     with pytest.raises(ValueError):
         hcms.attention(x.permute(1, 0, 2), x.permute(1, 0, 2), x.permute(1, 0, 2), 0.1)
+
+
+def test_training_forward_and_backward_validation(lib):
+    sizes = (ctypes.c_int * 2)(2, 2)
+    E, F, G_, H_ = 0x50000000, 0x60000000, 0x70000000, 0x80000000
+    L, Dl = 0x90000000, 0x98000000   # [H][S] fp32 statistics, far from the tensors
+
+    def fwd(lse=L, q=A, S=512):
+        return lib.hcms_attention_lse(q, B, C_, D_, lse, S, 4, 64, 0.125, sizes, 2, 1, None)
+
+    assert fwd(lse=None) == ENULL
+    assert fwd(lse=L + 2) == EALIGN
+    assert fwd(lse=A + 64) == EALIAS
+    assert fwd(S=0, lse=None, q=None) == OK
+
+    def bwd(dout=E, dq=F, dk=G_, dv=H_, lse=L, delta=Dl, S=512, d=64):
+        return lib.hcms_attention_backward(A, B, C_, D_, dout, lse, dq, dk, dv, delta, S, 4, d,
+                                           0.125, sizes, 2, 1, None)
+
+    assert bwd(dout=None) == ENULL
+    assert bwd(dq=None) == ENULL
+    assert bwd(lse=None) == ENULL
+    assert bwd(delta=None) == ENULL
+    assert bwd(dk=G_ + 8) == EALIGN
+    assert bwd(delta=Dl + 1) == EALIGN
+    assert bwd(dq=A) == EALIAS          # a gradient over an input
+    assert bwd(dk=F + 64) == EALIAS     # two gradients overlap
+    assert bwd(delta=L) == EALIAS       # statistics overlap each other
+    assert bwd(delta=F + 16) == EALIAS  # workspace over a gradient
+    assert bwd(d=96) == ESHAPE
+    assert bwd(S=0, dout=None, dq=None, dk=None, dv=None, lse=None, delta=None) == OK

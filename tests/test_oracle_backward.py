@@ -80,3 +80,14 @@ def test_row_subsets_equal_full_rows(oracle_mod):
     np.testing.assert_array_equal(sub[2], full[2][kr])
     only_q = oracle_mod.attention_backward_head(q, k, v, g, 0.4, q_rows=qr, k_rows=[])
     np.testing.assert_array_equal(only_q[0], full[0][qr])
+
+
+def test_lse_matches_torch_logsumexp_and_closed_forms(oracle_mod):
+    q, k, _, _ = _rand(40, 16, 9, scale=3.0)
+    want = torch.logsumexp(0.3 * torch.tensor(q) @ torch.tensor(k).T, dim=1).numpy() / np.log(2.0)
+    np.testing.assert_allclose(oracle_mod.lse_head(q, k, 0.3), want, rtol=0, atol=1e-12)
+    k_eq = np.repeat(k[:1], 40, axis=0)    # equal keys: scale s + log(S)
+    np.testing.assert_allclose(oracle_mod.lse_head(q, k_eq, 0.3),
+                               (0.3 * q @ k[0] + np.log(40)) / np.log(2.0), atol=1e-12)
+    np.testing.assert_allclose(oracle_mod.lse_head(q[:1], k[:1], 0.3), 0.3 * q[0] @ k[0] / np.log(2.0),
+                               atol=1e-12)
