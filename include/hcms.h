@@ -326,6 +326,9 @@ HCMS_API int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap)
  * synchronisation).  All modes and all chunkings give bit-identical o_seq.
  *   q_seq, k_seq, v_seq, o_seq : device, [P][S/P][H][d]
  *   q_hm, k_hm, v_hm, o_hm     : device workspaces, [H][S][d] each
+ *   lse                        : NULL, or [H][S] fp32: the attention's log2
+ *                                softmax denominators (hcms_attention_lse), kept
+ *                                for hcms_backward
  *   copy_stream, compute_stream: used in pipelined mode; must be distinct from
  *                                each other and from main_stream.  Inline mode
  *                                uses copy_stream only, lanes mode
@@ -335,10 +338,38 @@ HCMS_API int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap)
  */
 HCMS_API int hcms_forward(hcms_ctx *ctx,
                  const void *q_seq, const void *k_seq, const void *v_seq, void *o_seq,
-                 void *q_hm, void *k_hm, void *v_hm, void *o_hm,
+                 void *q_hm, void *k_hm, void *v_hm, void *o_hm, float *lse,
                  int P, int S, int H, int d, float scale,
                  const int *chunk_sizes, int n_chunks, int dtype, int mode,
                  void *main_stream, void *copy_stream, void *compute_stream);
+
+/*
+ * The backward of hcms_forward, for training: the reverse pipeline of the
+ * chunked schedule.  Per chunk c, on the same plan as hcms_plan(n_chunks,
+ * mode) (PACK, ATTENTION and UNPACK ops):
+ *   PACK c      dout_seq's heads of chunk c into do_hm ([P][S/P][H][d] ->
+ *               [H_c][S][d], the gradient's all-to-all to head shards);
+ *   ATTENTION c hcms_attention_backward of the chunk (D into delta, then dQ;
+ *               then dK, dV into dq_hm, dk_hm, dv_hm);
+ *   UNPACK c    dq_hm, dk_hm, dv_hm of chunk c into the head slots of
+ *               dq_seq, dk_seq, dv_seq (the all-to-all back to sequence
+ *               shards).
+ *   q_hm, k_hm, v_hm, o_hm, lse : as hcms_forward (with lse) left them for the
+ *                    same inputs, scale and d (any chunking)
+ *   dout_seq         : dL/dO, [P][S/P][H][d]
+ *   dq_seq, dk_seq, dv_seq : outputs, [P][S/P][H][d]
+ *   do_hm, dq_hm, dk_hm, dv_hm : device workspaces, [H][S][d] each
+ *   delta            : device workspace, [H][S] fp32
+ * Streams and modes as hcms_forward.  Every mode and chunking gives
+ * bit-identical gradients.  Errors: as hcms_forward and
+ * hcms_attention_backward.
+ */
+HCMS_API int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_seq,
+                           void *dv_seq, const void *q_hm, const void *k_hm, const void *v_hm,
+                           const void *o_hm, const float *lse, void *do_hm, void *dq_hm,
+                           void *dk_hm, void *dv_hm, float *delta, int P, int S, int H, int d,
+                           float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
+                           void *main_stream, void *copy_stream, void *compute_stream);
 
 #ifdef __cplusplus
 }

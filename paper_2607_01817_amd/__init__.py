@@ -80,8 +80,10 @@ def load():
         "hcms_ctx_destroy": ([vp], i),
         "hcms_ctx_set_timing": ([vp, i], i),
         "hcms_ctx_kernel_ms": ([vp, i, ctypes.POINTER(ctypes.c_float), i], i),
-        "hcms_forward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, ip, i, i, i,
+        "hcms_forward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, ip, i, i, i,
                           vp, vp, vp], i),
+        "hcms_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i,
+                           f, ip, i, i, i, vp, vp, vp], i),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -308,6 +310,8 @@ class Context:
         self._h = h
         self._ws = None
         self._ws_key = None
+        self._bws = None
+        self._bws_key = None
 
     @property
     def num_cu(self) -> int:
@@ -355,11 +359,14 @@ class Context:
     def forward(self, q_seq: torch.Tensor, k_seq: torch.Tensor, v_seq: torch.Tensor, P: int,
                 scale: float, chunk_sizes, mode: int = MODE_AUTO,
                 out: torch.Tensor | None = None, workspaces=None,
-                main_stream=None) -> torch.Tensor:
+                main_stream=None, lse: torch.Tensor | None = None) -> torch.Tensor:
         """One GPU's share of an HCMS forward: [S][H][d] in, [S][H][d] out.
 
         The result is ordered on ``main_stream`` (default: the current stream)
-        when this returns; nothing blocks the host.
+        when this returns; nothing blocks the host.  With ``lse`` (float32
+        [H][S]) the attention also writes its log2 softmax denominators, and
+        the workspaces keep the head-major Q, K, V, O: :meth:`backward` needs
+        both.
         """
         for t, n in ((q_seq, "q_seq"), (k_seq, "k_seq"), (v_seq, "v_seq")):
             _dev(t, n)
@@ -380,10 +387,81 @@ class Context:
                 raise ValueError("each workspace must hold [H][S][d] of the input dtype")
         sizes, n = _ints(chunk_sizes)
         main = _stream(main_stream)
+        lse_p = None
+        if lse is not None:
+            lse_p = _stats(lse, "lse", H, S, q_seq.device).data_ptr()
         _check(load().hcms_forward(
             self._h, q_seq.data_ptr(), k_seq.data_ptr(), v_seq.data_ptr(), out.data_ptr(),
-            ws[0].data_ptr(), ws[1].data_ptr(), ws[2].data_ptr(), ws[3].data_ptr(),
+            ws[0].data_ptr(), ws[1].data_ptr(), ws[2].data_ptr(), ws[3].data_ptr(), lse_p,
             P, S, H, d, float(scale), sizes, n, _dtype(q_seq), int(mode), main,
             ctypes.c_void_p(self.copy_stream.cuda_stream),
             ctypes.c_void_p(self.compute_stream.cuda_stream)))
         return out
+
+    def backward_workspaces(self, S: int, H: int, d: int, dtype: torch.dtype):
+        """Head-major dO, dQ, dK, dV workspaces and the [H][S] float32 delta."""
+        key = (S, H, d, dtype)
+        if self._bws_key != key:
+            dev = f"cuda:{self.device}"
+            self._bws = [torch.empty((H, S, d), dtype=dtype, device=dev) for _ in range(4)]
+            self._bws.append(torch.empty((H, S), dtype=torch.float32, device=dev))
+            self._bws_key = key
+        return self._bws
+
+    def backward(self, dout_seq: torch.Tensor, P: int, scale: float, chunk_sizes, workspaces,
+                 lse: torch.Tensor, mode: int = MODE_AUTO, dq=None, dk=None, dv=None,
+                 backward_workspaces=None, main_stream=None):
+        """Gradients (dq, dk, dv), each [S][H][d], of the forward whose head-major
+        workspaces and ``lse`` are given, for the output gradient ``dout_seq``."""
+        _dev(dout_seq, "dout_seq")
+        if dout_seq.dim() != 3:
+            raise ValueError("dout_seq must be [S][H][d]")
+        S, H, d = dout_seq.shape
+        outs = [torch.empty_like(dout_seq) if t is None else t for t in (dq, dk, dv)]
+        for t, nm in zip(outs, ("dq", "dk", "dv")):
+            _dev(t, nm)
+            if t.shape != dout_seq.shape or t.dtype != dout_seq.dtype:
+                raise ValueError(f"{nm} must match dout_seq")
+        fw = list(workspaces)
+        bw = backward_workspaces if backward_workspaces is not None else \
+            self.backward_workspaces(S, H, d, dout_seq.dtype)
+        for t in fw + list(bw[:4]):
+            _dev(t, "workspace")
+            if t.numel() != dout_seq.numel() or t.dtype != dout_seq.dtype:
+                raise ValueError("each workspace must hold [H][S][d] of the gradient's dtype")
+        lse = _stats(lse, "lse", H, S, dout_seq.device)
+        delta = _stats(bw[4], "delta", H, S, dout_seq.device)
+        sizes, n = _ints(chunk_sizes)
+        _check(load().hcms_backward(
+            self._h, dout_seq.data_ptr(), outs[0].data_ptr(), outs[1].data_ptr(), outs[2].data_ptr(),
+            fw[0].data_ptr(), fw[1].data_ptr(), fw[2].data_ptr(), fw[3].data_ptr(), lse.data_ptr(),
+            bw[0].data_ptr(), bw[1].data_ptr(), bw[2].data_ptr(), bw[3].data_ptr(), delta.data_ptr(),
+            P, S, H, d, float(scale), sizes, n, _dtype(dout_seq), int(mode), _stream(main_stream),
+            ctypes.c_void_p(self.copy_stream.cuda_stream),
+            ctypes.c_void_p(self.compute_stream.cuda_stream)))
+        return tuple(outs)
+
+
+class HcmsAttention(torch.autograd.Function):
+    """Autograd over :meth:`Context.forward` and :meth:`Context.backward`:
+    ``HcmsAttention.apply(q_seq, k_seq, v_seq, ctx, P, scale, chunk_sizes,
+    mode)`` returns the [S][H][d] output, and its backward runs the reverse
+    pipeline.  The forward allocates its own head-major workspaces (kept for
+    the backward) so that later calls on the same context do not overwrite
+    them."""
+
+    @staticmethod
+    def forward(fctx, q_seq, k_seq, v_seq, ctx, P, scale, chunk_sizes, mode=MODE_AUTO):
+        S, H, d = q_seq.shape
+        ws = [torch.empty((H, S, d), dtype=q_seq.dtype, device=q_seq.device) for _ in range(4)]
+        lse = torch.empty((H, S), dtype=torch.float32, device=q_seq.device)
+        out = ctx.forward(q_seq.contiguous(), k_seq.contiguous(), v_seq.contiguous(), P, scale,
+                          chunk_sizes, mode=mode, workspaces=ws, lse=lse)
+        fctx.hcms = (ctx, P, scale, tuple(chunk_sizes), mode, ws, lse)
+        return out
+
+    @staticmethod
+    def backward(fctx, dout):
+        ctx, P, scale, sizes, mode, ws, lse = fctx.hcms
+        dq, dk, dv = ctx.backward(dout.contiguous(), P, scale, sizes, ws, lse, mode=mode)
+        return dq, dk, dv, None, None, None, None, None

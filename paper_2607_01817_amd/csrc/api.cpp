@@ -353,6 +353,98 @@ struct hcms_ctx {
     std::vector<int> timed_chunks;       // chunk count of each timed call
 };
 
+namespace {
+
+// Validation shared by hcms_forward and hcms_backward; resolves
+// HCMS_MODE_AUTO into *mode and returns the row size's log2 unit count.
+int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const int *chunk_sizes,
+                   int n_chunks, int dtype, int *mode, int *log2u, void *main_stream,
+                   void *copy_stream, void *compute_stream) {
+    int st;
+    const int m = *mode;
+    if (!plan_mode(m) && m != HCMS_MODE_AUTO)
+        return fail(HCMS_ERR_ARG, "mode %d is not serial (0), pipelined (1), inline (2), lanes (3) "
+                    "or auto (4)", m);
+    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
+    if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
+    if ((st = row_log2_units(d, dtype, log2u)) != HCMS_OK) return st;
+    if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
+    if ((st = check_chunks(H, chunk_sizes, n_chunks)) != HCMS_OK) return st;
+    if (n_chunks > ctx->max_chunks)
+        return fail(HCMS_ERR_CHUNKS, "n_chunks=%d exceeds the context's max_chunks=%d", n_chunks,
+                    ctx->max_chunks);
+    if ((st = check_scale(scale)) != HCMS_OK) return st;
+    if (m == HCMS_MODE_PIPELINED &&
+        (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
+        return fail(HCMS_ERR_ARG, "pipelined mode needs three distinct streams");
+    const int r = m == HCMS_MODE_AUTO ? auto_mode(S, d, chunk_sizes, n_chunks, ctx->n_cu) : m;
+    if (r == HCMS_MODE_INLINE && copy_stream == main_stream)
+        return fail(HCMS_ERR_ARG, "inline mode needs a copy stream distinct from the main stream");
+    if (r == HCMS_MODE_LANES && compute_stream == main_stream)
+        return fail(HCMS_ERR_ARG, "lanes mode needs a compute stream distinct from the main stream");
+    int cur_dev = -1;
+    const hipError_t e = hipGetDevice(&cur_dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur_dev != ctx->device)
+        return fail(HCMS_ERR_ARG, "context is bound to device %d, current device is %d", ctx->device,
+                    cur_dev);
+    *mode = r;
+    return HCMS_OK;
+}
+
+// Issues the plan of `mode` (already resolved): RECORD / WAIT ops on the
+// context's events, kernel ops through launch(kind, h0, h_count, stream),
+// each bracketed by timing events while the context records.
+template <typename Launch>
+int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *main_stream,
+                 void *copy_stream, void *compute_stream, Launch &&launch) {
+    PlanWriter w{ctx->plan.data(), static_cast<int>(ctx->plan.size())};
+    const int n_ops = build_plan(C, mode, w);
+    ctx->last_mode = mode;
+    hipStream_t streams[3] = {static_cast<hipStream_t>(main_stream),
+                              static_cast<hipStream_t>(copy_stream),
+                              static_cast<hipStream_t>(compute_stream)};
+    std::vector<int> offs(C + 1, 0);
+    for (int c = 0; c < C; ++c) offs[c + 1] = offs[c] + chunk_sizes[c];
+    // Sync event id -> ctx event (ids: 0 E_main, 1..C E_pack, C+1..2C E_attn,
+    // 2C+1 E_done; the context keeps max_chunks of each kind).
+    auto event_of = [&](int id) -> hipEvent_t {
+        if (id == 0) return ctx->events[0];
+        if (id <= C) return ctx->events[id];
+        if (id <= 2 * C) return ctx->events[1 + ctx->max_chunks + (id - 1 - C)];
+        return ctx->events[1 + 2 * ctx->max_chunks];
+    };
+    const bool timed = static_cast<int>(ctx->timed_chunks.size()) < ctx->timing_calls;
+    const size_t call = ctx->timed_chunks.size();
+    hipError_t e;
+    for (int i = 0; i < n_ops; ++i) {
+        const hcms_op &op = ctx->plan[i];
+        hipStream_t s = streams[op.stream];
+        if (op.kind == HCMS_OP_RECORD) {
+            if ((e = hipEventRecord(event_of(op.event), s)) != hipSuccess)
+                return hip_fail(e, "hipEventRecord");
+            continue;
+        }
+        if (op.kind == HCMS_OP_WAIT) {
+            if ((e = hipStreamWaitEvent(s, event_of(op.event), 0)) != hipSuccess)
+                return hip_fail(e, "hipStreamWaitEvent");
+            continue;
+        }
+        const int c = op.chunk;
+        const size_t slot = (call * 3 + (op.kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
+        if (timed && (e = hipEventRecord(ctx->t_begin[slot], s)) != hipSuccess)
+            return hip_fail(e, "hipEventRecord");
+        if ((e = launch(op.kind, offs[c], chunk_sizes[c], s)) != hipSuccess)
+            return hip_fail(e, "kernel launch");
+        if (timed && (e = hipEventRecord(ctx->t_end[slot], s)) != hipSuccess)
+            return hip_fail(e, "hipEventRecord");
+    }
+    if (timed) ctx->timed_chunks.push_back(C);
+    return ok();
+}
+
+}  // namespace
+
 extern "C" {
 
 int hcms_abi_version(void) { return HCMS_ABI_VERSION; }
@@ -401,7 +493,9 @@ int hcms_unpack(const void *src_hm, void *dst_seq, int P, int S, int H, int d, i
     int log2u = 0;
     const int st = check_pack_args(src_hm, dst_seq, P, S, H, d, h_begin, h_count, dtype, &log2u);
     if (st != HCMS_OK) return st;
-    const hipError_t e = hcms::launch_unpack(src_hm, dst_seq, S, H, h_begin, h_count, log2u,
+    const void *src[1] = {src_hm};
+    void *dst[1] = {dst_seq};
+    const hipError_t e = hcms::launch_unpack(src, dst, 1, S, H, h_begin, h_count, log2u,
                                              static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "unpack launch");
     return ok();
@@ -627,37 +721,20 @@ int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap) {
 }
 
 int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void *v_seq, void *o_seq,
-                 void *q_hm, void *k_hm, void *v_hm, void *o_hm, int P, int S, int H, int d,
-                 float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
+                 void *q_hm, void *k_hm, void *v_hm, void *o_hm, float *lse, int P, int S, int H,
+                 int d, float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
                  void *main_stream, void *copy_stream, void *compute_stream) {
     int st;
     if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
     if (S > 0 && (!q_seq || !k_seq || !v_seq || !o_seq || !q_hm || !k_hm || !v_hm || !o_hm))
         return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
-    if (!plan_mode(mode) && mode != HCMS_MODE_AUTO)
-        return fail(HCMS_ERR_ARG, "mode %d is not serial (0), pipelined (1), inline (2), lanes (3) "
-                    "or auto (4)", mode);
-    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
-    if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
     int log2u = 0;
-    if ((st = row_log2_units(d, dtype, &log2u)) != HCMS_OK) return st;
-    if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
-    if ((st = check_chunks(H, chunk_sizes, n_chunks)) != HCMS_OK) return st;
-    if (n_chunks > ctx->max_chunks)
-        return fail(HCMS_ERR_CHUNKS, "n_chunks=%d exceeds the context's max_chunks=%d", n_chunks,
-                    ctx->max_chunks);
-    if ((st = check_scale(scale)) != HCMS_OK) return st;
-    if (mode == HCMS_MODE_PIPELINED &&
-        (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
-        return fail(HCMS_ERR_ARG, "pipelined mode needs three distinct streams");
-    if (mode == HCMS_MODE_AUTO) mode = auto_mode(S, d, chunk_sizes, n_chunks, ctx->n_cu);
-    if (mode == HCMS_MODE_INLINE && copy_stream == main_stream)
-        return fail(HCMS_ERR_ARG, "inline mode needs a copy stream distinct from the main stream");
-    if (mode == HCMS_MODE_LANES && compute_stream == main_stream)
-        return fail(HCMS_ERR_ARG, "lanes mode needs a compute stream distinct from the main stream");
+    if ((st = check_schedule(ctx, P, S, H, d, scale, chunk_sizes, n_chunks, dtype, &mode, &log2u,
+                             main_stream, copy_stream, compute_stream)) != HCMS_OK)
+        return st;
     const void *all[8] = {q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm};
     for (const void *p : all)
-        if (!aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+        if (S > 0 && !aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
     const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
     for (int i = 0; i < 8; ++i)
         for (int j = i + 1; j < 8; ++j) {
@@ -666,86 +743,93 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
             if (!both_inputs && overlaps(all[i], bytes, all[j], bytes))
                 return fail(HCMS_ERR_ALIAS, "tensor %d overlaps tensor %d", i, j);
         }
-    int cur_dev = -1;
-    hipError_t e = hipGetDevice(&cur_dev);
-    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (cur_dev != ctx->device)
-        return fail(HCMS_ERR_ARG, "context is bound to device %d, current device is %d", ctx->device,
-                    cur_dev);
-    if (S == 0) return ok();
-
-    PlanWriter w{ctx->plan.data(), static_cast<int>(ctx->plan.size())};
-    const int n_ops = build_plan(n_chunks, mode, w);
-    ctx->last_mode = mode;
-
-    hipStream_t streams[3] = {static_cast<hipStream_t>(main_stream),
-                              static_cast<hipStream_t>(copy_stream),
-                              static_cast<hipStream_t>(compute_stream)};
-    const int C = n_chunks;
-    int h0[64 + 1];
-    std::vector<int> h0_big;
-    int *offs = h0;
-    if (C + 1 > 65) {
-        h0_big.resize(C + 1);
-        offs = h0_big.data();
+    if (lse) {
+        if ((st = check_stats(lse, "lse", S, H, q_hm, k_hm, v_hm, o_hm, d, dtype)) != HCMS_OK) return st;
+        if ((st = check_stats(lse, "lse", S, H, q_seq, k_seq, v_seq, o_seq, d, dtype)) != HCMS_OK)
+            return st;
     }
-    offs[0] = 0;
-    for (int c = 0; c < C; ++c) offs[c + 1] = offs[c] + chunk_sizes[c];
+    if (S == 0) return ok();
 
     const int64_t head_bytes = static_cast<int64_t>(S) * d * elem_bytes(dtype);
     const float c_log2e = scale_log2e(scale);
-    // Sync event id -> ctx event (ids: 0 E_main, 1..C E_pack, C+1..2C E_attn,
-    // 2C+1 E_done; the context keeps max_chunks of each kind).
-    auto event_of = [&](int id) -> hipEvent_t {
-        if (id == 0) return ctx->events[0];
-        if (id <= C) return ctx->events[id];
-        if (id <= 2 * C) return ctx->events[1 + ctx->max_chunks + (id - 1 - C)];
-        return ctx->events[1 + 2 * ctx->max_chunks];
-    };
-
-    const bool timed = static_cast<int>(ctx->timed_chunks.size()) < ctx->timing_calls;
-    const size_t call = ctx->timed_chunks.size();
-    for (int i = 0; i < n_ops; ++i) {
-        const hcms_op &op = ctx->plan[i];
-        hipStream_t s = streams[op.stream];
-        if (op.kind == HCMS_OP_RECORD) {
-            e = hipEventRecord(event_of(op.event), s);
-            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-            continue;
-        }
-        if (op.kind == HCMS_OP_WAIT) {
-            e = hipStreamWaitEvent(s, event_of(op.event), 0);
-            if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
-            continue;
-        }
-        const int c = op.chunk;
-        const size_t slot = (call * 3 + (op.kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
-        if (timed) {
-            e = hipEventRecord(ctx->t_begin[slot], s);
-            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-        }
-        const int64_t off = head_bytes * offs[c];
-        const int hc = chunk_sizes[c];
-        if (op.kind == HCMS_OP_PACK) {
+    auto at = [head_bytes](void *p, int h0) { return static_cast<char *>(p) + head_bytes * h0; };
+    auto launch = [&](int kind, int h0, int hc, hipStream_t s) -> hipError_t {
+        if (kind == HCMS_OP_PACK) {
             const void *src[3] = {q_seq, k_seq, v_seq};
-            void *dst[3] = {static_cast<char *>(q_hm) + off, static_cast<char *>(k_hm) + off,
-                            static_cast<char *>(v_hm) + off};
-            e = hcms::launch_pack(src, dst, 3, S, H, offs[c], hc, log2u, s);
-        } else if (op.kind == HCMS_OP_ATTENTION) {
-            e = hcms::launch_attention(static_cast<char *>(q_hm) + off, static_cast<char *>(k_hm) + off,
-                                       static_cast<char *>(v_hm) + off, static_cast<char *>(o_hm) + off,
-                                       nullptr, S, hc, d, c_log2e, dtype, s);
-        } else {
-            e = hcms::launch_unpack(static_cast<char *>(o_hm) + off, o_seq, S, H, offs[c], hc, log2u, s);
+            void *dst[3] = {at(q_hm, h0), at(k_hm, h0), at(v_hm, h0)};
+            return hcms::launch_pack(src, dst, 3, S, H, h0, hc, log2u, s);
         }
-        if (e != hipSuccess) return hip_fail(e, "kernel launch");
-        if (timed) {
-            e = hipEventRecord(ctx->t_end[slot], s);
-            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-        }
+        if (kind == HCMS_OP_ATTENTION)
+            return hcms::launch_attention(at(q_hm, h0), at(k_hm, h0), at(v_hm, h0), at(o_hm, h0),
+                                          lse ? lse + static_cast<int64_t>(h0) * S : nullptr, S, hc,
+                                          d, c_log2e, dtype, s);
+        const void *src[1] = {at(o_hm, h0)};
+        void *dst[1] = {o_seq};
+        return hcms::launch_unpack(src, dst, 1, S, H, h0, hc, log2u, s);
+    };
+    return execute_plan(ctx, mode, chunk_sizes, n_chunks, main_stream, copy_stream, compute_stream,
+                        launch);
+}
+
+int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_seq, void *dv_seq,
+                  const void *q_hm, const void *k_hm, const void *v_hm, const void *o_hm,
+                  const float *lse, void *do_hm, void *dq_hm, void *dk_hm, void *dv_hm,
+                  float *delta, int P, int S, int H, int d, float scale, const int *chunk_sizes,
+                  int n_chunks, int dtype, int mode, void *main_stream, void *copy_stream,
+                  void *compute_stream) {
+    int st;
+    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    const void *all[13] = {q_hm, k_hm, v_hm, o_hm, dout_seq, dq_seq, dk_seq, dv_seq,
+                           do_hm, dq_hm, dk_hm, dv_hm, nullptr};
+    if (S > 0)
+        for (int i = 0; i < 12; ++i)
+            if (!all[i]) return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
+    int log2u = 0;
+    if ((st = check_schedule(ctx, P, S, H, d, scale, chunk_sizes, n_chunks, dtype, &mode, &log2u,
+                             main_stream, copy_stream, compute_stream)) != HCMS_OK)
+        return st;
+    for (int i = 0; i < 12; ++i)
+        if (S > 0 && !aligned16(all[i])) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    // The first five are read only and may alias each other; the seven
+    // written tensors must not overlap anything.
+    const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
+    for (int i = 0; i < 12; ++i)
+        for (int j = i + 1; j < 12; ++j)
+            if (j >= 5 && overlaps(all[i], bytes, all[j], bytes))
+                return fail(HCMS_ERR_ALIAS, "tensor %d overlaps tensor %d", i, j);
+    for (int i = 0; i < 12; i += 4) {
+        const void *const *g = all + i;
+        if ((st = check_stats(lse, "lse", S, H, g[0], g[1], g[2], g[3], d, dtype)) != HCMS_OK) return st;
+        if ((st = check_stats(delta, "delta", S, H, g[0], g[1], g[2], g[3], d, dtype)) != HCMS_OK)
+            return st;
     }
-    if (timed) ctx->timed_chunks.push_back(C);
-    return ok();
+    if (S > 0 && overlaps(lse, int64_t{S} * H * 4, delta, int64_t{S} * H * 4))
+        return fail(HCMS_ERR_ALIAS, "lse and delta overlap");
+    if (S == 0) return ok();
+
+    const int64_t head_bytes = static_cast<int64_t>(S) * d * elem_bytes(dtype);
+    auto at = [head_bytes](const void *p, int h0) {
+        return const_cast<char *>(static_cast<const char *>(p)) + head_bytes * h0;
+    };
+    auto launch = [&](int kind, int h0, int hc, hipStream_t s) -> hipError_t {
+        if (kind == HCMS_OP_PACK) {
+            const void *src[1] = {dout_seq};
+            void *dst[1] = {at(do_hm, h0)};
+            return hcms::launch_pack(src, dst, 1, S, H, h0, hc, log2u, s);
+        }
+        if (kind == HCMS_OP_ATTENTION) {
+            const int64_t so = static_cast<int64_t>(h0) * S;
+            return hcms::launch_attention_backward(at(q_hm, h0), at(k_hm, h0), at(v_hm, h0),
+                                                   at(o_hm, h0), at(do_hm, h0), lse + so,
+                                                   at(dq_hm, h0), at(dk_hm, h0), at(dv_hm, h0),
+                                                   delta + so, S, hc, d, scale, dtype, s);
+        }
+        const void *src[3] = {at(dq_hm, h0), at(dk_hm, h0), at(dv_hm, h0)};
+        void *dst[3] = {dq_seq, dk_seq, dv_seq};
+        return hcms::launch_unpack(src, dst, 3, S, H, h0, hc, log2u, s);
+    };
+    return execute_plan(ctx, mode, chunk_sizes, n_chunks, main_stream, copy_stream, compute_stream,
+                        launch);
 }
 
 }  // extern "C"

@@ -20,9 +20,9 @@ hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors,
                        int64_t S, int64_t H, int64_t h0, int64_t hc, int log2_units,
                        hipStream_t stream);
 
-//   dst[t][h0 + j][:] = src[j][t][:]   (unpack)
-hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64_t h0,
-                         int64_t hc, int log2_units, hipStream_t stream);
+// Each tensor z moves  dst[z][t][h0 + j][:] = src[z][j][t][:]   (unpack)
+hipError_t launch_unpack(const void *const *src, void *const *dst, int n_tensors, int64_t S,
+                         int64_t H, int64_t h0, int64_t hc, int log2_units, hipStream_t stream);
 
 // Attention of `n_heads` consecutive heads, head-major [n_heads][S][d]
 // buffers starting at the chunk's first head.  scale_log2e = scale * log2(e).

@@ -96,13 +96,13 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(PackPtrs p, int64_t S, i
         __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, (tid << 4) + i * (kThreads << 4), 0, 0);
 }
 
-// grid: x = ceil(S * U / kUnitsPerBlock), y = hc.
+// grid: x = ceil(S * U / kUnitsPerBlock), y = hc, z = tensor.
 template <int LOG2U>
-__global__ __launch_bounds__(kThreads) void unpack_kernel(const char *src_all, char *dst_all,
-                                                          int64_t S, int64_t H, int64_t h0) {
+__global__ __launch_bounds__(kThreads) void unpack_kernel(PackPtrs p, int64_t S, int64_t H,
+                                                          int64_t h0) {
     const BlockSpans b = block_spans<LOG2U>(S, H, h0);
-    const __amdgpu_buffer_rsrc_t src = span_rsrc(src_all + b.dense_off, b.dense_left);
-    const __amdgpu_buffer_rsrc_t dst = span_rsrc(dst_all + b.strided_off, b.strided_left);
+    const __amdgpu_buffer_rsrc_t src = span_rsrc(p.src[blockIdx.z] + b.dense_off, b.dense_left);
+    const __amdgpu_buffer_rsrc_t dst = span_rsrc(p.dst[blockIdx.z] + b.strided_off, b.strided_left);
     const uint32_t tid = threadIdx.x;
     const uint32_t so = strided_lane_off<LOG2U>(tid, static_cast<uint32_t>(H));
     const uint32_t step = static_cast<uint32_t>(H) * (kThreads << 4);
@@ -129,9 +129,9 @@ void pack_dispatch(const PackPtrs &p, int n_tensors, int64_t S, int64_t H, int64
 }
 
 template <int LOG2U>
-void unpack_dispatch(const char *src, char *dst, int64_t S, int64_t H, int64_t h0, int64_t hc,
-                     hipStream_t stream) {
-    unpack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, 1), kThreads, 0, stream>>>(src, dst, S, H, h0);
+void unpack_dispatch(const PackPtrs &p, int n_tensors, int64_t S, int64_t H, int64_t h0,
+                     int64_t hc, hipStream_t stream) {
+    unpack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, n_tensors), kThreads, 0, stream>>>(p, S, H, h0);
 }
 
 // Lane offsets on the strided side are 32-bit: a workgroup spans at most
@@ -162,20 +162,23 @@ hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, 
     return hipGetLastError();
 }
 
-hipError_t launch_unpack(const void *src, void *dst, int64_t S, int64_t H, int64_t h0,
-                         int64_t hc, int log2_units, hipStream_t stream) {
+hipError_t launch_unpack(const void *const *src, void *const *dst, int n_tensors, int64_t S,
+                         int64_t H, int64_t h0, int64_t hc, int log2_units, hipStream_t stream) {
     if (S == 0 || hc == 0) return hipSuccess;
-    if (!strided_span_fits(H)) return hipErrorInvalidValue;
-    const char *s = static_cast<const char *>(src);
-    char *d = static_cast<char *>(dst);
+    if (!strided_span_fits(H) || n_tensors < 1 || n_tensors > 3) return hipErrorInvalidValue;
+    PackPtrs p{};
+    for (int z = 0; z < n_tensors; ++z) {
+        p.src[z] = static_cast<const char *>(src[z]);
+        p.dst[z] = static_cast<char *>(dst[z]);
+    }
     switch (log2_units) {
-        case 0: unpack_dispatch<0>(s, d, S, H, h0, hc, stream); break;
-        case 1: unpack_dispatch<1>(s, d, S, H, h0, hc, stream); break;
-        case 2: unpack_dispatch<2>(s, d, S, H, h0, hc, stream); break;
-        case 3: unpack_dispatch<3>(s, d, S, H, h0, hc, stream); break;
-        case 4: unpack_dispatch<4>(s, d, S, H, h0, hc, stream); break;
-        case 5: unpack_dispatch<5>(s, d, S, H, h0, hc, stream); break;
-        case 6: unpack_dispatch<6>(s, d, S, H, h0, hc, stream); break;
+        case 0: unpack_dispatch<0>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 1: unpack_dispatch<1>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 2: unpack_dispatch<2>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 3: unpack_dispatch<3>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 4: unpack_dispatch<4>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 5: unpack_dispatch<5>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 6: unpack_dispatch<6>(p, n_tensors, S, H, h0, hc, stream); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

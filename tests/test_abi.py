@@ -324,8 +324,10 @@ def test_forward_and_ctx_validation(lib):
     assert lib.hcms_ctx_create(0, 0, ctypes.byref(h)) == ECHUNKS
     assert lib.hcms_ctx_destroy(None) == OK
     sizes = (ctypes.c_int * 2)(2, 2)
-    assert lib.hcms_forward(None, A, B, C_, D_, A + 2**24, B + 2**24, C_ + 2**24, D_ + 2**24,
+    assert lib.hcms_forward(None, A, B, C_, D_, A + 2**24, B + 2**24, C_ + 2**24, D_ + 2**24, None,
                             4, 512, 4, 64, 0.125, sizes, 2, 1, 1, None, None, None) == ENULL
+    assert lib.hcms_backward(None, A, B, C_, D_, A, B, C_, D_, None, A, B, C_, D_, None,
+                             4, 512, 4, 64, 0.125, sizes, 2, 1, 1, None, None, None) == ENULL
     assert lib.hcms_ctx_set_timing(None, 1) == ENULL
     buf = (ctypes.c_float * 4)()
     assert lib.hcms_ctx_kernel_ms(None, hcms.OP_ATTENTION, buf, 4) == ENULL

@@ -128,3 +128,98 @@ def test_backward_wan_p8_sampled_and_gradient_sums(hcms, oracle_mod):
         # The sums cancel over 56160 rows; bound them by the rows' magnitudes.
         assert float(sk.abs().max()) <= GRAD_TOL * float(dk[h].double().abs().sum(dim=0).max())
         assert float((sv.cpu() - sg).abs().max()) <= GRAD_TOL * float(sg.abs().max() + 1)
+
+
+# ---------------------------------------------------------------------------
+# The reverse pipeline (hcms_backward) and autograd
+# ---------------------------------------------------------------------------
+def _seq_case(name):
+    w = inputs.WORKLOADS[name]
+    qs, ks, vs = (x.cuda() for x in inputs.make_qkv(w))
+    dos = inputs.make_dout(w).cuda()
+    return w, qs, ks, vs, dos
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "wan_p4"])
+def test_backward_pipeline_bitwise_across_modes_and_chunkings(hcms, name):
+    """hcms_backward (pack dO, backward, unpack dQ/dK/dV on the forward's plan)
+    equals the direct backward on torch-transposed inputs, bitwise, for every
+    mode and chunking."""
+    w, qs, ks, vs, dos = _seq_case(name)
+    log(f"[backward pipeline] {name}")
+    hm = [x.permute(1, 0, 2).contiguous() for x in (qs, ks, vs, dos)]
+    out, lse = hcms.attention_lse(hm[0], hm[1], hm[2], w.scale)
+    ref = [t.permute(1, 0, 2).contiguous()
+           for t in hcms.attention_backward(hm[0], hm[1], hm[2], out, hm[3], lse, w.scale)]
+    ctx = hcms.Context(max_chunks=16)
+    for sizes in w.chunkings:
+        for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED, hcms.MODE_INLINE, hcms.MODE_LANES,
+                     hcms.MODE_AUTO):
+            ws = [torch.empty_like(hm[0]) for _ in range(4)]
+            lse2 = torch.empty_like(lse)
+            o2 = ctx.forward(qs, ks, vs, w.P, w.scale, sizes, mode=mode, workspaces=ws, lse=lse2)
+            got = ctx.backward(dos, w.P, w.scale, sizes, ws, lse2, mode=mode)
+            assert torch.equal(bits(lse2), bits(lse)), (name, sizes, mode, "lse")
+            assert torch.equal(bits(o2), bits(out.permute(1, 0, 2))), (name, sizes, mode, "out")
+            for a, b, nm in zip(got, ref, ("dq", "dk", "dv")):
+                assert torch.equal(bits(a), bits(b)), (name, sizes, mode, nm)
+    ctx.close()
+
+
+def test_autograd_matches_oracle(hcms, oracle_mod):
+    """loss = <dO, attention(Q, K, V)> through HcmsAttention: loss.backward()
+    gives the oracle's gradients (Tiny, fp32 storage, chunks 2 + 2)."""
+    w, qs, ks, vs, dos = _seq_case("tiny")
+    q, k, v = (x.clone().requires_grad_(True) for x in (qs, ks, vs))
+    ctx = hcms.Context()
+    out = hcms.HcmsAttention.apply(q, k, v, ctx, w.P, w.scale, (2, 2), hcms.MODE_LANES)
+    (out * dos).sum().backward()
+    for h in range(w.H):
+        Q, K, V, G = (x[:, h].double().cpu().numpy() for x in (qs, ks, vs, dos))
+        rq, rk, rv = oracle_mod.attention_backward_head(Q, K, V, G, w.scale)
+        for name, got, want in (("dq", q.grad, rq), ("dk", k.grad, rk), ("dv", v.grad, rv)):
+            _check_grad(got[:, h].double().cpu().numpy(), want, f"autograd {name} head {h}")
+    ctx.close()
+
+
+def _delay(stream, cycles=40_000_000):
+    with torch.cuda.stream(stream):
+        torch.cuda._sleep(cycles)
+
+
+@pytest.mark.parametrize("mode", ["pipelined", "inline", "lanes"])
+@pytest.mark.parametrize("late", ["copy", "compute", "main"])
+def test_backward_pipeline_respects_events_under_delay(hcms, late, mode):
+    """Poison the backward workspaces and outputs, delay one stream with a
+    bounded spin kernel, read the gradients on the main stream right after the
+    call returns: a missing wait would expose poison or stale values."""
+    w, qs, ks, vs, dos = _seq_case("small")
+    m = {"pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES}[mode]
+    sizes = (3, 3, 2)
+    ctx = hcms.Context(max_chunks=8)
+    ws = [torch.empty((w.H, w.S, w.d), dtype=qs.dtype, device="cuda") for _ in range(4)]
+    lse = torch.empty((w.H, w.S), dtype=torch.float32, device="cuda")
+    ctx.forward(qs, ks, vs, w.P, w.scale, sizes, mode=hcms.MODE_SERIAL, workspaces=ws, lse=lse)
+    ref = [t.clone() for t in ctx.backward(dos, w.P, w.scale, sizes, ws, lse, mode=hcms.MODE_SERIAL)]
+    torch.cuda.synchronize()
+    bws = ctx.backward_workspaces(w.S, w.H, w.d, qs.dtype)
+    outs = [torch.empty_like(qs) for _ in range(3)]
+    for t in (*bws[:4], *outs):
+        t.view(torch.int16).fill_(0x7FC1)
+    bws[4].fill_(float("nan"))
+    d_in = dos
+    if late == "main":
+        d_in = torch.empty_like(dos)
+        d_in.view(torch.int16).fill_(0x7FC1)
+        torch.cuda.synchronize()
+        _delay(torch.cuda.current_stream())
+        d_in.copy_(dos)
+    else:
+        torch.cuda.synchronize()
+        _delay(ctx.copy_stream if late == "copy" else ctx.compute_stream)
+    ctx.backward(d_in, w.P, w.scale, sizes, ws, lse, mode=m, dq=outs[0], dk=outs[1], dv=outs[2])
+    seen = [t.clone() for t in outs]   # on the main stream, no host sync in between
+    torch.cuda.synchronize()
+    for a, b, nm in zip(seen, ref, ("dq", "dk", "dv")):
+        assert torch.equal(bits(a), bits(b)), (late, mode, nm)
+    ctx.close()
