@@ -226,6 +226,66 @@ def time_model_sweep(ctx, w, reps: int, dev):
     return res
 
 
+def training_step(ctx, w, chunks, reps: int, dev):
+    """Forward (keeping the softmax statistic) and backward of the hot path,
+    per step: the auto schedule against serial, interleaved; the backward
+    attention launches' roofline (algorithmic 10 S^2 H d FLOP: the five
+    products Q K^T, dO V^T, P^T dO, dS K, dS^T Q)."""
+    q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
+    dout = inputs.make_dout(w).to(dev)
+    fws = [torch.empty((w.H, w.S, w.d), dtype=q.dtype, device=dev) for _ in range(4)]
+    lse = torch.empty((w.H, w.S), dtype=torch.float32, device=dev)
+    out = torch.empty_like(q)
+    grads = [torch.empty_like(q) for _ in range(3)]
+
+    def fwd(mode):
+        ctx.forward(q, k, v, w.P, w.scale, chunks, mode=mode, out=out, workspaces=fws, lse=lse)
+
+    def bwd(mode):
+        ctx.backward(dout, w.P, w.scale, chunks, fws, lse, mode=mode, dq=grads[0], dk=grads[1],
+                     dv=grads[2])
+
+    for _ in range(3):
+        fwd(hcms.MODE_AUTO)
+        bwd(hcms.MODE_AUTO)
+    times = {m: {"fwd": [], "bwd": []} for m in ("serial", "auto")}
+    for r in range(reps + 1):
+        for m in (("serial", "auto") if r % 2 == 0 else ("auto", "serial")):
+            tf = time_region(lambda: fwd(MODES[m]), 1)
+            tb = time_region(lambda: bwd(MODES[m]), 1)
+            if r > 0:
+                times[m]["fwd"] += tf
+                times[m]["bwd"] += tb
+    ctx.set_timing(reps)
+    for _ in range(reps):
+        bwd(hcms.MODE_SERIAL)
+    torch.cuda.synchronize()
+    attn_ms = ctx.kernel_ms(hcms.OP_ATTENTION)
+    ctx.set_timing(0)
+    C = len(chunks)
+    alg = [10.0 * w.S * w.S * chunks[i % C] * w.d for i in range(len(attn_ms))]
+    achieved = sum(alg) / (sum(attn_ms) * 1e-3) / 1e12
+    res = {"workload": w.name, "chunks": list(chunks)}
+    for m in times:
+        f = quartiles(times[m]["fwd"])
+        b = quartiles(times[m]["bwd"])
+        res[m] = {"forward_ms": f, "backward_ms": b,
+                  "step_ms": round(f["median"] + b["median"], 4),
+                  "step_TFLOPs": round(14.0 * w.S * w.S * w.H * w.d /
+                                       ((f["median"] + b["median"]) * 1e-3) / 1e12, 2)}
+    res["auto_runs"] = MODE_NAMES[ctx.last_mode]
+    res["backward_roofline"] = {
+        "bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+        "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+        "kernels": "attention_dq_kernel<128, bf16> + attention_dkdv_kernel<128, bf16>",
+        "per_launch": f"10*S^2*H_c*d FLOP per chunk (executed: 14*S^2*H_c*d, Q K^T and dO V^T "
+                      f"are computed in both launches); avg {statistics.mean(attn_ms):.4f} ms over "
+                      f"{len(attn_ms)} chunk backward launches, serial schedule"}
+    res["note"] = "step_TFLOPs counts 4 S^2 H d (forward) + 10 S^2 H d (backward)"
+    del q, k, v, dout, fws, lse, out, grads
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -391,6 +451,9 @@ def main():
         for ch in ((5, 5), (10,)):
             cmp.append(compare_modes(ctx, wp4, ch, reps, dev))
         result["schedules"] = cmp
+
+        # ---- training: forward with the softmax statistic, then backward ----
+        result["training"] = training_step(ctx, w, sizes, max(10, args.steps // 4), dev)
 
         # ---- the time model over the chunk count (Wan-P8, Wan-P4) ----
         result["time_model"] = [time_model_sweep(ctx, tw, reps, dev)
