@@ -17,19 +17,22 @@
 // does not depend on the chunking:
 //   * attention_dq_kernel, query-parallel (the forward's decomposition): a
 //     wave owns 32 queries, keeps Q and dO as MFMA B operands in registers and
-//     walks the key blocks.  Per block, S^T = K Q^T and dP^T = V dO^T (K and V
-//     row-major in LDS), then dS, then dQ^T += K^T dS^T with K^T stored
-//     transposed in LDS, keys permuted like V^T in the forward so that dS
-//     leaves the accumulator layout directly as the B operand.  Its prologue
-//     computes D_i from dO and O and stores it for the second launch.
-//   * attention_dkdv_kernel, key-parallel: a wave owns 32 keys, keeps K and V
-//     as B operands, and walks blocks of 32 queries.  Per block, S = Q K^T and
+//     walks the key blocks, one 32-key half at a time: S^T = K Q^T and
+//     dP^T = V dO^T (K and V row-major in LDS), then dS, then
+//     dQ^T += K^T dS^T with K^T stored transposed in LDS, keys permuted like
+//     V^T in the forward so that dS leaves the accumulator layout directly as
+//     the B operand.  Its prologue computes D_i from dO and O and stores it
+//     for the second launch.
+//   * attention_dkdv_kernel, key-parallel: a wave owns 32 keys, keeps K as B
+//     operands in registers (the workgroup's V rows sit in LDS for the whole
+//     launch), and walks blocks of 32 queries.  Per block, S = Q K^T and
 //     dP = dO V^T put one key per lane (the column) and 16 queries per lane
 //     (rows), so P and dS are already B operands of dV^T += dO^T P and
 //     dK^T += Q^T dS, with dO^T and Q^T transposed in LDS, queries permuted.
-// Both hold four waves per workgroup, one per SIMD: the register sets
-// (Q, dO, dQ^T, S^T, dP^T; or K, V, dK^T, dV^T, S, dP, the per-row L and D)
-// need more than the 256 registers two waves per SIMD would leave.
+// Both run two waves per SIMD (8 waves per workgroup at d = 128, 4 waves and
+// two workgroups per CU at d = 64): the 32-key halves in the first kernel
+// and V in LDS in the second keep each wave within 256 registers, so one
+// wave's MFMAs overlap the other's exponentials and LDS reads.
 //
 // Tails: loads go through buffer resources bounded by the head's tensor (rows
 // >= S read as zeros); keys or queries past S get P = 0 and are not stored.
@@ -41,8 +44,14 @@ namespace {
 
 using namespace tiles;
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+// Query-parallel kernel: 8 waves (d = 128) or 4 waves at two workgroups per
+// CU (d = 64), two waves per SIMD either way.
+template <int D>
+struct QTile {
+    static constexpr int waves = D == 128 ? 8 : 4;
+    static constexpr int threads = 64 * waves;
+    static constexpr int per_cu = 8 / waves;
+};
 constexpr int kQB = 32;  // queries per block of the key-parallel kernel
 
 // Transposed tiles of 32 queries: [D][kQB + 8], the same 16-byte padding as
@@ -87,7 +96,7 @@ __device__ inline f32x16 rows_times_regs(const __bf16 *a, int rs, const bf16x8 (
 // dQ (and D): query-parallel
 // ---------------------------------------------------------------------------
 template <int D, typename T>
-__global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
+__global__ __launch_bounds__(QTile<D>::threads, QTile<D>::per_cu) void attention_dq_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ o, const T *__restrict__ dout, const float *__restrict__ lse,
     T *__restrict__ dq, float *__restrict__ delta, int S, int n_qtiles, float c, float scale) {
@@ -109,7 +118,7 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int li = lane & 31, g = lane >> 5;
-    const int qi = qtile * (kQW * kWaves) + wave * kQW + li;
+    const int qi = qtile * (kQW * QTile<D>::waves) + wave * kQW + li;
 
     bf16x8 qreg[KK], doreg[KK];
     float dpart = 0.f;
@@ -137,7 +146,7 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
 
     // Staging: V in the row pattern, K in the key-pair pattern (written both
     // row-major and transposed).
-    Stage<D, T, kWaves> st;
+    Stage<D, T, QTile<D>::waves> st;
     st.load(vr, kr, 0, 0, tid);
     st.store_k(vbuf[0], tid);
     st.store_v_rows(kbuf[0], tid);
@@ -147,27 +156,21 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
     for (int j = 0; j < nkb; ++j) {
         const int b = j & 1;
         if (j + 1 < nkb) st.load(vr, kr, j + 1, j + 1, tid);
-        f32x16 sacc[2], dpacc[2];
+        const int kvalid = S - j * kBC;
+        // The block's two 32-key halves one after the other: S^T and dP^T of
+        // the half, dS, then its two 16-key steps of dQ^T += K^T dS^T.
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt) {
-            sacc[mt] = f32x16{};
-            dpacc[mt] = f32x16{};
+            f32x16 sacc = {}, dpacc = {};
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
                 const int row = (mt * 32 + li) * Lds<D>::KS + kk * 16 + g * 8;
                 const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kbuf[b] + row);
                 const bf16x8 va = *reinterpret_cast<const bf16x8 *>(vbuf[b] + row);
-                sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc[mt], 0, 0, 0);
-                dpacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc[mt], 0, 0, 0);
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
             }
-        }
-        // dS^T in the accumulator layout: lane (g, query li), keys
-        // 32 mt + 8 (r / 4) + 4 g + r % 4; packed as the B operands of the
-        // four 16-key steps (keys permuted as in the forward's P).
-        const int kvalid = S - j * kBC;
-        bf16x8 dsb[4];
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
+            bf16x8 dsb[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 f32x8 x;
@@ -176,19 +179,21 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
                     const int rr = h * 8 + r;
                     const int key = mt * 32 + (rr >> 2) * 8 + g * 4 + (rr & 3);
                     const float p = key < kvalid
-                        ? __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][rr], c, -Li)) : 0.f;
-                    x[r] = p * (dpacc[mt][rr] - Di);
+                        ? __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rr], c, -Li)) : 0.f;
+                    x[r] = p * (dpacc[rr] - Di);
                 }
-                dsb[mt * 2 + h] = __builtin_convertvector(x, bf16x8);
+                dsb[h] = __builtin_convertvector(x, bf16x8);
             }
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
+            for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
-                    ktbuf[b] + (dt * 32 + li) * Lds<D>::VS + (ks * 2 + g) * 8);
-                dqacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[ks], dqacc[dt], 0, 0, 0);
-            }
+                for (int h = 0; h < 2; ++h) {
+                    const int ks = mt * 2 + h;
+                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                        ktbuf[b] + (dt * 32 + li) * Lds<D>::VS + (ks * 2 + g) * 8);
+                    dqacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[h], dqacc[dt], 0, 0, 0);
+                }
+        }
         if (j + 1 < nkb) {
             st.store_k(vbuf[b ^ 1], tid);
             st.store_v_rows(kbuf[b ^ 1], tid);
@@ -213,15 +218,26 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dq_kernel(
 // ---------------------------------------------------------------------------
 // dK, dV: key-parallel
 // ---------------------------------------------------------------------------
-// Staging of one block of 32 queries: Q and dO in query pairs (row-major and
-// transposed stores), L and D as 32 floats each.
+// Key-parallel kernel: 8 waves (d = 128) or 4 waves at two workgroups per CU
+// (d = 64); a wave owns 32 keys.
+template <int D>
+struct KTile {
+    static constexpr int waves = D == 128 ? 8 : 4;
+    static constexpr int threads = 64 * waves;
+    static constexpr int per_cu = 8 / waves;
+    static constexpr int keys = kQW * waves;
+};
+
+// Staging of one block of 32 queries: Q (first half of the threads) and dO
+// (second half) in query pairs, stored row-major and transposed; L and D as 32
+// floats each.
 template <int D, typename T>
 struct QStage {
     static constexpr int CH = D / 8;
     static constexpr unsigned ROWB = D * sizeof(T), CHB = 8 * sizeof(T);
-    static constexpr int TASKS = (kQB / 2) * CH;  // (query pair, chunk) tasks
-    static_assert(TASKS <= kThreads, "one task per thread at most");
-    u32x4 qv[2], dv[2];
+    static constexpr int TASKS = (kQB / 2) * CH;  // (query pair, chunk) tasks per tensor
+    static_assert(2 * TASKS <= KTile<D>::threads, "one task per thread at most");
+    u32x4 x[2];
     f32x4 stat;
 
     __device__ static int pair(int t) { return t & 15; }
@@ -230,12 +246,11 @@ struct QStage {
     __device__ void load(__amdgpu_buffer_rsrc_t qr, __amdgpu_buffer_rsrc_t dr,
                          __amdgpu_buffer_rsrc_t lr, __amdgpu_buffer_rsrc_t er, int blk, int tid) {
         const unsigned q0 = static_cast<unsigned>(blk) * kQB;
-        if (tid < TASKS) {
-            const unsigned off = (q0 + 2 * pair(tid)) * ROWB + chunk(tid) * CHB;
-            qv[0] = load8<T>(qr, off);
-            qv[1] = load8<T>(qr, off + ROWB);
-            dv[0] = load8<T>(dr, off);
-            dv[1] = load8<T>(dr, off + ROWB);
+        if (tid < 2 * TASKS) {
+            const int t = tid % TASKS;
+            const unsigned off = (q0 + 2 * pair(t)) * ROWB + chunk(t) * CHB;
+            x[0] = load8<T>(tid < TASKS ? qr : dr, off);
+            x[1] = load8<T>(tid < TASKS ? qr : dr, off + ROWB);
         }
         // Threads 0..7 fetch L, 8..15 fetch D, 4 floats each.
         if (tid < 16) {
@@ -247,23 +262,17 @@ struct QStage {
 
     __device__ void store(__bf16 *qrow, __bf16 *drow, __bf16 *qt, __bf16 *dt, float *ls, float *ds,
                           int tid) const {
-        if (tid < TASKS) {
-            const int p = pair(tid), ch = chunk(tid);
-            __bf16 *a = qrow + 2 * p * QLds<D>::RS + ch * 8;
-            __bf16 *b = drow + 2 * p * QLds<D>::RS + ch * 8;
-            *reinterpret_cast<u32x4 *>(a) = qv[0];
-            *reinterpret_cast<u32x4 *>(a + QLds<D>::RS) = qv[1];
-            *reinterpret_cast<u32x4 *>(b) = dv[0];
-            *reinterpret_cast<u32x4 *>(b + QLds<D>::RS) = dv[1];
-            __bf16 *ta = qt + ch * 8 * QLds<D>::TS + vt_pos(2 * p);
-            __bf16 *tb = dt + ch * 8 * QLds<D>::TS + vt_pos(2 * p);
+        if (tid < 2 * TASKS) {
+            const int t = tid % TASKS, p = pair(t), ch = chunk(t);
+            __bf16 *r = (tid < TASKS ? qrow : drow) + 2 * p * QLds<D>::RS + ch * 8;
+            *reinterpret_cast<u32x4 *>(r) = x[0];
+            *reinterpret_cast<u32x4 *>(r + QLds<D>::RS) = x[1];
+            __bf16 *tp = (tid < TASKS ? qt : dt) + ch * 8 * QLds<D>::TS + vt_pos(2 * p);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
-                *reinterpret_cast<unsigned *>(ta + e * QLds<D>::TS) =
-                    __builtin_amdgcn_perm(qv[1][e >> 1], qv[0][e >> 1], sel);
-                *reinterpret_cast<unsigned *>(tb + e * QLds<D>::TS) =
-                    __builtin_amdgcn_perm(dv[1][e >> 1], dv[0][e >> 1], sel);
+                *reinterpret_cast<unsigned *>(tp + e * QLds<D>::TS) =
+                    __builtin_amdgcn_perm(x[1][e >> 1], x[0][e >> 1], sel);
             }
         }
         if (tid < 16) *reinterpret_cast<f32x4 *>((tid < 8 ? ls : ds) + (tid & 7) * 4) = stat;
@@ -271,11 +280,12 @@ struct QStage {
 };
 
 template <int D, typename T>
-__global__ __launch_bounds__(kThreads, 1) void attention_dkdv_kernel(
+__global__ __launch_bounds__(KTile<D>::threads, KTile<D>::per_cu) void attention_dkdv_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v,
     const T *__restrict__ dout, const float *__restrict__ lse, const float *__restrict__ delta,
     T *__restrict__ dk, T *__restrict__ dv, int S, int n_ktiles, float c, float scale) {
-    constexpr int KK = D / 16, DT = D / 32;
+    constexpr int KK = D / 16, DT = D / 32, NT = KTile<D>::threads;
+    __shared__ __attribute__((aligned(16))) __bf16 vrows[KTile<D>::keys * QLds<D>::RS];
     __shared__ __attribute__((aligned(16))) __bf16 qbuf[2][QLds<D>::R];
     __shared__ __attribute__((aligned(16))) __bf16 dbuf[2][QLds<D>::R];
     __shared__ __attribute__((aligned(16))) __bf16 qtbuf[2][QLds<D>::TT];
@@ -297,15 +307,22 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dkdv_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int li = lane & 31, g = lane >> 5;
-    const int kj = ktile * (kQW * kWaves) + wave * kQW + li;
+    const int key0 = ktile * KTile<D>::keys;
+    const int kj = key0 + wave * kQW + li;
 
-    // K^T and V^T as B operands: lane (g, key li) holds head dims 16 kk + 8 g + [0, 8).
-    bf16x8 kreg[KK], vreg[KK];
+    // K^T as B operands in registers: lane (g, key li) holds head dims
+    // 16 kk + 8 g + [0, 8).  The workgroup's V rows go to LDS once.
+    bf16x8 kreg[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-        const unsigned off = static_cast<unsigned>(kj * D + kk * 16 + g * 8) * sizeof(T);
-        kreg[kk] = __builtin_bit_cast(bf16x8, load8<T>(kr, off));
-        vreg[kk] = __builtin_bit_cast(bf16x8, load8<T>(vr, off));
+    for (int kk = 0; kk < KK; ++kk)
+        kreg[kk] = __builtin_bit_cast(
+            bf16x8, load8<T>(kr, static_cast<unsigned>(kj * D + kk * 16 + g * 8) * sizeof(T)));
+    constexpr int CH = D / 8;
+#pragma unroll
+    for (int i = 0; i < KTile<D>::keys * CH / NT; ++i) {
+        const int u = tid + i * NT, row = u / CH, ch = u % CH;
+        *reinterpret_cast<u32x4 *>(vrows + row * QLds<D>::RS + ch * 8) =
+            load8<T>(vr, static_cast<unsigned>((key0 + row) * D + ch * 8) * sizeof(T));
     }
     f32x16 dkacc[DT], dvacc[DT];
 #pragma unroll
@@ -314,6 +331,7 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dkdv_kernel(
         dvacc[dt] = f32x16{};
     }
     const int nqb = (S + kQB - 1) / kQB;
+    const __bf16 *vmine = vrows + (wave * kQW + li) * QLds<D>::RS + g * 8;
 
     QStage<D, T> st;
     st.load(qr, dr, lr, er, 0, tid);
@@ -324,8 +342,16 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dkdv_kernel(
         const int b = i & 1;
         if (i + 1 < nqb) st.load(qr, dr, lr, er, i + 1, tid);
         // S and dP: lane (g, key li), rows = queries 8 (r / 4) + 4 g + r % 4.
-        const f32x16 s = rows_times_regs<D>(qbuf[b], QLds<D>::RS, kreg, li, g);
-        const f32x16 dp = rows_times_regs<D>(dbuf[b], QLds<D>::RS, vreg, li, g);
+        f32x16 s = {}, dp = {};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const int off = li * QLds<D>::RS + kk * 16 + g * 8;
+            const bf16x8 qa = *reinterpret_cast<const bf16x8 *>(qbuf[b] + off);
+            const bf16x8 da = *reinterpret_cast<const bf16x8 *>(dbuf[b] + off);
+            const bf16x8 vb = *reinterpret_cast<const bf16x8 *>(vmine + kk * 16);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], s, 0, 0, 0);
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
+        }
         const int qvalid = S - i * kQB;
         bf16x8 pb[2], dsb[2];
 #pragma unroll
@@ -347,8 +373,6 @@ __global__ __launch_bounds__(kThreads, 1) void attention_dkdv_kernel(
             pb[h] = __builtin_convertvector(p, bf16x8);
             dsb[h] = __builtin_convertvector(ds, bf16x8);
         }
-        // dV^T += dO^T P and dK^T += Q^T dS over the block's 32 queries (two
-        // 16-query steps; transposed rows hold the queries permuted).
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -386,17 +410,18 @@ hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const v
                             const void *dout, const float *lse, void *dq, void *dk, void *dv,
                             float *delta, int S, int n_heads, float c, float scale,
                             hipStream_t stream) {
-    constexpr int BR = kQW * kWaves;
-    const int n_tiles = (S + BR - 1) / BR;
+    const int n_qt = (S + kQW * QTile<D>::waves - 1) / (kQW * QTile<D>::waves);
+    const int64_t qblocks = static_cast<int64_t>(n_qt) * n_heads;
+    const int n_tiles = (S + KTile<D>::keys - 1) / KTile<D>::keys;
     const int64_t blocks = static_cast<int64_t>(n_tiles) * n_heads;
-    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    attention_dq_kernel<D, T><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+    if (blocks > 0x7fffffff || qblocks > 0x7fffffff) return hipErrorInvalidValue;
+    attention_dq_kernel<D, T><<<static_cast<unsigned>(qblocks), QTile<D>::threads, 0, stream>>>(
         static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
         static_cast<const T *>(o), static_cast<const T *>(dout), lse, static_cast<T *>(dq), delta, S,
-        n_tiles, c, scale);
+        n_qt, c, scale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    attention_dkdv_kernel<D, T><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+    attention_dkdv_kernel<D, T><<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
         static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
         static_cast<const T *>(dout), lse, delta, static_cast<T *>(dk), static_cast<T *>(dv), S,
         n_tiles, c, scale);
