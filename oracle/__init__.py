@@ -23,6 +23,10 @@ Contents, each a plain statement of what the paper defines:
   respect to Q, K and V for a given output gradient, by the chain rule through
   the row softmax, in C (``hcms_oracle.c``).
 
+Modules beside this one: ``oracle.time_model`` (the appendix's time model) and
+``oracle.layer`` (QKV projection, rotary position embedding and output
+projection around the hot path, Alg. 1's main-stream steps).
+
 Every function here is pinned by tests in ``tests/test_oracle.py`` against
 values the paper prints (the uneven-partition table), closed forms, invariants
 and a library routine (PyTorch's CPU scaled-dot-product attention in fp64).
