@@ -15,7 +15,9 @@
 //     kernels occupy part of the GPU can never be queued behind two running
 //     ones on the same CU, and every staged K/V block feeds 256 queries;
 //   * K and V blocks are staged in LDS by all threads (global -> registers ->
-//     LDS), K one block ahead of V, each double-buffered;
+//     LDS), K one block ahead of V, each double-buffered.  With bf16 storage
+//     two register sets alternate, so each block's global loads are issued a
+//     whole step before its LDS stores and their latency is hidden;
 //   * scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: keys are the M dimension and queries the N
 //     dimension.  In the accumulator layout each lane then holds one query
@@ -26,22 +28,22 @@
 //     never leaves registers.  V is stored transposed in LDS ([d][key]) with the
 //     keys of every 16-key group permuted (bits 2 and 3 of the key index
 //     swapped) to match the order in which the accumulator rows arrive;
-//   * software pipeline: while the VALU computes the softmax of block j, the
-//     MFMA unit already computes the scores of block j + 1 (no dependency
-//     between the two), then O^T += V_j^T P_j^T.  The K operands of the score
-//     MFMAs are read from LDS four MFMAs ahead; the loop is unrolled by two so
-//     the score registers alternate roles instead of being copied;
-//   * lazy rescaling: the running maximum used for the exponentials is only
-//     raised when a block's maximum exceeds it by more than 2^8 in the exp2
-//     domain.  Exponentials are then at most 2^8, which bf16 and fp32 hold
-//     exactly in range; the final O / l is unchanged.  The decision is taken per
-//     query (per lane); a wave only skips the multiply when no lane needs it,
-//     and a lane that does not need it multiplies by exactly 1.  So the
-//     arithmetic of every query depends only on its own row, never on which
-//     other queries share the wave, tile, chunk or launch: any head chunking
-//     gives bit-identical results;
+//   * software pipeline: while the VALU computes the exponentials of block j,
+//     the MFMA unit already computes the scores of block j + 1 (no dependency
+//     between the two), then O^T += V_j^T P_j^T.  K and V operands are read
+//     from LDS four MFMAs ahead (the first V operands before the overflow
+//     test below); scheduling hints spread the exponentials between the score
+//     MFMAs and the next blocks' LDS stores between the PV MFMAs.  The loop is
+//     unrolled by two so the score registers alternate roles instead of being
+//     copied;
 //   * exp2 is the hardware v_exp_f32 on the argument s * c - m * c (one FMA),
 //     c = scale * log2(e);
+//   * lazy rescaling: the running maximum m is set by block 0 and raised only
+//     when a block's exponentials, summed over its 64 keys, exceed 2^8; that
+//     block is then recomputed against its own maximum and O and l are
+//     rescaled.  So the common path computes no maximum at all, every
+//     exponential used is at most 2^8 (bf16 and fp32 hold it exactly in
+//     range), and the final O / l is unchanged;
 //   * P is rounded to bf16 (nearest-even, v_cvt_pk_bf16_f32) for the PV MFMA;
 //     the row sum l adds exactly these rounded values (v_dot2c_f32_bf16 with a
 //     (1, 1) pair), so the weights that multiply V are normalised exactly; all
@@ -56,16 +58,21 @@
 #include "attention_tiles.h"
 #include "hcms_internal.h"
 
+#ifndef HCMS_ATTN_NT128
+#define HCMS_ATTN_NT128 1
+#endif
+
 namespace hcms {
 namespace {
 
 using namespace tiles;
 
-// S^T[mt] = K[mt] Q^T for the 64 keys of a block (2 tiles of 32 keys); the
-// K operands are read from LDS four MFMAs ahead of their use.
-template <int D>
-__device__ inline void qk_mfma(f32x16 (&sacc)[2], const __bf16 *ks, const bf16x8 (&qreg)[D / 16],
-                               int li, int g) {
+// S^T[nt][mt] = K[mt] Q[nt]^T for the 64 keys of a block (2 tiles of 32
+// keys) and the wave's NT tiles of 32 queries; every K operand read from LDS
+// feeds NT MFMAs, and the reads run four operands ahead of their use.
+template <int D, int NT>
+__device__ inline void qk_mfma(f32x16 (&sacc)[NT][2], const __bf16 *ks,
+                               const bf16x8 (&qreg)[NT][D / 16], int li, int g) {
     constexpr int N = 2 * (D / 16);
     constexpr int AHEAD = 4;
     bf16x8 a[N];
@@ -73,66 +80,147 @@ __device__ inline void qk_mfma(f32x16 (&sacc)[2], const __bf16 *ks, const bf16x8
     for (int i = 0; i < AHEAD; ++i)
         a[i] = *reinterpret_cast<const bf16x8 *>(ks + ((i & 1) * 32 + li) * Lds<D>::KS + ((i >> 1) * 2 + g) * 8);
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) sacc[mt] = f32x16{};
-#pragma unroll
     for (int i = 0; i < N; ++i) {
         if (i + AHEAD < N) {
             const int n = i + AHEAD;
             a[n] = *reinterpret_cast<const bf16x8 *>(ks + ((n & 1) * 32 + li) * Lds<D>::KS + ((n >> 1) * 2 + g) * 8);
         }
-        sacc[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], qreg[i >> 1], sacc[i & 1], 0, 0, 0);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            sacc[nt][i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                a[i], qreg[nt][i >> 1], i < 2 ? f32x16{} : sacc[nt][i & 1], 0, 0, 0);
     }
 }
 
-// O^T[dt] += V^T[dt] P^T over the 64 keys of a block (4 k-steps of 16 keys).
+// O^T[dt][nt] += V^T[dt] P[nt]^T over the 64 keys of a block (4 k-steps of 16
+// keys); every V operand read from LDS feeds NT MFMAs.  The first AHEAD
+// operands come in `pre` (read earlier by pv_prefetch), the others are read
+// AHEAD MFMAs ahead of their use.
+constexpr int kPvAhead = 4;
+
+// Operand i = (ks, dt) = (i / DT, i % DT): consecutive MFMAs update different
+// O^T tiles, so none waits for the result of the one before it; each tile
+// still accumulates its four k-steps in order.
 template <int D>
-__device__ inline void pv_mfma(f32x16 (&oacc)[D / 32], const bf16x8 (&pb)[4], const __bf16 *vts,
-                               int li, int g) {
+__device__ inline const bf16x8 &vt_operand(const __bf16 *vts, int i, int li, int g) {
+    constexpr int DT = D / 32;
+    return *reinterpret_cast<const bf16x8 *>(vts + ((i % DT) * 32 + li) * Lds<D>::VS + ((i / DT) * 2 + g) * 8);
+}
+
+template <int D>
+__device__ inline void pv_prefetch(bf16x8 (&pre)[kPvAhead], const __bf16 *vts, int li, int g) {
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) {
+    for (int i = 0; i < kPvAhead; ++i) pre[i] = vt_operand<D>(vts, i, li, g);
+}
+
+template <int D, int NT>
+__device__ inline void pv_mfma(f32x16 (&oacc)[D / 32][NT], const bf16x8 (&pb)[NT][4],
+                               const __bf16 *vts, const bf16x8 (&pre)[kPvAhead], int li, int g) {
+    constexpr int N = 4 * (D / 32);
+    bf16x8 a[N];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(vts + (dt * 32 + li) * Lds<D>::VS +
-                                                                (ks * 2 + g) * 8);
-            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[dt], 0, 0, 0);
+    for (int i = 0; i < kPvAhead; ++i) a[i] = pre[i];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        if (i + kPvAhead < N) a[i + kPvAhead] = vt_operand<D>(vts, i + kPvAhead, li, g);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            oacc[i % (D / 32)][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                a[i], pb[nt][i / (D / 32)], oacc[i % (D / 32)][nt], 0, 0, 0);
+    }
+}
+
+// Scheduling hints.  First half of a step: block j's exponentials (FMA,
+// v_exp_f32, bf16 conversion and row sum) fill the LDS latency of the first K
+// operand reads and then run between block j + 1's score MFMAs, about 6 VALU
+// instructions per MFMA, so the VALU works while the MFMA unit is busy; the
+// first V operands of the PV MFMAs are read before the overflow test.
+template <int D, int NT>
+__device__ inline void interleave_qk_exp() {
+    constexpr int N = 2 * (D / 16);  // K operands per block
+    constexpr int AHEAD = 4;         // K operand reads in flight (as in qk_mfma)
+    __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);  // DS read
+    __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);     // VALU
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
+        }
+        if (i + AHEAD < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, kPvAhead, 0);  // V operand prefetch
+}
+
+// Second half: the PV MFMAs with their V operand reads, and between them the
+// LDS stores of the next K and V blocks (and the V transpose's byte
+// permutes), so those stores are done by the time the step's barrier comes.
+template <int D, int NT>
+__device__ inline void interleave_pv_stage() {
+    constexpr int N = 4 * (D / 32);  // V operands per block
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (i + kPvAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // DS read
+        if (i >= 2) {
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
         }
     }
 }
 
-// Online softmax of one block for this lane's query: updates the running
-// maximum m_used (lazily) and the row sum, returns the rescale factor of O and
-// the bf16 B operands P^T.  With MASK, keys at or past `kvalid` inside the
-// block get score -inf.
-template <bool MASK>
-__device__ inline float softmax_block(f32x16 (&sacc)[2], float &m_used, float &lsum,
-                                      bf16x8 (&pb)[4], float c, int g, int kvalid, bool &raise) {
-    if (MASK) {
+// Both 32-lane halves of the wave hold the same 32 queries (different keys).
+// v_permlane32_swap with both operands x returns (x of the lower half,
+// x of the upper half) in every lane, so both halves combine the two values in
+// the same order and get bit-identical results.
+__device__ inline float halves_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, x), false, false);
+    return __builtin_bit_cast(float, static_cast<unsigned>(r[0])) +
+           __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
+}
+
+__device__ inline float halves_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, x), false, false);
+    return fmaxf(__builtin_bit_cast(float, static_cast<unsigned>(r[0])),
+                 __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
+}
+
+// A block's exponentials are recomputed against its own maximum when their
+// sum over the 64 keys exceeds this bound.
+constexpr float kRaiseBound = 256.0f;
+
+// Keys at or past `kvalid` inside the block get the score -inf.
+__device__ inline void mask_block(f32x16 (&s)[2], int g, int kvalid) {
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-                if (key >= kvalid) sacc[mt][r] = -INFINITY;
-            }
-    }
-    float mx = sacc[0][0];
+        for (int r = 0; r < 16; ++r) {
+            const int key = mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+            if (key >= kvalid) s[mt][r] = -INFINITY;
+        }
+}
+
+// Block maximum of this lane's query over all 64 keys (both halves).
+__device__ inline float block_max(const f32x16 (&s)[2]) {
+    float mx = s[0][0];
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[0][r]);
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[1][r]);
-    {
-        const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
-                                                        __builtin_bit_cast(unsigned, mx), false, false);
-        mx = fmaxf(__builtin_bit_cast(float, static_cast<unsigned>(r[0])),
-                   __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
-    }
-    // First block: m_used = -inf, so the test is true and alpha = 0.
-    raise = (mx - m_used) * c > kRescaleThreshold;
-    const float alpha = raise ? __builtin_amdgcn_exp2f((m_used - mx) * c) : 1.0f;
-    m_used = raise ? mx : m_used;
-    lsum *= alpha;
-    const float mc = m_used * c;
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+    return halves_max(mx);
+}
+
+// P = exp2(c s - mc) rounded to bf16 as the B operands of the PV MFMAs
+// (one FMA and one v_exp_f32 per score); returns this lane's sum of exactly
+// those rounded values (v_dot2c_f32_bf16 with a (1, 1) pair), so the weights
+// that multiply V are normalised exactly.
+__device__ inline float exp_block(const f32x16 (&s)[2], float c, float mc, bf16x8 (&pb)[4]) {
     const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+    float sum = 0.f;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -140,21 +228,21 @@ __device__ inline float softmax_block(f32x16 (&sacc)[2], float &m_used, float &l
             f32x8 p;
 #pragma unroll
             for (int r = 0; r < 8; ++r)
-                p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][h * 8 + r], c, -mc));
+                p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mt][h * 8 + r], c, -mc));
             const bf16x8 pbf = __builtin_convertvector(p, bf16x8);
             pb[mt * 2 + h] = pbf;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const bf16x2 pair = {pbf[2 * r], pbf[2 * r + 1]};
-                lsum = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, lsum, false);
+                sum = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, sum, false);
             }
         }
     }
-    return alpha;
+    return sum;
 }
 
-template <int D, typename T, int WAVES>
-__global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
+template <int D, typename T, int WAVES, int NT, int PER_CU>
+__global__ __launch_bounds__(64 * WAVES, PER_CU * WAVES / 4) void attention_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v, T *__restrict__ o,
     float *__restrict__ lse, int S, int n_qtiles, float c) {
     constexpr int KK = D / 16;  // MFMA k-steps over the head dimension
@@ -182,125 +270,200 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_kernel(
     const int wave = tid >> 6;
     const int li = lane & 31;   // row / column index inside a 32-wide MFMA tile
     const int g = lane >> 5;    // which half of the wave
-    const int q0 = qtile * (kQW * WAVES) + wave * kQW;
-    const int qi = q0 + li;     // this lane's query
+    // The wave's queries: tile nt holds q0 + 32 nt + [0, 32); this lane holds
+    // query q0 + 32 nt + li of each tile.
+    const int q0 = (qtile * WAVES + wave) * (kQW * NT);
 
     // Q^T as the B operand: lane (g, n) holds query n, head dims 16 kk + 8 g + [0, 8).
     // Rows past S read as zeros and are never stored.
-    bf16x8 qreg[KK];
+    bf16x8 qreg[NT][KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-        qreg[kk] = __builtin_bit_cast(
-            bf16x8, load8<T>(qr, static_cast<unsigned>(qi * D + kk * 16 + g * 8) * sizeof(T)));
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            qreg[nt][kk] = __builtin_bit_cast(
+                bf16x8, load8<T>(qr, static_cast<unsigned>((q0 + nt * kQW + li) * D + kk * 16 + g * 8) *
+                                         sizeof(T)));
 
-    f32x16 oacc[DT];
+    f32x16 oacc[DT][NT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
-    float m_used = -INFINITY, lsum = 0.f;
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) oacc[dt][nt] = f32x16{};
     const int nkb = (S + kBC - 1) / kBC;
 
     // Prologue: K_0, V_0 and K_1 in LDS, scores of block 0.
-    Stage<D, T, WAVES> st;
-    st.load(kr, vr, 0, 0, tid);
-    st.store_k(kbuf[0], tid);
-    st.store_v(vbuf[0], tid);
-    st.load(kr, vr, 1, 1, tid);
-    st.store_k(kbuf[1], tid);
+    // NSETS register sets carry the next blocks from global memory to LDS.
+    // With two (bf16 storage), the loads for the blocks stored in step j are
+    // issued in step j - 1, a whole step ahead of their use; with one (fp32
+    // storage, whose loads need twice the registers), in step j itself.
+    constexpr int NSETS = sizeof(T) == 2 ? 2 : 1;
+    Stage<D, T, WAVES> st[NSETS];
+    st[0].load(kr, vr, 0, 0, tid);
+    st[0].store_k(kbuf[0], tid);
+    st[0].store_v(vbuf[0], tid);
+    st[1 % NSETS].load(kr, vr, 1, 1, tid);
+    st[1 % NSETS].store_k(kbuf[1], tid);
+    if (NSETS == 2) st[0].load(kr, vr, 2, 1, tid);
     __syncthreads();
-    f32x16 scur[2];
-    qk_mfma<D>(scur, kbuf[0], qreg, li, g);
-    __syncthreads();  // kbuf[0] is overwritten in the first iteration
+    f32x16 sa[NT][2], sb[NT][2];
+    qk_mfma<D, NT>(sa, kbuf[0], qreg, li, g);
+    __syncthreads();  // kbuf[0] is overwritten below
 
-    // Steady state: block j's softmax and PV overlap block j + 1's scores.
-    // LDS holds K_{j+1} in kbuf[(j+1)&1] and V_j in vbuf[j&1]; K_{j+2} and
-    // V_{j+1} travel through registers and land in the buffers freed by K_j
-    // and V_{j-1}.
-    auto step = [&](int j, f32x16(&scur)[2], f32x16(&snext)[2]) {
-        st.load(kr, vr, j + 2, j + 1, tid);
-        qk_mfma<D>(snext, kbuf[(j + 1) & 1], qreg, li, g);
-        bf16x8 pb[4];
-        bool raise;
-        const float alpha = softmax_block<false>(scur, m_used, lsum, pb, c, g, kBC, raise);
-        if (__any(raise)) {
+    // Block 0 sets the running maximum m used by the exponentials
+    // exp2(c s - c m).  m is raised lazily: only when a block's exponentials,
+    // summed over its 64 keys, exceed 2^8 is the block recomputed against its
+    // own maximum (and O, l rescaled).  Every exponential used is therefore at
+    // most 2^8, and the common path needs no maximum at all.  The decision is
+    // per query (both halves of the wave combine their sums in the same
+    // order); a wave only takes the recompute branch when some query needs it,
+    // and a query that does not need it recomputes the same values and
+    // multiplies by exactly 1 there.  So the arithmetic of every query depends
+    // only on its own row, never on which other queries share the wave, tile,
+    // chunk or launch: any head chunking gives bit-identical results.
+    float m[NT], mc[NT], lsum[NT];
+    bf16x8 pb[NT][4];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        if (nkb == 1) mask_block(sa[nt], g, S);
+        m[nt] = block_max(sa[nt]);
+        mc[nt] = m[nt] * c;
+        lsum[nt] = exp_block(sa[nt], c, mc[nt], pb[nt]);
+    }
+
+    // Recompute branch of a block whose exponentials overflowed the bound.
+    auto raise_m = [&](const f32x16(&s)[NT][2], const bool (&up)[NT], float (&bsum)[NT]) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const float mx = block_max(s[nt]);
+            const float m_new = up[nt] ? mx : m[nt];
+            const float alpha = up[nt] ? __builtin_amdgcn_exp2f((m[nt] - mx) * c) : 1.0f;
+            m[nt] = m_new;
+            mc[nt] = m_new * c;
+            bsum[nt] = exp_block(s[nt], c, mc[nt], pb[nt]);
+            lsum[nt] *= alpha;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+                for (int r = 0; r < 16; ++r) oacc[dt][nt][r] *= alpha;
         }
-        pv_mfma<D>(oacc, pb, vbuf[j & 1], li, g);
-        st.store_k(kbuf[j & 1], tid);
-        st.store_v(vbuf[(j + 1) & 1], tid);
+    };
+    // Exponentials of one block, the per-query overflow test and, when some
+    // query needs it, the recompute branch.
+    bf16x8 vpre[kPvAhead];
+    auto softmax = [&](const f32x16(&s)[NT][2], const __bf16 *vts) {
+        float bsum[NT];
+        bool up[NT], any_up = false;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) bsum[nt] = exp_block(s[nt], c, mc[nt], pb[nt]);
+        pv_prefetch<D>(vpre, vts, li, g);
+        interleave_qk_exp<D, NT>();
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            up[nt] = halves_sum(bsum[nt]) > kRaiseBound;
+            any_up = any_up || up[nt];
+        }
+        if (__any(any_up)) raise_m(s, up, bsum);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) lsum[nt] += bsum[nt];
+    };
+
+    if (nkb > 1) {
+        // Block 0's PV and block 1's scores.
+        st[1 % NSETS].load(kr, vr, 1 + NSETS, NSETS, tid);
+        qk_mfma<D, NT>(sb, kbuf[1], qreg, li, g);
+        pv_prefetch<D>(vpre, vbuf[0], li, g);
+        pv_mfma<D, NT>(oacc, pb, vbuf[0], vpre, li, g);
+        st[0].store_k(kbuf[0], tid);
+        st[0].store_v(vbuf[1], tid);
+        __syncthreads();
+    }
+
+    // Steady state: block j's exponentials and PV overlap block j + 1's
+    // scores.  LDS holds K_{j+1} in kbuf[(j+1)&1] and V_j in vbuf[j&1]; K_{j+2}
+    // and V_{j+1} land from registers in the buffers freed by K_j and V_{j-1}.
+    // Step j loads K_{j+1+NSETS} and V_{j+NSETS} into set (j + 1) % NSETS and
+    // stores from set j % NSETS.
+    auto step = [&](int j, f32x16(&scur)[NT][2], f32x16(&snext)[NT][2], Stage<D, T, WAVES> &ld,
+                    Stage<D, T, WAVES> &sto) {
+        ld.load(kr, vr, j + 1 + NSETS, j + NSETS, tid);
+        qk_mfma<D, NT>(snext, kbuf[(j + 1) & 1], qreg, li, g);
+        softmax(scur, vbuf[j & 1]);
+        pv_mfma<D, NT>(oacc, pb, vbuf[j & 1], vpre, li, g);
+        sto.store_k(kbuf[j & 1], tid);
+        sto.store_v(vbuf[(j + 1) & 1], tid);
+        interleave_pv_stage<D, NT>();
         __syncthreads();
     };
-    f32x16 salt[2];
-    int j0 = 0;
-    for (; j0 + 2 < nkb; j0 += 2) {
-        step(j0, scur, salt);
-        step(j0 + 1, salt, scur);
-    }
-    if (j0 + 1 < nkb) {
-        step(j0, scur, salt);
-        scur[0] = salt[0];
-        scur[1] = salt[1];
-    }
-
-    // Last block: mask the keys past S.
-    {
-        const int j = nkb - 1;
-        bf16x8 pb[4];
-        bool raise;
-        const float alpha = softmax_block<true>(scur, m_used, lsum, pb, c, g, S - j * kBC, raise);
-        if (__any(raise)) {
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+    int j = 1;
+    if (nkb > 1) {
+        for (; j + 2 < nkb; j += 2) {
+            step(j, sb, sa, st[0], st[1 % NSETS]);
+            step(j + 1, sa, sb, st[1 % NSETS], st[0]);
         }
-        pv_mfma<D>(oacc, pb, vbuf[j & 1], li, g);
+        if (j + 1 < nkb) {
+            step(j, sb, sa, st[0], st[1 % NSETS]);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                sb[nt][0] = sa[nt][0];
+                sb[nt][1] = sa[nt][1];
+            }
+            ++j;
+        }
+        // Last block (j = nkb - 1): mask the keys past S.
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) mask_block(sb[nt], g, S - j * kBC);
+        softmax(sb, vbuf[j & 1]);
+        pv_mfma<D, NT>(oacc, pb, vbuf[j & 1], vpre, li, g);
+    } else {
+        pv_prefetch<D>(vpre, vbuf[0], li, g);
+        pv_mfma<D, NT>(oacc, pb, vbuf[0], vpre, li, g);
     }
 
     // ---- O = O^T / l, rounded to the storage type ----
-    float l;
-    {
-        const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, lsum),
-                                                        __builtin_bit_cast(unsigned, lsum), false, false);
-        l = __builtin_bit_cast(float, static_cast<unsigned>(r[0])) +
-            __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
-    }
-    const float inv = 1.0f / l;
-    // log2 of the softmax denominator of c * s: P_ij = exp2(c s_ij - L2_i)
-    // (the statistic the backward pass recomputes P from).
-    if (lse != nullptr && g == 0 && qi < S)
-        lse[static_cast<int64_t>(head) * S + qi] = m_used * c + __builtin_amdgcn_logf(l);
-    if (qi < S) {
-        T *orow = oh + static_cast<int64_t>(qi) * D;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
+    for (int nt = 0; nt < NT; ++nt) {
+        const int qi = q0 + nt * kQW + li;
+        const float l = halves_sum(lsum[nt]);
+        const float inv = 1.0f / l;
+        // log2 of the softmax denominator of c * s: P_ij = exp2(c s_ij - L2_i)
+        // (the statistic the backward pass recomputes P from).
+        if (lse != nullptr && g == 0 && qi < S)
+            lse[static_cast<int64_t>(head) * S + qi] = mc[nt] + __builtin_amdgcn_logf(l);
+        if (qi < S) {
+            T *orow = oh + static_cast<int64_t>(qi) * D;
 #pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                const f32x4 x = {oacc[dt][rb * 4 + 0] * inv, oacc[dt][rb * 4 + 1] * inv,
-                                 oacc[dt][rb * 4 + 2] * inv, oacc[dt][rb * 4 + 3] * inv};
-                store4(orow + dt * 32 + rb * 8 + g * 4, x);
-            }
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const f32x4 x = {oacc[dt][nt][rb * 4 + 0] * inv, oacc[dt][nt][rb * 4 + 1] * inv,
+                                     oacc[dt][nt][rb * 4 + 2] * inv, oacc[dt][nt][rb * 4 + 3] * inv};
+                    store4(orow + dt * 32 + rb * 8 + g * 4, x);
+                }
+        }
     }
 }
 
-// Waves per workgroup: 8 for d = 128 (one workgroup per CU, two waves per
-// SIMD), 4 for d = 64 (two workgroups per CU).
+// Launch shape per head dimension: WAVES waves per workgroup, NT tiles of 32
+// queries per wave, 256 queries per workgroup.  d = 128: four waves of 64
+// queries, one wave per SIMD (every K and V operand read from LDS feeds two
+// MFMAs); d = 64: four waves of 32 queries, two workgroups per CU.
 template <int D>
-struct Waves {
-    static constexpr int value = D == 128 ? 8 : 4;
+struct Shape {
+    static constexpr int NT = D == 128 ? HCMS_ATTN_NT128 : 1;
+    static constexpr int WAVES = D == 128 && NT == 1 ? 8 : 4;
+    static constexpr int BR = kQW * NT * WAVES;       // queries per workgroup
+    static constexpr int PER_CU = D == 128 ? 1 : 2;   // workgroups one CU holds
 };
 
 template <int D, typename T>
 hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, float *lse, int S,
                         int n_heads, float c, hipStream_t stream) {
-    constexpr int WAVES = Waves<D>::value;
-    constexpr int BR = kQW * WAVES;
-    const int n_qtiles = (S + BR - 1) / BR;
+    using Sh = Shape<D>;
+    const int n_qtiles = (S + Sh::BR - 1) / Sh::BR;
     const int64_t blocks = static_cast<int64_t>(n_qtiles) * n_heads;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    attention_kernel<D, T, WAVES><<<static_cast<unsigned>(blocks), 64 * WAVES, 0, stream>>>(
+    attention_kernel<D, T, Sh::WAVES, Sh::NT, Sh::PER_CU><<<static_cast<unsigned>(blocks), 64 * Sh::WAVES, 0, stream>>>(
         static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
         static_cast<T *>(o), lse, S, n_qtiles, c);
     return hipGetLastError();
@@ -308,8 +471,8 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, fl
 
 }  // namespace
 
-int attention_queries_per_block(int d) { return kQW * (d == 128 ? Waves<128>::value : Waves<64>::value); }
-int attention_blocks_per_cu(int d) { return 8 / (d == 128 ? Waves<128>::value : Waves<64>::value); }
+int attention_queries_per_block(int d) { return d == 128 ? Shape<128>::BR : Shape<64>::BR; }
+int attention_blocks_per_cu(int d) { return d == 128 ? Shape<128>::PER_CU : Shape<64>::PER_CU; }
 
 hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, float *lse, int S,
                             int n_heads, int d, float scale_log2e, int dtype, hipStream_t stream) {

@@ -19,7 +19,6 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 inline constexpr int kQW = 32;              // queries per wave (one 32-wide MFMA tile)
 inline constexpr int kBC = 64;              // keys per block
-inline constexpr float kRescaleThreshold = 8.0f;  // log2 of the largest tolerated exp
 
 // Buffer resource over one head's [S][D] tensor: loads past its end return 0,
 // which is how the query and key tails are read without branches.
