@@ -30,9 +30,9 @@
 //     swapped) to match the order in which the accumulator rows arrive;
 //   * software pipeline: while the VALU computes the exponentials of block j,
 //     the MFMA unit already computes the scores of block j + 1 (no dependency
-//     between the two), then O^T += V_j^T P_j^T.  K and V operands are read
-//     from LDS four MFMAs ahead (the first V operands before the overflow
-//     test below); scheduling hints spread the exponentials between the score
+//     between the two), then O^T += V_j^T P_j^T.  K operands are read from
+//     LDS four MFMAs ahead and V operands two (the first two before the
+//     overflow test below); scheduling hints spread the exponentials between the score
 //     MFMAs and the next blocks' LDS stores between the PV MFMAs.  The loop is
 //     unrolled by two so the score registers alternate roles instead of being
 //     copied;
@@ -93,10 +93,12 @@ __device__ inline void qk_mfma(f32x16 (&sacc)[NT][2], const __bf16 *ks,
 }
 
 // O^T[dt][nt] += V^T[dt] P[nt]^T over the 64 keys of a block (4 k-steps of 16
-// keys); every V operand read from LDS feeds NT MFMAs.  The first AHEAD
+// keys); every V operand read from LDS feeds NT MFMAs.  The first kPvAhead
 // operands come in `pre` (read earlier by pv_prefetch), the others are read
-// AHEAD MFMAs ahead of their use.
-constexpr int kPvAhead = 4;
+// kPvAhead MFMAs ahead of their use.  Two, not more: the kernel stays within
+// 248 VGPRs, so two waves per SIMD leave 16 registers per lane for the waves
+// of a pack or unpack running beside them.
+constexpr int kPvAhead = 2;
 
 // Operand i = (ks, dt) = (i / DT, i % DT): consecutive MFMAs update different
 // O^T tiles, so none waits for the result of the one before it; each tile

@@ -15,15 +15,17 @@
 // its loads before any store to keep several 16-byte requests in flight.  The
 // source is read once, so its loads carry the non-temporal hint.
 //
-// Register budget.  In the pipelined schedule these kernels run while an
-// attention workgroup holds its CU; that workgroup leaves 32 VGPRs per SIMD
-// lane free (two waves of at most 240).  A copy wave that fits in those 32
+// Register budget.  In the pipelined schedules these kernels run while an
+// attention workgroup holds its CU; that workgroup leaves 16 VGPRs per SIMD
+// lane free (two waves of at most 248).  A copy wave that fits in those 16
 // registers is placed beside the attention waves instead of waiting for the CU
 // to drain, so the copy never delays an attention workgroup's start.  The
-// kernels therefore address memory through buffer resources built per
-// workgroup (64-bit bases in scalar registers, 32-bit lane offsets), and the
-// hardware range check of the resource replaces per-lane tail branches:
-// out-of-range loads return zero and out-of-range stores are dropped.
+// kernels therefore keep three 16-byte units per lane in flight, address
+// memory through buffer resources built per workgroup (64-bit bases in scalar
+// registers, one 32-bit lane offset, the per-unit step as a scalar offset),
+// and let the hardware range check of the resource replace per-lane tail
+// branches: out-of-range loads return zero and out-of-range stores are
+// dropped.
 #include "hcms_internal.h"
 
 namespace hcms {
@@ -32,7 +34,7 @@ namespace {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 3;
 constexpr int kUnitsPerBlock = kThreads * kUnroll;  // 16-byte units per workgroup
 constexpr int kNonTemporal = 2;                     // cache-policy bit of a streaming load
 
@@ -90,10 +92,10 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(PackPtrs p, int64_t S, i
     u32x4 buf[kUnroll];
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i)
-        buf[i] = __builtin_amdgcn_raw_buffer_load_b128(src, so + i * step, 0, kNonTemporal);
+        buf[i] = __builtin_amdgcn_raw_buffer_load_b128(src, so, i * step, kNonTemporal);
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i)
-        __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, (tid << 4) + i * (kThreads << 4), 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, tid << 4, i * (kThreads << 4), 0);
 }
 
 // grid: x = ceil(S * U / kUnitsPerBlock), y = hc, z = tensor.
@@ -109,11 +111,10 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(PackPtrs p, int64_t S,
     u32x4 buf[kUnroll];
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i)
-        buf[i] = __builtin_amdgcn_raw_buffer_load_b128(src, (tid << 4) + i * (kThreads << 4), 0,
-                                                       kNonTemporal);
+        buf[i] = __builtin_amdgcn_raw_buffer_load_b128(src, tid << 4, i * (kThreads << 4), kNonTemporal);
 #pragma unroll
     for (int i = 0; i < kUnroll; ++i)
-        __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, so + i * step, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(buf[i], dst, so, i * step, 0);
 }
 
 dim3 grid_for(int64_t S, int64_t hc, int log2_units, int n_tensors) {
