@@ -371,6 +371,89 @@ HCMS_API int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, vo
                            float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
                            void *main_stream, void *copy_stream, void *compute_stream);
 
+/* ------------------------------------------------------------------------ */
+/* Layer neighbours of the chunk loop: projections and rotary embedding      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Projection GEMM (the QKV projection before Alg. 1's split along heads and
+ * the output projection after its Concat; Sec. 2 lists them in the Ulysses
+ * layer):  y[m][n] = sum_k x[m][k] w[n][k],  i.e. y = x w^T.
+ *   x : device, [M][K];  w : device, [N][K] (the weight stored [out][in]);
+ *   y : device, [M][N], must not overlap x or w.
+ * bf16 MFMA operands (fp32 storage is rounded to bf16 when loaded), fp32
+ * accumulation, y rounded to the storage type.  Deterministic.
+ * Requires K a positive multiple of 64 and at most 2^20, N a multiple of 8
+ * and at most 2^20, M >= 0 (M = 0 or N = 0: nothing is enqueued).
+ * Errors: NULL, SHAPE, DTYPE, ALIGN, ALIAS, HIP.
+ */
+HCMS_API int hcms_linear(const void *x, const void *w, void *y, int M, int N, int K, int dtype,
+                         void *stream);
+
+/*
+ * Rotary position embedding on a latent grid (RoFormer's rotation, cited by
+ * the paper in Sec. 2 for the Ulysses layer).  Token t of a sequence laid on
+ * the row-major grid grid[0] x ... x grid[n_axes-1] (last axis fastest, e.g.
+ * frames x rows x columns of video latents) has one coordinate c_a per axis.
+ * The d/2 pairs (2i, 2i + 1) of a head vector form consecutive groups of
+ * axis_pairs[a] pairs; pair i' of group a turns by the angle
+ *   c_a * base^(-i' / axis_pairs[a])
+ * mapping (x, y) to (x cos - y sin, x sin + y cos).  One axis is RoFormer's
+ * one-dimensional position.
+ *
+ * hcms_rope_table_entries: the number E = sum_a grid[a] * axis_pairs[a] of
+ *   (cos, sin) entries of the rotation table; host only.  Errors: NULL, ARG
+ *   (n_axes not in 1..4), SHAPE (a size < 1, more than 2^31 - 1 tokens or
+ *   2^28 entries).
+ * hcms_rope_table: fills `table` (device, E pairs of fp32, 16-byte aligned)
+ *   with the (cos, sin) of every axis, coordinate and pair, computed in fp64 and
+ *   rounded to fp32.  Errors: as above, plus NULL, ALIGN and ARG (base not
+ *   finite and > 1), HIP.
+ */
+HCMS_API int hcms_rope_table_entries(const int *grid, const int *axis_pairs, int n_axes);
+HCMS_API int hcms_rope_table(float *table, const int *grid, const int *axis_pairs, int n_axes,
+                             double base, void *stream);
+
+/*
+ * QKV projection with the split along heads and the rotary embedding fused:
+ *   qkv[t][n] = sum_k x[t][k] w_qkv[n][k],  n = z H d + h d + e,
+ *   q_seq[t][h][e] = qkv[t][0 H d + h d + e], k_seq likewise from z = 1,
+ *   v_seq from z = 2, and, unless table is NULL, the pairs of q_seq[t][h] and
+ *   k_seq[t][h] rotated for token t (hcms_rope_table on the same grid,
+ *   axis_pairs, n_axes), in fp32 before the rounding to the storage type.
+ *   x : device, [S][D];  w_qkv : device, [3 H d][D];
+ *   q_seq, k_seq, v_seq : device, [S][H][d] each (the sequence-sharded
+ *   [P][S/P][H][d] layout hcms_forward takes), disjoint from the inputs and
+ *   each other.
+ * Requires D as K of hcms_linear, d a positive multiple of 8, 3 H d <= 2^20,
+ * and with a table: the grid's product = S, the pair counts' sum = d/2.
+ * Errors: as hcms_linear and hcms_rope_table_entries, plus ALIAS for table.
+ */
+HCMS_API int hcms_qkv_projection(const void *x, const void *w_qkv, const float *table,
+                                 const int *grid, const int *axis_pairs, int n_axes, void *q_seq,
+                                 void *k_seq, void *v_seq, int S, int D, int H, int d, int dtype,
+                                 void *stream);
+
+/*
+ * One attention layer around the HCMS chunk loop on one GPU: on main_stream
+ * hcms_qkv_projection(x, w_qkv, table, ...) into q_seq, k_seq, v_seq; then
+ * hcms_forward(ctx, q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm, NULL,
+ * ...) in `mode`; then, on main_stream after the join,
+ *   y[t][j] = sum_{h, e} o_seq[t][h][e] w_o[j][h d + e]
+ * (hcms_linear of the concatenated heads, [S][H d], by w_o [D][H d]).
+ *   y : device, [S][D].  Every other argument as in hcms_qkv_projection and
+ *   hcms_forward; no output or workspace may overlap an input or y.
+ * All modes and chunkings give bit-identical y.  Validation of all three
+ * steps completes before anything is enqueued.
+ */
+HCMS_API int hcms_layer_forward(hcms_ctx *ctx, const void *x, const void *w_qkv, const void *w_o,
+                                const float *table, const int *grid, const int *axis_pairs,
+                                int n_axes, void *y, void *q_seq, void *k_seq, void *v_seq,
+                                void *o_seq, void *q_hm, void *k_hm, void *v_hm, void *o_hm, int P,
+                                int S, int D, int H, int d, float scale, const int *chunk_sizes,
+                                int n_chunks, int dtype, int mode, void *main_stream,
+                                void *copy_stream, void *compute_stream);
+
 #ifdef __cplusplus
 }
 #endif

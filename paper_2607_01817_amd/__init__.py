@@ -84,6 +84,12 @@ def load():
                           vp, vp, vp], i),
         "hcms_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i,
                            f, ip, i, i, i, vp, vp, vp], i),
+        "hcms_linear": ([vp, vp, vp, i, i, i, i, vp], i),
+        "hcms_rope_table_entries": ([ip, ip, i], i),
+        "hcms_rope_table": ([vp, ip, ip, i, d, vp], i),
+        "hcms_qkv_projection": ([vp, vp, vp, ip, ip, i, vp, vp, vp, i, i, i, i, i, vp], i),
+        "hcms_layer_forward": ([vp, vp, vp, vp, vp, ip, ip, i, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                i, i, i, i, i, f, ip, i, i, i, vp, vp, vp], i),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -290,6 +296,71 @@ def attention_backward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: t
         sizes, n, _dtype(q), _stream(stream)))
     return dq, dk, dv
 
+def linear(x: torch.Tensor, w: torch.Tensor, out: torch.Tensor | None = None,
+           stream=None) -> torch.Tensor:
+    """Projection GEMM: x [M][K] times w [N][K] (weight stored [out][in]),
+    out [M][N] = x w^T, in the library's MFMA kernel."""
+    _dev(x, "x")
+    _dev(w, "w")
+    if x.dim() != 2 or w.dim() != 2 or x.shape[1] != w.shape[1] or x.dtype != w.dtype:
+        raise ValueError("x must be [M][K] and w [N][K] of one dtype")
+    M, K = x.shape
+    N = w.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=x.dtype, device=x.device)
+    _dev(out, "out")
+    if out.shape != (M, N) or out.dtype != x.dtype:
+        raise ValueError("out must be [M][N] of the input dtype")
+    _check(load().hcms_linear(x.data_ptr(), w.data_ptr(), out.data_ptr(), M, N, K, _dtype(x),
+                              _stream(stream)))
+    return out
+
+
+def rope_table(grid, axis_pairs, base: float = 10000.0, device="cuda",
+               stream=None) -> torch.Tensor:
+    """The rotation table of the latent grid ``grid`` whose head vectors'
+    pairs split into consecutive groups of ``axis_pairs`` (one per axis):
+    float32 [E][2] (cos, sin), filled on the GPU."""
+    g, na = _ints(grid)
+    p, npairs = _ints(axis_pairs)
+    if na != npairs:
+        raise ValueError("one pair count per grid axis")
+    lib = load()
+    n = _check(lib.hcms_rope_table_entries(g, p, na))
+    table = torch.empty((max(1, n), 2), dtype=torch.float32, device=device)
+    _check(lib.hcms_rope_table(table.data_ptr(), g, p, na, float(base), _stream(stream)))
+    return table[:n]
+
+
+def qkv_projection(x: torch.Tensor, w_qkv: torch.Tensor, H: int, d: int,
+                   table: torch.Tensor | None = None, grid=None, axis_pairs=None,
+                   out=None, stream=None):
+    """x [S][D] times w_qkv [3 H d][D]: (q, k, v) [S][H][d] each, the query
+    and key pairs rotated by ``table`` (from :func:`rope_table` on the same
+    grid and axis_pairs) when it is given."""
+    _dev(x, "x")
+    _dev(w_qkv, "w_qkv")
+    S, D = x.shape
+    if out is None:
+        out = tuple(torch.empty((S, H, d), dtype=x.dtype, device=x.device) for _ in range(3))
+    for t in out:
+        _dev(t, "out")
+        if t.shape != (S, H, d) or t.dtype != x.dtype:
+            raise ValueError("outputs must be [S][H][d] of the input dtype")
+    g = p = None
+    na = 0
+    tp = None
+    if table is not None:
+        _dev(table, "table")
+        g, na = _ints(grid)
+        p, _ = _ints(axis_pairs)
+        tp = table.data_ptr()
+    _check(load().hcms_qkv_projection(x.data_ptr(), w_qkv.data_ptr(), tp, g, p, na,
+                                      out[0].data_ptr(), out[1].data_ptr(), out[2].data_ptr(),
+                                      S, D, H, d, _dtype(x), _stream(stream)))
+    return out
+
+
 class Context:
     """The chunk scheduler (Alg. 1 and its one-GPU schedules) on one device.
 
@@ -394,6 +465,42 @@ class Context:
             self._h, q_seq.data_ptr(), k_seq.data_ptr(), v_seq.data_ptr(), out.data_ptr(),
             ws[0].data_ptr(), ws[1].data_ptr(), ws[2].data_ptr(), ws[3].data_ptr(), lse_p,
             P, S, H, d, float(scale), sizes, n, _dtype(q_seq), int(mode), main,
+            ctypes.c_void_p(self.copy_stream.cuda_stream),
+            ctypes.c_void_p(self.compute_stream.cuda_stream)))
+        return out
+
+    def layer_forward(self, x: torch.Tensor, w_qkv: torch.Tensor, w_o: torch.Tensor, P: int,
+                      H: int, d: int, scale: float, chunk_sizes, table=None, grid=None,
+                      axis_pairs=None, mode: int = MODE_AUTO, out=None, buffers=None,
+                      main_stream=None) -> torch.Tensor:
+        """One attention layer around the chunk loop: x [S][D] -> y [S][D]
+        (QKV projection with the rotation, :meth:`forward`, output projection).
+        ``buffers`` (q_seq, k_seq, v_seq, o_seq, each [S][H][d]) are kept
+        between calls with the same shape."""
+        _dev(x, "x")
+        S, D = x.shape
+        if out is None:
+            out = torch.empty((S, D), dtype=x.dtype, device=x.device)
+        if buffers is None:
+            key = (S, H, d, x.dtype)
+            if getattr(self, "_lbuf_key", None) != key:
+                self._lbuf = [torch.empty((S, H, d), dtype=x.dtype, device=x.device)
+                              for _ in range(4)]
+                self._lbuf_key = key
+            buffers = self._lbuf
+        ws = self.workspaces(S, H, d, x.dtype)
+        g = p = None
+        na = 0
+        tp = None
+        if table is not None:
+            g, na = _ints(grid)
+            p, _ = _ints(axis_pairs)
+            tp = table.data_ptr()
+        sizes, n = _ints(chunk_sizes)
+        _check(load().hcms_layer_forward(
+            self._h, x.data_ptr(), w_qkv.data_ptr(), w_o.data_ptr(), tp, g, p, na,
+            out.data_ptr(), *[b.data_ptr() for b in buffers], *[t.data_ptr() for t in ws],
+            P, S, D, H, d, float(scale), sizes, n, _dtype(x), int(mode), _stream(main_stream),
             ctypes.c_void_p(self.copy_stream.cuda_stream),
             ctypes.c_void_p(self.compute_stream.cuda_stream)))
         return out

@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libhcms.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "model.cpp", "pack.hip", "attention.hip", "attention_bwd.hip"]
+SOURCES = ["api.cpp", "model.cpp", "pack.hip", "attention.hip", "attention_bwd.hip", "linear.hip"]
 
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

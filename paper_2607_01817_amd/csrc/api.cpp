@@ -443,6 +443,178 @@ int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *m
     return ok();
 }
 
+// Arguments of one hcms_forward call.
+struct ForwardArgs {
+    hcms_ctx *ctx;
+    const void *q_seq, *k_seq, *v_seq;
+    void *o_seq, *q_hm, *k_hm, *v_hm, *o_hm;
+    float *lse;
+    int P, S, H, d;
+    float scale;
+    const int *chunk_sizes;
+    int n_chunks, dtype, mode;
+    void *main_stream, *copy_stream, *compute_stream;
+};
+
+// Everything hcms_forward validates; resolves the mode and the row unit.
+int check_forward(const ForwardArgs &f, int *mode, int *log2u) {
+    int st;
+    if (!f.ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    if (f.S > 0 && (!f.q_seq || !f.k_seq || !f.v_seq || !f.o_seq || !f.q_hm || !f.k_hm || !f.v_hm ||
+                    !f.o_hm))
+        return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
+    if ((st = check_schedule(f.ctx, f.P, f.S, f.H, f.d, f.scale, f.chunk_sizes, f.n_chunks, f.dtype,
+                             mode, log2u, f.main_stream, f.copy_stream, f.compute_stream)) != HCMS_OK)
+        return st;
+    const void *all[8] = {f.q_seq, f.k_seq, f.v_seq, f.o_seq, f.q_hm, f.k_hm, f.v_hm, f.o_hm};
+    for (const void *p : all)
+        if (f.S > 0 && !aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t bytes = static_cast<int64_t>(f.S) * f.H * f.d * elem_bytes(f.dtype);
+    for (int i = 0; i < 8; ++i)
+        for (int j = i + 1; j < 8; ++j) {
+            // Inputs may alias each other (read-only); everything else must not.
+            const bool both_inputs = i < 3 && j < 3;
+            if (!both_inputs && overlaps(all[i], bytes, all[j], bytes))
+                return fail(HCMS_ERR_ALIAS, "tensor %d overlaps tensor %d", i, j);
+        }
+    if (f.lse) {
+        if ((st = check_stats(f.lse, "lse", f.S, f.H, f.q_hm, f.k_hm, f.v_hm, f.o_hm, f.d, f.dtype)) !=
+            HCMS_OK)
+            return st;
+        if ((st = check_stats(f.lse, "lse", f.S, f.H, f.q_seq, f.k_seq, f.v_seq, f.o_seq, f.d,
+                              f.dtype)) != HCMS_OK)
+            return st;
+    }
+    return HCMS_OK;
+}
+
+// Issues a validated hcms_forward (S > 0) in the resolved mode.
+int issue_forward(const ForwardArgs &f, int mode, int log2u) {
+    const int64_t head_bytes = static_cast<int64_t>(f.S) * f.d * elem_bytes(f.dtype);
+    const float c_log2e = scale_log2e(f.scale);
+    auto at = [head_bytes](void *p, int h0) { return static_cast<char *>(p) + head_bytes * h0; };
+    auto launch = [&](int kind, int h0, int hc, hipStream_t s) -> hipError_t {
+        if (kind == HCMS_OP_PACK) {
+            const void *src[3] = {f.q_seq, f.k_seq, f.v_seq};
+            void *dst[3] = {at(f.q_hm, h0), at(f.k_hm, h0), at(f.v_hm, h0)};
+            return hcms::launch_pack(src, dst, 3, f.S, f.H, h0, hc, log2u, s);
+        }
+        if (kind == HCMS_OP_ATTENTION)
+            return hcms::launch_attention(at(f.q_hm, h0), at(f.k_hm, h0), at(f.v_hm, h0),
+                                          at(f.o_hm, h0),
+                                          f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr,
+                                          f.S, hc, f.d, c_log2e, f.dtype, s);
+        const void *src[1] = {at(f.o_hm, h0)};
+        void *dst[1] = {f.o_seq};
+        return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, s);
+    };
+    return execute_plan(f.ctx, mode, f.chunk_sizes, f.n_chunks, f.main_stream, f.copy_stream,
+                        f.compute_stream, launch);
+}
+
+// ---------------------------------------------------------------------------
+// Layer neighbours: projections and rotary position embedding
+// ---------------------------------------------------------------------------
+
+// Y[M][N] = X[M][K] W[N][K]^T: shapes, pointers, alignment, aliasing.
+int check_linear(const void *x, const void *w, const void *y, int M, int N, int K, int dtype) {
+    int st;
+    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
+    if (M < 0 || N < 0) return fail(HCMS_ERR_SHAPE, "need M >= 0 and N >= 0 (M=%d N=%d)", M, N);
+    const int kq = hcms::linear_k_multiple();
+    if (K < kq || K % kq != 0 || K > (1 << 20))
+        return fail(HCMS_ERR_SHAPE, "K=%d must be a positive multiple of %d, at most 2^20", K, kq);
+    if (N % 8 != 0 || N > (1 << 20))
+        return fail(HCMS_ERR_SHAPE, "N=%d must be a multiple of 8, at most 2^20", N);
+    if (M == 0 || N == 0) return HCMS_OK;
+    if (!x || !w || !y) return fail(HCMS_ERR_NULL, "x, w or y is NULL");
+    if (!aligned16(x) || !aligned16(w) || !aligned16(y))
+        return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t es = elem_bytes(dtype);
+    const int64_t xb = static_cast<int64_t>(M) * K * es, wb = static_cast<int64_t>(N) * K * es;
+    const int64_t yb = static_cast<int64_t>(M) * N * es;
+    if (overlaps(y, yb, x, xb) || overlaps(y, yb, w, wb))
+        return fail(HCMS_ERR_ALIAS, "the output overlaps an input");
+    return HCMS_OK;
+}
+
+// Rotation axes from the caller's grid and pair counts: 1..kRopeMaxAxes axes,
+// every size >= 1; *tokens = product of the grid, *pairs = sum of the counts,
+// *entries = table entries.
+int rope_axes(const int *grid, const int *axis_pairs, int n_axes, hcms::RopeAxes *ax,
+              int64_t *tokens, int64_t *pairs, int64_t *entries) {
+    if (!grid || !axis_pairs) return fail(HCMS_ERR_NULL, "grid or axis_pairs is NULL");
+    if (n_axes < 1 || n_axes > hcms::kRopeMaxAxes)
+        return fail(HCMS_ERR_ARG, "n_axes=%d must be in [1, %d]", n_axes, hcms::kRopeMaxAxes);
+    *ax = hcms::RopeAxes{};
+    ax->n_axes = n_axes;
+    int64_t prod = 1, np = 0, off = 0;
+    for (int a = 0; a < n_axes; ++a) {
+        if (grid[a] < 1 || axis_pairs[a] < 1)
+            return fail(HCMS_ERR_SHAPE, "axis %d: grid size %d and pair count %d must be >= 1", a,
+                        grid[a], axis_pairs[a]);
+        ax->grid[a] = grid[a];
+        ax->pairs[a] = axis_pairs[a];
+        ax->pair_start[a] = static_cast<int>(np);
+        ax->tab_off[a] = static_cast<int>(off);
+        prod *= grid[a];
+        np += axis_pairs[a];
+        off += static_cast<int64_t>(grid[a]) * axis_pairs[a];
+        if (prod > 0x7fffffffLL || off > (1LL << 28))
+            return fail(HCMS_ERR_SHAPE, "grid too large (%lld tokens, %lld table entries)",
+                        static_cast<long long>(prod), static_cast<long long>(off));
+    }
+    *tokens = prod;
+    *pairs = np;
+    *entries = off;
+    return HCMS_OK;
+}
+
+// q, k, v [S][H][d] outputs of the QKV projection of x [S][D] by w [3 H d][D],
+// rotated by `table` when it is not NULL.
+int check_qkv(const void *x, const void *w, const float *table, const int *grid,
+              const int *axis_pairs, int n_axes, const void *q, const void *k, const void *v, int S,
+              int D, int H, int d, int dtype, hcms::RopeAxes *ax) {
+    int st;
+    if (S < 0 || H < 1 || d < 8 || d % 8 != 0)
+        return fail(HCMS_ERR_SHAPE, "need S >= 0, H >= 1, d a positive multiple of 8 (S=%d H=%d d=%d)",
+                    S, H, d);
+    if (static_cast<int64_t>(3) * H * d > (1 << 20))
+        return fail(HCMS_ERR_SHAPE, "3 H d = %lld exceeds 2^20", 3LL * H * d);
+    if ((st = check_linear(x, w, q, S, 3 * H * d, D, dtype)) != HCMS_OK) return st;
+    *ax = hcms::RopeAxes{};
+    if (S == 0) return HCMS_OK;
+    if (!k || !v) return fail(HCMS_ERR_NULL, "k or v is NULL");
+    if (!aligned16(k) || !aligned16(v)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
+    const int64_t es = elem_bytes(dtype);
+    const int64_t tb = static_cast<int64_t>(S) * H * d * es;
+    const int64_t xb = static_cast<int64_t>(S) * D * es, wb = 3LL * H * d * D * es;
+    const void *outs[3] = {q, k, v};
+    for (int i = 0; i < 3; ++i) {
+        if (overlaps(outs[i], tb, x, xb) || overlaps(outs[i], tb, w, wb))
+            return fail(HCMS_ERR_ALIAS, "output %d overlaps an input", i);
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i], tb, outs[j], tb))
+                return fail(HCMS_ERR_ALIAS, "outputs %d and %d overlap", i, j);
+    }
+    if (table) {
+        int64_t tokens = 0, pairs = 0, entries = 0;
+        if ((st = rope_axes(grid, axis_pairs, n_axes, ax, &tokens, &pairs, &entries)) != HCMS_OK)
+            return st;
+        if (tokens != S)
+            return fail(HCMS_ERR_SHAPE, "the grid holds %lld tokens, not S=%d",
+                        static_cast<long long>(tokens), S);
+        if (pairs * 2 != d)
+            return fail(HCMS_ERR_SHAPE, "the axis pair counts sum to %lld, not d/2=%d",
+                        static_cast<long long>(pairs), d / 2);
+        if (!aligned16(table)) return fail(HCMS_ERR_ALIGN, "table must be 16-byte aligned");
+        for (int i = 0; i < 3; ++i)
+            if (overlaps(table, entries * 8, outs[i], tb))
+                return fail(HCMS_ERR_ALIAS, "table overlaps output %d", i);
+    }
+    return HCMS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -724,51 +896,108 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
                  void *q_hm, void *k_hm, void *v_hm, void *o_hm, float *lse, int P, int S, int H,
                  int d, float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
                  void *main_stream, void *copy_stream, void *compute_stream) {
+    const ForwardArgs f{ctx, q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm, lse, P, S, H, d,
+                        scale, chunk_sizes, n_chunks, dtype, mode, main_stream, copy_stream,
+                        compute_stream};
+    int st, log2u = 0, resolved = mode;
+    if ((st = check_forward(f, &resolved, &log2u)) != HCMS_OK) return st;
+    if (S == 0) return ok();
+    return issue_forward(f, resolved, log2u);
+}
+
+int hcms_linear(const void *x, const void *w, void *y, int M, int N, int K, int dtype,
+                void *stream) {
     int st;
-    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
-    if (S > 0 && (!q_seq || !k_seq || !v_seq || !o_seq || !q_hm || !k_hm || !v_hm || !o_hm))
-        return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
-    int log2u = 0;
-    if ((st = check_schedule(ctx, P, S, H, d, scale, chunk_sizes, n_chunks, dtype, &mode, &log2u,
-                             main_stream, copy_stream, compute_stream)) != HCMS_OK)
+    if ((st = check_linear(x, w, y, M, N, K, dtype)) != HCMS_OK) return st;
+    if (M == 0 || N == 0) return ok();
+    const hipError_t e = hcms::launch_linear(x, w, y, M, N, K, dtype, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "linear launch");
+    return ok();
+}
+
+int hcms_rope_table_entries(const int *grid, const int *axis_pairs, int n_axes) {
+    hcms::RopeAxes ax;
+    int64_t tokens = 0, pairs = 0, entries = 0;
+    const int st = rope_axes(grid, axis_pairs, n_axes, &ax, &tokens, &pairs, &entries);
+    if (st != HCMS_OK) return st;
+    ok();
+    return static_cast<int>(entries);
+}
+
+int hcms_rope_table(float *table, const int *grid, const int *axis_pairs, int n_axes, double base,
+                    void *stream) {
+    hcms::RopeAxes ax;
+    int64_t tokens = 0, pairs = 0, entries = 0;
+    int st;
+    if ((st = rope_axes(grid, axis_pairs, n_axes, &ax, &tokens, &pairs, &entries)) != HCMS_OK) return st;
+    if (!table) return fail(HCMS_ERR_NULL, "table is NULL");
+    if (!aligned16(table)) return fail(HCMS_ERR_ALIGN, "table must be 16-byte aligned");
+    if (!std::isfinite(base) || !(base > 1.0))
+        return fail(HCMS_ERR_ARG, "base must be finite and > 1 (got %g)", base);
+    const hipError_t e = hcms::launch_rope_table(table, ax, base, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "rope table launch");
+    return ok();
+}
+
+int hcms_qkv_projection(const void *x, const void *w_qkv, const float *table, const int *grid,
+                        const int *axis_pairs, int n_axes, void *q_seq, void *k_seq, void *v_seq,
+                        int S, int D, int H, int d, int dtype, void *stream) {
+    hcms::RopeAxes ax;
+    int st;
+    if ((st = check_qkv(x, w_qkv, table, grid, axis_pairs, n_axes, q_seq, k_seq, v_seq, S, D, H, d,
+                        dtype, &ax)) != HCMS_OK)
         return st;
-    const void *all[8] = {q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm};
-    for (const void *p : all)
-        if (S > 0 && !aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
-    const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
-    for (int i = 0; i < 8; ++i)
-        for (int j = i + 1; j < 8; ++j) {
-            // Inputs may alias each other (read-only); everything else must not.
-            const bool both_inputs = i < 3 && j < 3;
-            if (!both_inputs && overlaps(all[i], bytes, all[j], bytes))
-                return fail(HCMS_ERR_ALIAS, "tensor %d overlaps tensor %d", i, j);
+    if (S == 0) return ok();
+    const hipError_t e = hcms::launch_qkv_projection(x, w_qkv, q_seq, k_seq, v_seq, table, ax, S, D,
+                                                     H, d, dtype, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "qkv projection launch");
+    return ok();
+}
+
+int hcms_layer_forward(hcms_ctx *ctx, const void *x, const void *w_qkv, const void *w_o,
+                       const float *table, const int *grid, const int *axis_pairs, int n_axes,
+                       void *y, void *q_seq, void *k_seq, void *v_seq, void *o_seq, void *q_hm,
+                       void *k_hm, void *v_hm, void *o_hm, int P, int S, int D, int H, int d,
+                       float scale, const int *chunk_sizes, int n_chunks, int dtype, int mode,
+                       void *main_stream, void *copy_stream, void *compute_stream) {
+    int st;
+    hcms::RopeAxes ax;
+    if ((st = check_qkv(x, w_qkv, table, grid, axis_pairs, n_axes, q_seq, k_seq, v_seq, S, D, H, d,
+                        dtype, &ax)) != HCMS_OK)
+        return st;
+    const ForwardArgs f{ctx, q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm, nullptr, P, S, H,
+                        d, scale, chunk_sizes, n_chunks, dtype, mode, main_stream, copy_stream,
+                        compute_stream};
+    int log2u = 0, resolved = mode;
+    if ((st = check_forward(f, &resolved, &log2u)) != HCMS_OK) return st;
+    if ((st = check_linear(o_seq, w_o, y, S, D, H * d, dtype)) != HCMS_OK) return st;
+    if (S > 0) {
+        // No output or workspace of the layer may overlap an input or y.
+        const int64_t es = elem_bytes(dtype);
+        const int64_t xb = static_cast<int64_t>(S) * D * es, tb = static_cast<int64_t>(S) * H * d * es;
+        const int64_t wqb = 3LL * H * d * D * es, wob = static_cast<int64_t>(D) * H * d * es;
+        const void *in[3] = {x, w_qkv, w_o};
+        const int64_t inb[3] = {xb, wqb, wob};
+        const void *t[9] = {q_seq, k_seq, v_seq, o_seq, q_hm, k_hm, v_hm, o_hm, y};
+        for (int i = 0; i < 9; ++i) {
+            const int64_t ti = i == 8 ? xb : tb;
+            for (int j = 0; j < 3; ++j)
+                if (overlaps(t[i], ti, in[j], inb[j]))
+                    return fail(HCMS_ERR_ALIAS, "layer buffer %d overlaps input %d", i, j);
+            if (i < 8 && overlaps(t[i], tb, y, xb))
+                return fail(HCMS_ERR_ALIAS, "layer buffer %d overlaps y", i);
         }
-    if (lse) {
-        if ((st = check_stats(lse, "lse", S, H, q_hm, k_hm, v_hm, o_hm, d, dtype)) != HCMS_OK) return st;
-        if ((st = check_stats(lse, "lse", S, H, q_seq, k_seq, v_seq, o_seq, d, dtype)) != HCMS_OK)
-            return st;
     }
     if (S == 0) return ok();
-
-    const int64_t head_bytes = static_cast<int64_t>(S) * d * elem_bytes(dtype);
-    const float c_log2e = scale_log2e(scale);
-    auto at = [head_bytes](void *p, int h0) { return static_cast<char *>(p) + head_bytes * h0; };
-    auto launch = [&](int kind, int h0, int hc, hipStream_t s) -> hipError_t {
-        if (kind == HCMS_OP_PACK) {
-            const void *src[3] = {q_seq, k_seq, v_seq};
-            void *dst[3] = {at(q_hm, h0), at(k_hm, h0), at(v_hm, h0)};
-            return hcms::launch_pack(src, dst, 3, S, H, h0, hc, log2u, s);
-        }
-        if (kind == HCMS_OP_ATTENTION)
-            return hcms::launch_attention(at(q_hm, h0), at(k_hm, h0), at(v_hm, h0), at(o_hm, h0),
-                                          lse ? lse + static_cast<int64_t>(h0) * S : nullptr, S, hc,
-                                          d, c_log2e, dtype, s);
-        const void *src[1] = {at(o_hm, h0)};
-        void *dst[1] = {o_seq};
-        return hcms::launch_unpack(src, dst, 1, S, H, h0, hc, log2u, s);
-    };
-    return execute_plan(ctx, mode, chunk_sizes, n_chunks, main_stream, copy_stream, compute_stream,
-                        launch);
+    const hipStream_t ms = static_cast<hipStream_t>(main_stream);
+    hipError_t e = hcms::launch_qkv_projection(x, w_qkv, q_seq, k_seq, v_seq, table, ax, S, D, H, d,
+                                               dtype, ms);
+    if (e != hipSuccess) return hip_fail(e, "qkv projection launch");
+    if ((st = issue_forward(f, resolved, log2u)) != HCMS_OK) return st;
+    // o_seq [S][H][d] is the concatenation of the heads, [S][H d].
+    e = hcms::launch_linear(o_seq, w_o, y, S, D, H * d, dtype, ms);
+    if (e != hipSuccess) return hip_fail(e, "output projection launch");
+    return ok();
 }
 
 int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_seq, void *dv_seq,

@@ -47,4 +47,30 @@ hipError_t launch_attention_backward(const void *q, const void *k, const void *v
                                      void *dv, float *delta, int S, int n_heads, int d,
                                      float scale, int dtype, hipStream_t stream);
 
+// Rotary position embedding on a latent grid of n_axes axes (row-major, the
+// last axis fastest): the d/2 pairs of a head vector form consecutive groups
+// of pairs[a] pairs, starting at pair_start[a], that turn with coordinate a.
+// The rotation table holds grid[a] * pairs[a] (cos, sin) entries per axis,
+// axis a's first at entry tab_off[a].
+inline constexpr int kRopeMaxAxes = 4;
+struct RopeAxes {
+    int n_axes;
+    int grid[kRopeMaxAxes], pairs[kRopeMaxAxes], pair_start[kRopeMaxAxes], tab_off[kRopeMaxAxes];
+};
+
+// Projection GEMM Y[M][N] = X[M][K] W[N][K]^T (bf16 MFMA, fp32 accumulation,
+// Y rounded to the storage type); K a multiple of linear_k_multiple(), N of 8.
+int linear_k_multiple();
+hipError_t launch_linear(const void *x, const void *w, void *y, int M, int N, int K, int dtype,
+                         hipStream_t stream);
+
+// QKV projection: X[S][D] times W[3 H d][D]^T, split into q, k, v [S][H][d],
+// q and k rotated with `table` (NULL: no rotation).
+hipError_t launch_qkv_projection(const void *x, const void *w, void *q, void *k, void *v,
+                                 const float *table, const RopeAxes &ax, int S, int D, int H, int d,
+                                 int dtype, hipStream_t stream);
+
+// Fills the rotation table of `ax` (fp32 (cos, sin) pairs).
+hipError_t launch_rope_table(float *table, const RopeAxes &ax, double base, hipStream_t stream);
+
 }  // namespace hcms

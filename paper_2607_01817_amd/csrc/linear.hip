@@ -1,0 +1,291 @@
+// Projection GEMM for gfx950 (MI355X), bf16 MFMA with fp32 accumulation:
+//   Y[m][n] = sum_k X[m][k] W[n][k]       X [M][K], W [N][K], Y [M][N]
+// i.e. Y = X W^T with the weight stored [out][in].  It is the QKV projection
+// before the split along heads and the output projection after the
+// concatenation (Alg. 1, the main-stream steps around the chunk loop).
+//
+// Two epilogues.  The plain one stores Y.  The QKV one splits Y's columns
+// n = z H d + h d + e into three [M][H][d] tensors (z = 0, 1, 2: queries, keys,
+// values) and rotates the query and key pairs (e, e + 1), e even, by the rotary
+// position embedding of token m on its latent grid (RoFormer's rotation; the
+// pairs of a head vector form consecutive groups, each turning with one grid
+// axis), in fp32 before the rounding to the storage type: the split along
+// heads and the position embedding fused into the producing kernel.
+//
+// Work decomposition
+//   * one workgroup = 8 waves = one 256 (m) x 256 (n) tile of Y; wave w owns
+//     the 64 rows 64 (w >> 1) + [0, 64) and the 128 columns 128 (w & 1) +
+//     [0, 128) of the tile, as 2 x 4 tiles of 32 x 32;
+//   * both operands are K-contiguous rows, which is the operand layout of
+//     v_mfma_f32_32x32x16_bf16 (8 consecutive k per lane), so neither needs a
+//     transpose: the MFMA computes Y^T tiles, D[n][m] = sum_k W[n][k] X[m][k],
+//     with W rows as the A operand and X rows as the B operand.  Each lane
+//     then holds one row m and, per 32 x 32 tile, 4 runs of 4 consecutive
+//     columns n: 8-byte stores of bf16, and whole rotation pairs;
+//   * k advances in blocks of 64: the 256 x 64 blocks of X and W are staged
+//     global -> registers -> LDS (rows padded to 144 bytes, so 16 lanes
+//     reading 16 rows hit 16 disjoint groups of 4 banks), double-buffered, the
+//     next block's global loads in flight while the current one is consumed;
+//     every operand read from LDS feeds 2 (W) or 4 (X) MFMAs;
+//   * tiles are ordered in groups of 8 row tiles (all column tiles of a group
+//     before the next group), and the 8 XCDs each take a contiguous range of
+//     that order, so the 32 workgroups resident on an XCD share 8 X panels and
+//     4 W panels through its L2.
+//
+// Tails: rows past M or N are read through buffer resources bounded by the
+// last row, so they read as zeros; rows past M and columns past N are not
+// stored.  K must be a multiple of 64 and N of 8 (checked by the caller).
+#include "attention_tiles.h"
+#include "hcms_internal.h"
+
+namespace hcms {
+namespace {
+
+using namespace tiles;
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBM = 256, kBN = 256, kBK = 64;
+constexpr int kThreads = 512;
+constexpr int kRow = kBK + 8;            // LDS row stride, elements (144 bytes)
+constexpr int kTile = 256 * kRow;        // one staged 256 x 64 block, elements
+constexpr int kGroupM = 8;               // row tiles per group of the tile order
+constexpr int kPass = 256 * (kBK / 8) / kThreads;  // 16-byte chunks per thread per block
+
+// Arguments of the QKV epilogue: destinations, and the rotation (table NULL:
+// no rotation).  table holds (cos, sin) pairs; axis a, coordinate c, pair i'
+// of the axis's group is entry tab_off[a] + c * pairs[a] + i'.
+template <typename T>
+struct QkvOut {
+    T *dst[3];
+    const float *table;
+    int H, d;
+    RopeAxes ax;
+};
+
+// Resource over [base, base + min(bytes, 2^32 - 1)).
+__device__ inline __amdgpu_buffer_rsrc_t span_rsrc(const void *base, int64_t bytes) {
+    const int64_t n = bytes < 0 ? 0 : (bytes > 0xFFFFFFFFll ? 0xFFFFFFFFll : bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0,
+                                             static_cast<int>(static_cast<uint32_t>(n)), 0x00020000);
+}
+
+// Global -> register staging of the 256 x 64 blocks of X and W at column k0.
+// Thread tid moves chunk tid % 8 (8 elements) of rows tid / 8 + 64 p.
+template <typename T>
+struct Stager {
+    u32x4 xr[kPass], wr[kPass];
+    __device__ void load(__amdgpu_buffer_rsrc_t xs, __amdgpu_buffer_rsrc_t ws, unsigned row_bytes,
+                         int k0, int tid) {
+        const unsigned col = (static_cast<unsigned>(k0) + (tid & 7) * 8) * sizeof(T);
+#pragma unroll
+        for (int p = 0; p < kPass; ++p) {
+            const unsigned off = static_cast<unsigned>(tid / 8 + 64 * p) * row_bytes + col;
+            xr[p] = load8<T>(xs, off);
+            wr[p] = load8<T>(ws, off);
+        }
+    }
+    __device__ void store(__bf16 *xt, __bf16 *wt, int tid) const {
+#pragma unroll
+        for (int p = 0; p < kPass; ++p) {
+            const int e = (tid / 8 + 64 * p) * kRow + (tid & 7) * 8;
+            *reinterpret_cast<u32x4 *>(xt + e) = xr[p];
+            *reinterpret_cast<u32x4 *>(wt + e) = wr[p];
+        }
+    }
+};
+
+template <typename T, bool QKV>
+__global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict__ x,
+                                                             const T *__restrict__ w,
+                                                             T *__restrict__ y, int M, int N, int K,
+                                                             int tiles_m, int tiles_n, QkvOut<T> qo) {
+    __shared__ __attribute__((aligned(16))) __bf16 xt[2][kTile];
+    __shared__ __attribute__((aligned(16))) __bf16 wt[2][kTile];
+
+    // XCD-aware order: workgroup b runs on XCD b % 8 and takes position
+    // xcd * per + b / 8 of the grouped tile order.
+    const int nb = gridDim.x, b = blockIdx.x;
+    const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
+    const int L = xcd * per + min(xcd, rem) + (b >> 3);
+    const int group = L / (kGroupM * tiles_n);
+    const int first_m = group * kGroupM;
+    const int gm = min(tiles_m - first_m, kGroupM);
+    const int in_group = L - group * kGroupM * tiles_n;
+    const int tm = first_m + in_group % gm;
+    const int tn = in_group / gm;
+    const int m0 = tm * kBM, n0 = tn * kBN;
+
+    const unsigned row_bytes = static_cast<unsigned>(K) * sizeof(T);
+    const __amdgpu_buffer_rsrc_t xs =
+        span_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<int64_t>(M - m0) * row_bytes);
+    const __amdgpu_buffer_rsrc_t ws =
+        span_rsrc(w + static_cast<int64_t>(n0) * K, static_cast<int64_t>(N - n0) * row_bytes);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 31, g = lane >> 5;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    f32x16 acc[4][2];  // [n tile][m tile]
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) acc[nt][mt] = f32x16{};
+
+    const int nkb = K / kBK;
+    Stager<T> st;
+    st.load(xs, ws, row_bytes, 0, tid);
+    st.store(xt[0], wt[0], tid);
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+        const bool more = kb + 1 < nkb;
+        if (more) st.load(xs, ws, row_bytes, (kb + 1) * kBK, tid);
+        const __bf16 *xa = xt[kb & 1] + (wm * 64 + li) * kRow + g * 8;
+        const __bf16 *wa = wt[kb & 1] + (wn * 128 + li) * kRow + g * 8;
+#pragma unroll
+        for (int ks = 0; ks < kBK / 16; ++ks) {
+            bf16x8 a[4], bx[2];
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+                a[nt] = *reinterpret_cast<const bf16x8 *>(wa + nt * 32 * kRow + ks * 16);
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
+                bx[mt] = *reinterpret_cast<const bf16x8 *>(xa + mt * 32 * kRow + ks * 16);
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt)
+                    acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nt], bx[mt], acc[nt][mt],
+                                                                          0, 0, 0);
+        }
+        if (more) st.store(xt[(kb + 1) & 1], wt[(kb + 1) & 1], tid);
+        __syncthreads();
+    }
+
+    // ---- Y[m][n .. n + 3] from the D^T accumulators, rounded to T ----
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+        const int m = m0 + wm * 64 + mt * 32 + li;
+        if (m >= M) continue;
+        // Per grid axis, the table entry of pair 0 of the axis at token m's
+        // coordinate (QKV epilogue with a rotation only).
+        int tab_row[kRopeMaxAxes] = {};
+        if (QKV && qo.table != nullptr) {
+            int rest = m;
+            for (int a = qo.ax.n_axes - 1; a >= 0; --a) {
+                const int cc = rest % qo.ax.grid[a];
+                rest /= qo.ax.grid[a];
+                tab_row[a] = qo.ax.tab_off[a] + cc * qo.ax.pairs[a] - qo.ax.pair_start[a];
+            }
+        }
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const int n = n0 + wn * 128 + nt * 32 + rb * 8 + g * 4;
+                if (n >= N) continue;
+                f32x4 v = {acc[nt][mt][rb * 4 + 0], acc[nt][mt][rb * 4 + 1],
+                           acc[nt][mt][rb * 4 + 2], acc[nt][mt][rb * 4 + 3]};
+                if constexpr (QKV) {
+                    const int hd = qo.H * qo.d;
+                    const int z = n / hd, r = n - z * hd;
+                    if (z < 2 && qo.table != nullptr) {
+                        const int e = r % qo.d;  // a multiple of 4: pairs e/2 and e/2 + 1
+#pragma unroll
+                        for (int q2 = 0; q2 < 2; ++q2) {
+                            const int p = e / 2 + q2;
+                            int a = 0;
+                            while (a + 1 < qo.ax.n_axes && p >= qo.ax.pair_start[a + 1]) ++a;
+                            const f32x2 cs =
+                                *reinterpret_cast<const f32x2 *>(qo.table + 2 * (tab_row[a] + p));
+                            const float x0 = v[2 * q2], x1 = v[2 * q2 + 1];
+                            v[2 * q2] = __builtin_fmaf(x0, cs[0], -(x1 * cs[1]));
+                            v[2 * q2 + 1] = __builtin_fmaf(x0, cs[1], x1 * cs[0]);
+                        }
+                    }
+                    store4(qo.dst[z] + static_cast<int64_t>(m) * hd + r, v);
+                } else {
+                    store4(y + static_cast<int64_t>(m) * N + n, v);
+                }
+            }
+    }
+}
+
+// Rotation table: entry e of axis a (tab_off[a] <= e < tab_off[a] + grid[a] *
+// pairs[a]) is (cos, sin) of c * base^(-i' / pairs[a]), c = (e - tab_off[a]) /
+// pairs[a], i' = (e - tab_off[a]) % pairs[a]; computed in fp64, rounded to fp32.
+__global__ __launch_bounds__(256) void rope_table_kernel(float *table, RopeAxes ax, double base,
+                                                         int total) {
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= total) return;
+    int a = 0;
+    while (a + 1 < ax.n_axes && e >= ax.tab_off[a + 1]) ++a;
+    const int rel = e - ax.tab_off[a];
+    const int c = rel / ax.pairs[a], ip = rel % ax.pairs[a];
+    const double ang = static_cast<double>(c) *
+                       pow(base, -static_cast<double>(ip) / static_cast<double>(ax.pairs[a]));
+    table[2 * e] = static_cast<float>(cos(ang));
+    table[2 * e + 1] = static_cast<float>(sin(ang));
+}
+
+template <typename T, bool QKV>
+hipError_t launch_typed(const void *x, const void *w, void *y, int M, int N, int K,
+                        const QkvOut<T> &qo, hipStream_t stream) {
+    const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+    const int64_t blocks = static_cast<int64_t>(tiles_m) * tiles_n;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    linear_kernel<T, QKV><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
+        static_cast<const T *>(x), static_cast<const T *>(w), static_cast<T *>(y), M, N, K, tiles_m,
+        tiles_n, qo);
+    return hipGetLastError();
+}
+
+template <typename T>
+QkvOut<T> qkv_out(void *q, void *k, void *v, const float *table, const RopeAxes &ax, int H, int d) {
+    QkvOut<T> o{};
+    o.dst[0] = static_cast<T *>(q);
+    o.dst[1] = static_cast<T *>(k);
+    o.dst[2] = static_cast<T *>(v);
+    o.table = table;
+    o.H = H;
+    o.d = d;
+    o.ax = ax;
+    return o;
+}
+
+}  // namespace
+
+int linear_k_multiple() { return kBK; }
+
+hipError_t launch_linear(const void *x, const void *w, void *y, int M, int N, int K, int dtype,
+                         hipStream_t stream) {
+    if (M == 0 || N == 0) return hipSuccess;
+    if (dtype == 0) return launch_typed<__bf16, false>(x, w, y, M, N, K, QkvOut<__bf16>{}, stream);
+    if (dtype == 1) return launch_typed<float, false>(x, w, y, M, N, K, QkvOut<float>{}, stream);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_qkv_projection(const void *x, const void *w, void *q, void *k, void *v,
+                                 const float *table, const RopeAxes &ax, int S, int D, int H, int d,
+                                 int dtype, hipStream_t stream) {
+    if (S == 0) return hipSuccess;
+    const int N = 3 * H * d;
+    if (dtype == 0)
+        return launch_typed<__bf16, true>(x, w, nullptr, S, N, D,
+                                          qkv_out<__bf16>(q, k, v, table, ax, H, d), stream);
+    if (dtype == 1)
+        return launch_typed<float, true>(x, w, nullptr, S, N, D,
+                                         qkv_out<float>(q, k, v, table, ax, H, d), stream);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_rope_table(float *table, const RopeAxes &ax, double base, hipStream_t stream) {
+    const int last = ax.n_axes - 1;
+    const int total = ax.tab_off[last] + ax.grid[last] * ax.pairs[last];
+    if (total == 0) return hipSuccess;
+    rope_table_kernel<<<(total + 255) / 256, 256, 0, stream>>>(table, ax, base, total);
+    return hipGetLastError();
+}
+
+}  // namespace hcms

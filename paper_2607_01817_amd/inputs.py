@@ -124,3 +124,87 @@ def sample_rows(w: Workload, n: int | None = None, seed: int | None = None):
     return [np.sort(rng.choice(w.S, size=n, replace=False)).astype(np.int64)
             for _ in range(w.H)]
 
+
+
+# ---------------------------------------------------------------------------
+# Layer workloads: the attention layer around the chunk loop
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass(frozen=True)
+class LayerWorkload:
+    """One GPU's share of an attention layer: S tokens of width D, H local
+    heads of dimension d (the QKV projection produces 3 H d features per
+    token, the output projection maps the H d concatenated head features
+    back to D), the tokens laid on a latent grid for the rotary embedding,
+    whose d/2 pairs split into the groups ``axis_pairs`` (one per axis)."""
+    name: str
+    grid: tuple
+    axis_pairs: tuple
+    H: int
+    d: int
+    D: int
+    dtype: str
+    P: int
+    chunkings: tuple
+    seed: int
+    oracle_rows: int      # token rows checked against the oracle (0 = all)
+    base: float = 10000.0
+
+    @property
+    def S(self) -> int:
+        return int(np.prod(self.grid))
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.d)
+
+    @property
+    def flops(self) -> dict:
+        """Algorithmic FLOPs of the three steps (2 per multiply-add)."""
+        S, H, d, D = self.S, self.H, self.d, self.D
+        return {"qkv_projection": 2.0 * S * D * 3 * H * d,
+                "attention": 4.0 * S * S * H * d,
+                "output_projection": 2.0 * S * H * d * D}
+
+
+LAYERS = {
+    # Small enough for the whole layer in the oracle.
+    "layer_small": LayerWorkload("layer_small", (4, 6, 10), (12, 10, 10), 4, 64, 256, "bf16", 4,
+                                 ((4,), (2, 2), (3, 1)), 11, 0),
+    # Odd grid, tails in every dimension of the tiles.
+    "layer_ragged": LayerWorkload("layer_ragged", (3, 7, 13), (22, 21, 21), 3, 128, 192, "bf16",
+                                  3, ((3,), (2, 1)), 12, 0),
+    # fp32 storage.
+    "layer_fp32": LayerWorkload("layer_fp32", (2, 8, 16), (12, 10, 10), 2, 64, 128, "fp32", 2,
+                                ((2,), (1, 1)), 13, 0),
+    # Wan2.2-14B-shaped rank share at P = 8: 36 latent frames of 30 x 52 patch
+    # tokens (1560 per frame), 5 of the 40 heads, model width 5120.
+    "layer_wan_p8": LayerWorkload("layer_wan_p8", (36, 30, 52), (22, 21, 21), 5, 128, 5120,
+                                  "bf16", 8, ((5,), (2, 2, 1)), 14, 32),
+}
+
+
+def make_layer(w: LayerWorkload, seed: int | None = None):
+    """Host tensors of a layer: x [S][D] ~ N(0, 1), the QKV weight [3 H d][D]
+    and the output weight [D][H d], each ~ N(0, 1) divided by the square root
+    of its input width (so every projected feature has unit variance), all
+    stored [out][in], drawn in that order as fp32 ``randn`` from a CPU
+    generator seeded with ``seed`` (default ``w.seed``) and rounded to the
+    storage dtype."""
+    seed = w.seed if seed is None else seed
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    S, H, d, D = w.S, w.H, w.d, w.D
+    x = torch.randn((S, D), generator=g, dtype=torch.float32).to(dt)
+    w_qkv = (torch.randn((3 * H * d, D), generator=g, dtype=torch.float32) / math.sqrt(D)).to(dt)
+    w_o = (torch.randn((D, H * d), generator=g, dtype=torch.float32) / math.sqrt(H * d)).to(dt)
+    return x, w_qkv, w_o
+
+
+def sample_tokens(w: LayerWorkload, n: int | None = None, seed: int | None = None) -> np.ndarray:
+    """Sorted token rows for oracle checks of a layer (all when n is 0)."""
+    n = w.oracle_rows if n is None else n
+    seed = w.seed if seed is None else seed
+    if n == 0 or n >= w.S:
+        return np.arange(w.S, dtype=np.int64)
+    rng = np.random.default_rng(seed + 1000)
+    return np.sort(rng.choice(w.S, size=n, replace=False)).astype(np.int64)

@@ -371,3 +371,88 @@ def test_training_forward_and_backward_validation(lib):
     assert bwd(delta=F + 16) == EALIAS  # workspace over a gradient
     assert bwd(d=96) == ESHAPE
     assert bwd(S=0, dout=None, dq=None, dk=None, dv=None, lse=None, delta=None) == OK
+
+
+# ---------------------------------------------------------------------------
+# Layer neighbours: projection GEMM, rotation table, QKV projection, layer
+# ---------------------------------------------------------------------------
+def _ints(xs):
+    return (ctypes.c_int * max(1, len(xs)))(*xs)
+
+
+def test_linear_validation(lib):
+    f = lib.hcms_linear
+
+    def call(x=A, w=B, y=C_, M=300, N=264, K=128, dtype=0):
+        return f(x, w, y, M, N, K, dtype, None)
+
+    assert call(dtype=3) == EDTYPE
+    assert call(K=0) == ESHAPE
+    assert call(K=100) == ESHAPE            # not a multiple of 64
+    assert call(K=2**21) == ESHAPE
+    assert call(N=12) == ESHAPE             # not a multiple of 8
+    assert call(M=-1) == ESHAPE
+    assert call(x=None) == ENULL
+    assert call(y=None) == ENULL
+    assert call(w=B + 8) == EALIGN
+    assert call(y=A) == EALIAS
+    assert call(y=B + 1024) == EALIAS
+    assert call(M=0) == OK                  # nothing enqueued
+    assert call(M=0, x=None, y=None) == OK
+    assert call(N=0, w=None, y=None) == OK
+
+
+def test_rope_table_validation(lib):
+    assert lib.hcms_rope_table_entries(_ints((36, 30, 52)), _ints((22, 21, 21)), 3) == \
+        36 * 22 + 30 * 21 + 52 * 21
+    assert lib.hcms_rope_table_entries(_ints((512,)), _ints((32,)), 1) == 512 * 32
+    assert lib.hcms_rope_table_entries(None, _ints((1,)), 1) == ENULL
+    assert lib.hcms_rope_table_entries(_ints((4,)), _ints((1,)), 0) == EARG
+    assert lib.hcms_rope_table_entries(_ints((1,) * 5), _ints((1,) * 5), 5) == EARG
+    assert lib.hcms_rope_table_entries(_ints((4, 0)), _ints((1, 1)), 2) == ESHAPE
+    assert lib.hcms_rope_table_entries(_ints((4, 4)), _ints((1, 0)), 2) == ESHAPE
+    assert lib.hcms_rope_table_entries(_ints((2**16, 2**16)), _ints((1, 1)), 2) == ESHAPE
+    g, p = _ints((4, 6)), _ints((8, 8))
+    assert lib.hcms_rope_table(None, g, p, 2, 1e4, None) == ENULL
+    assert lib.hcms_rope_table(A + 4, g, p, 2, 1e4, None) == EALIGN
+    assert lib.hcms_rope_table(A, g, p, 2, 1.0, None) == EARG
+    assert lib.hcms_rope_table(A, g, p, 2, float("inf"), None) == EARG
+
+
+def test_qkv_projection_validation(lib):
+    f = lib.hcms_qkv_projection
+    big = 2**26
+
+    def call(x=A, w=B, table=C_, grid=(4, 6, 10), pairs=(12, 10, 10), q=D_, k=D_ + big,
+             v=D_ + 2 * big, S=240, D=256, H=4, d=64, dtype=0):
+        return f(x, w, table, _ints(grid), _ints(pairs), len(grid), q, k, v, S, D, H, d, dtype, None)
+
+    assert call(d=12) == ESHAPE                 # not a multiple of 8
+    assert call(H=0) == ESHAPE
+    assert call(D=100) == ESHAPE                # K of the GEMM
+    assert call(grid=(4, 6, 11)) == ESHAPE      # 264 tokens, not 240
+    assert call(pairs=(12, 10, 9)) == ESHAPE    # 31 pairs, not 32
+    assert call(k=None) == ENULL
+    assert call(v=D_ + 2 * big + 4) == EALIGN
+    assert call(table=C_ + 8) == EALIGN
+    assert call(k=D_ + 1024) == EALIAS          # outputs overlap
+    assert call(q=A) == EALIAS                  # output overlaps x
+    assert call(table=D_ + 4096) == EALIAS      # table overlaps q
+    assert call(S=0, x=None, q=None, k=None, v=None) == OK
+    # Without a table, grid and pairs are not looked at.
+    assert f(A, B, None, None, None, 0, D_, D_ + big, D_ + 2 * big, 0, 256, 4, 64, 0, None) == OK
+
+
+def test_layer_forward_validation(lib):
+    big = 2**26
+    sizes = _ints((2, 2))
+
+    def call(ctx=None, x=A, wq=B, wo=B + big, table=C_, y=C_ + big, S=240, D=256, H=4, d=64,
+             grid=(4, 6, 10), pairs=(12, 10, 10)):
+        t = [D_ + i * big for i in range(8)]
+        return lib.hcms_layer_forward(ctx, x, wq, wo, table, _ints(grid), _ints(pairs), len(grid),
+                                      y, *t, 4, S, D, H, d, 0.125, sizes, 2, 0, 1, None, None, None)
+
+    assert call() == ENULL                      # no context
+    assert call(grid=(4, 6, 11)) == ESHAPE      # checked before the context
+    assert call(D=100) == ESHAPE
