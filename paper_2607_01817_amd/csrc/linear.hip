@@ -24,9 +24,10 @@
 //     columns n: 8-byte stores of bf16, and whole rotation pairs;
 //   * k advances in blocks of 64: the 256 x 64 blocks of X and W are staged
 //     global -> registers -> LDS (rows padded to 144 bytes, so 16 lanes
-//     reading 16 rows hit 16 disjoint groups of 4 banks), double-buffered, the
-//     next block's global loads in flight while the current one is consumed;
-//     every operand read from LDS feeds 2 (W) or 4 (X) MFMAs;
+//     reading 16 rows hit 16 disjoint groups of 4 banks), double-buffered in
+//     LDS, with two register sets so that each block's global loads are
+//     issued two k-blocks before its MFMAs; every operand read from LDS feeds
+//     2 (W) or 4 (X) MFMAs;
 //   * tiles are ordered in groups of 8 row tiles (all column tiles of a group
 //     before the next group), and the 8 XCDs each take a contiguous range of
 //     that order, so the 32 workgroups resident on an XCD share 8 X panels and
@@ -46,11 +47,20 @@ using namespace tiles;
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBM = 256, kBN = 256, kBK = 64;
-constexpr int kThreads = 512;
+#ifndef HCMS_LINEAR_WAVES
+#define HCMS_LINEAR_WAVES 8
+#endif
+constexpr int kWaves = HCMS_LINEAR_WAVES;    // 8: 64 x 128 per wave; 4: 128 x 128 per wave
+constexpr int kThreads = 64 * kWaves;
+constexpr int kWavesN = 2;                   // waves across the 256 columns
+constexpr int kWavesM = kWaves / kWavesN;    // waves across the 256 rows
+constexpr int kMT = kBM / kWavesM / 32;      // 32-row tiles per wave
+constexpr int kNT = kBN / kWavesN / 32;      // 32-column tiles per wave
 constexpr int kRow = kBK + 8;            // LDS row stride, elements (144 bytes)
 constexpr int kTile = 256 * kRow;        // one staged 256 x 64 block, elements
 constexpr int kGroupM = 8;               // row tiles per group of the tile order
 constexpr int kPass = 256 * (kBK / 8) / kThreads;  // 16-byte chunks per thread per block
+constexpr int kRowsPerPass = kThreads / 8;
 
 // Arguments of the QKV epilogue: destinations, and the rotation (table NULL:
 // no rotation).  table holds (cos, sin) pairs; axis a, coordinate c, pair i'
@@ -71,7 +81,7 @@ __device__ inline __amdgpu_buffer_rsrc_t span_rsrc(const void *base, int64_t byt
 }
 
 // Global -> register staging of the 256 x 64 blocks of X and W at column k0.
-// Thread tid moves chunk tid % 8 (8 elements) of rows tid / 8 + 64 p.
+// Thread tid moves chunk tid % 8 (8 elements) of rows tid / 8 + kRowsPerPass p.
 template <typename T>
 struct Stager {
     u32x4 xr[kPass], wr[kPass];
@@ -80,7 +90,7 @@ struct Stager {
         const unsigned col = (static_cast<unsigned>(k0) + (tid & 7) * 8) * sizeof(T);
 #pragma unroll
         for (int p = 0; p < kPass; ++p) {
-            const unsigned off = static_cast<unsigned>(tid / 8 + 64 * p) * row_bytes + col;
+            const unsigned off = static_cast<unsigned>(tid / 8 + kRowsPerPass * p) * row_bytes + col;
             xr[p] = load8<T>(xs, off);
             wr[p] = load8<T>(ws, off);
         }
@@ -88,7 +98,7 @@ struct Stager {
     __device__ void store(__bf16 *xt, __bf16 *wt, int tid) const {
 #pragma unroll
         for (int p = 0; p < kPass; ++p) {
-            const int e = (tid / 8 + 64 * p) * kRow + (tid & 7) * 8;
+            const int e = (tid / 8 + kRowsPerPass * p) * kRow + (tid & 7) * 8;
             *reinterpret_cast<u32x4 *>(xt + e) = xr[p];
             *reinterpret_cast<u32x4 *>(wt + e) = wr[p];
         }
@@ -125,48 +135,63 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int li = lane & 31, g = lane >> 5;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / kWavesN, wn = wave % kWavesN;
 
-    f32x16 acc[4][2];  // [n tile][m tile]
+    f32x16 acc[kNT][kMT];  // [n tile][m tile]
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+    for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) acc[nt][mt] = f32x16{};
+        for (int mt = 0; mt < kMT; ++mt) acc[nt][mt] = f32x16{};
 
+    // NSETS register sets carry the blocks from global memory to LDS.  With
+    // two (bf16 storage), block b is loaded into set b & 1 during k-block
+    // b - 2 and stored to LDS buffer b & 1 after k-block b - 1's MFMAs, so each
+    // load has two k-blocks to arrive; with one (fp32 storage, whose loads
+    // need twice the registers) it is loaded during k-block b - 1.  The loop
+    // has no branches: the loads of blocks past the end read within the
+    // resources (the next row's data or zeros) and the last store goes to a
+    // buffer nobody reads.
+    constexpr int NSETS = sizeof(T) == 2 ? 2 : 1;
     const int nkb = K / kBK;
-    Stager<T> st;
-    st.load(xs, ws, row_bytes, 0, tid);
-    st.store(xt[0], wt[0], tid);
+    Stager<T> st[NSETS];
+    st[0].load(xs, ws, row_bytes, 0, tid);
+    st[0].store(xt[0], wt[0], tid);
+    if (NSETS == 2) st[1 % NSETS].load(xs, ws, row_bytes, kBK, tid);
     __syncthreads();
-    for (int kb = 0; kb < nkb; ++kb) {
-        const bool more = kb + 1 < nkb;
-        if (more) st.load(xs, ws, row_bytes, (kb + 1) * kBK, tid);
-        const __bf16 *xa = xt[kb & 1] + (wm * 64 + li) * kRow + g * 8;
-        const __bf16 *wa = wt[kb & 1] + (wn * 128 + li) * kRow + g * 8;
+    auto step = [&](int kb, Stager<T> &ld, const Stager<T> &sto) {
+        ld.load(xs, ws, row_bytes, (kb + NSETS) * kBK, tid);
+        const __bf16 *xa = xt[kb & 1] + (wm * kMT * 32 + li) * kRow + g * 8;
+        const __bf16 *wa = wt[kb & 1] + (wn * kNT * 32 + li) * kRow + g * 8;
 #pragma unroll
         for (int ks = 0; ks < kBK / 16; ++ks) {
-            bf16x8 a[4], bx[2];
+            bf16x8 a[kNT], bx[kMT];
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < kNT; ++nt)
                 a[nt] = *reinterpret_cast<const bf16x8 *>(wa + nt * 32 * kRow + ks * 16);
 #pragma unroll
-            for (int mt = 0; mt < 2; ++mt)
+            for (int mt = 0; mt < kMT; ++mt)
                 bx[mt] = *reinterpret_cast<const bf16x8 *>(xa + mt * 32 * kRow + ks * 16);
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt)
+                for (int mt = 0; mt < kMT; ++mt)
                     acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nt], bx[mt], acc[nt][mt],
                                                                           0, 0, 0);
         }
-        if (more) st.store(xt[(kb + 1) & 1], wt[(kb + 1) & 1], tid);
+        sto.store(xt[(kb + 1) & 1], wt[(kb + 1) & 1], tid);
         __syncthreads();
+    };
+    int kb = 0;
+    for (; kb + 1 < nkb; kb += 2) {
+        step(kb, st[0], st[1 % NSETS]);
+        step(kb + 1, st[1 % NSETS], st[0]);
     }
+    if (kb < nkb) step(kb, st[0], st[1 % NSETS]);
 
     // ---- Y[m][n .. n + 3] from the D^T accumulators, rounded to T ----
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-        const int m = m0 + wm * 64 + mt * 32 + li;
+    for (int mt = 0; mt < kMT; ++mt) {
+        const int m = m0 + wm * kMT * 32 + mt * 32 + li;
         if (m >= M) continue;
         // Per grid axis, the table entry of pair 0 of the axis at token m's
         // coordinate (QKV epilogue with a rotation only).
@@ -180,10 +205,10 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
             }
         }
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb) {
-                const int n = n0 + wn * 128 + nt * 32 + rb * 8 + g * 4;
+                const int n = n0 + wn * kNT * 32 + nt * 32 + rb * 8 + g * 4;
                 if (n >= N) continue;
                 f32x4 v = {acc[nt][mt][rb * 4 + 0], acc[nt][mt][rb * 4 + 1],
                            acc[nt][mt][rb * 4 + 2], acc[nt][mt][rb * 4 + 3]};
