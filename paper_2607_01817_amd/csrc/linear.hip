@@ -105,6 +105,25 @@ struct Stager {
     }
 };
 
+// Scheduling hint for one k-block: the operand reads of k-step ks + 1 and
+// the LDS stores of the next block run between the MFMAs of k-step ks.
+__device__ inline void interleave_k_block() {
+    constexpr int kReads = kNT + kMT;            // operand reads per k-step
+    constexpr int kMfma = kNT * kMT;             // MFMAs per k-step
+    constexpr int kWrites = 2 * kPass;           // LDS stores per k-block
+    constexpr int kSteps = kBK / 16;
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);  // DS read, k-step 0
+#pragma unroll
+    for (int ks = 0; ks < kSteps; ++ks) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __builtin_amdgcn_sched_group_barrier(0x008, kMfma / 2, 0);           // MFMA
+            if (ks + 1 < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, kReads / 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x200, kWrites / (2 * kSteps), 0);  // DS write
+        }
+    }
+}
+
 template <typename T, bool QKV>
 __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict__ x,
                                                              const T *__restrict__ w,
@@ -179,6 +198,7 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
                                                                           0, 0, 0);
         }
         sto.store(xt[(kb + 1) & 1], wt[(kb + 1) & 1], tid);
+        interleave_k_block();
         __syncthreads();
     };
     int kb = 0;
