@@ -286,6 +286,66 @@ def training_step(ctx, w, chunks, reps: int, dev):
     return res
 
 
+def layer_step(ctx, lw, chunks, reps: int, dev):
+    """One attention layer around the chunk loop on the Wan2.2-shaped rank
+    share: the QKV projection (split and rotary embedding fused), the chunked
+    forward in the auto schedule, the output projection, each timed on its
+    own, and the whole hcms_layer_forward.  The projection GEMM's roofline is
+    the bf16 MFMA peak; torch.matmul (hipBLASLt) on the same shapes is shown
+    beside it as a reference only."""
+    x, w_qkv, w_o = (t.to(dev) for t in inputs.make_layer(lw))
+    table = hcms.rope_table(lw.grid, lw.axis_pairs, lw.base)
+    S, H, d, D = lw.S, lw.H, lw.d, lw.D
+    qkv = tuple(torch.empty((S, H, d), dtype=x.dtype, device=dev) for _ in range(3))
+    o = torch.empty((S, H, d), dtype=x.dtype, device=dev)
+    y = torch.empty((S, D), dtype=x.dtype, device=dev)
+    ws = ctx.workspaces(S, H, d, x.dtype)
+    steps = {
+        "qkv_projection": lambda: hcms.qkv_projection(x, w_qkv, H, d, table, lw.grid,
+                                                      lw.axis_pairs, out=qkv),
+        "attention_chunks": lambda: ctx.forward(qkv[0], qkv[1], qkv[2], lw.P, lw.scale, chunks,
+                                                out=o, workspaces=ws),
+        "output_projection": lambda: hcms.linear(o.view(S, H * d), w_o, out=y),
+        "layer": lambda: ctx.layer_forward(x, w_qkv, w_o, lw.P, H, d, lw.scale, chunks, table,
+                                           lw.grid, lw.axis_pairs, out=y),
+    }
+    for fn in steps.values():
+        for _ in range(5):
+            fn()
+    torch.cuda.synchronize()
+    res = {"workload": f"{lw.name}: S={S} ({'x'.join(map(str, lw.grid))} latent grid), H={H}, "
+                       f"d={d}, D={D}, bf16, chunks {'+'.join(map(str, chunks))}",
+           "chunks": list(chunks)}
+    fl = lw.flops
+    flops = {"qkv_projection": fl["qkv_projection"], "attention_chunks": fl["attention"],
+             "output_projection": fl["output_projection"], "layer": sum(fl.values())}
+    for name, fn in steps.items():
+        q3 = quartiles(time_region(fn, reps))
+        res[name] = {"ms": q3, "TFLOPs": round(flops[name] / (q3["median"] * 1e-3) / 1e12, 1)}
+    ref = {}
+    xr = o.view(S, H * d)
+    for name, a, b_ in (("qkv_projection", x, w_qkv), ("output_projection", xr, w_o)):
+        out = torch.empty((a.shape[0], b_.shape[0]), dtype=a.dtype, device=dev)
+        for _ in range(5):
+            torch.matmul(a, b_.t(), out=out)
+        ref[name] = round(statistics.median(
+            time_region(lambda: torch.matmul(a, b_.t(), out=out), reps)), 4)
+        del out
+    qp = res["qkv_projection"]
+    res["gemm_roofline"] = {
+        "bound": "mfma", "achieved": qp["TFLOPs"], "peak": MFMA_BF16_PEAK_TFLOPS,
+        "unit": "TFLOP/s", "frac": round(qp["TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4),
+        "kernel": "linear_kernel<bf16, qkv epilogue>",
+        "per_launch": f"2*S*D*3*H*d = {fl['qkv_projection']:.3e} FLOP per launch; median "
+                      f"{qp['ms']['median']} ms over {reps} launches"}
+    res["reference_torch_matmul_ms"] = ref
+    res["note"] = ("TFLOPs of each step count its algorithmic FLOPs (2 per multiply-add; attention "
+                   "4 S^2 H d); reference_torch_matmul_ms is hipBLASLt on the plain GEMMs of the "
+                   "same shapes, not part of the path")
+    del x, w_qkv, w_o, qkv, o, y, table
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -454,6 +514,10 @@ def main():
 
         # ---- training: forward with the softmax statistic, then backward ----
         result["training"] = training_step(ctx, w, sizes, max(10, args.steps // 4), dev)
+
+        # ---- the attention layer around the chunk loop (Wan-P8 share) ----
+        lw = inputs.LAYERS["layer_wan_p8"]
+        result["layer"] = layer_step(ctx, lw, lw.chunkings[-1], max(10, args.steps // 2), dev)
 
         # ---- the time model over the chunk count (Wan-P8, Wan-P4) ----
         result["time_model"] = [time_model_sweep(ctx, tw, reps, dev)
