@@ -135,7 +135,7 @@ def cpu_baseline(w, q, k, v, seconds: float):
 
 
 MODES = {"serial": hcms.MODE_SERIAL, "pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE,
-         "lanes": hcms.MODE_LANES, "auto": hcms.MODE_AUTO}
+         "lanes": hcms.MODE_LANES, "auto": hcms.MODE_AUTO, "slots": hcms.MODE_SLOTS}
 MODE_NAMES = {v: k for k, v in MODES.items()}
 
 
@@ -151,12 +151,20 @@ def compare_modes(ctx, w, chunks, reps: int, dev):
     q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
     out = torch.empty_like(q)
     ws = ctx.workspaces(w.S, w.H, w.d, q.dtype)
-    modes = ["serial", "pipelined", "inline", "lanes"]
+    slots = ctx.slot_workspaces(w.S, max(chunks), w.d, q.dtype)
+    modes = ["serial", "pipelined", "inline", "lanes", "slots_two_slot"]
+
+    def run(m):
+        if m == "slots_two_slot":   # the slots plan on two chunk slots
+            return lambda: ctx.forward_slots(q, k, v, w.P, w.scale, chunks, mode=hcms.MODE_SLOTS,
+                                             out=out, slots=slots)
+        return lambda: ctx.forward(q, k, v, w.P, w.scale, chunks, mode=MODES[m], out=out,
+                                   workspaces=ws)
+
     times = {m: [] for m in modes}
     for r in range(reps + 1):
         for m in (modes if r % 2 == 0 else modes[::-1]):
-            t = time_region(lambda: ctx.forward(q, k, v, w.P, w.scale, chunks, mode=MODES[m],
-                                                out=out, workspaces=ws), 1)
+            t = time_region(run(m), 1)
             if r > 0:
                 times[m] += t
     ctx.forward(q, k, v, w.P, w.scale, chunks, mode=hcms.MODE_AUTO, out=out, workspaces=ws)
@@ -168,7 +176,10 @@ def compare_modes(ctx, w, chunks, reps: int, dev):
         qm["gain_vs_serial_ms"] = round(ser["median"] - qm["median"], 4)
         qm["below_serial"] = bool(qm["iqr"][1] < ser["iqr"][0])
         res[m + "_ms"] = qm
-    del q, k, v, out
+    es = q.element_size()
+    res["workspace_bytes"] = {"full": 4 * w.S * w.H * w.d * es,
+                              "two_slot": 4 * 2 * max(chunks) * w.S * w.d * es}
+    del q, k, v, out, slots
     return res
 
 

@@ -182,6 +182,7 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
 #define HCMS_MODE_INLINE 2     /* one lane, four synchronisations (see hcms_plan) */
 #define HCMS_MODE_LANES 3      /* chunks alternate between two streams (see hcms_plan) */
 #define HCMS_MODE_AUTO 4       /* hcms_forward only: inline or lanes, per hcms_auto_mode */
+#define HCMS_MODE_SLOTS 5      /* Alg. 1's streams, copies interleaved so slots can be reused */
 
 /* Op kinds, streams and event ids of a plan (hcms_plan). */
 #define HCMS_OP_RECORD 0     /* record event `event` on `stream` */
@@ -230,6 +231,12 @@ typedef struct hcms_op {
  * copies, the attention launches of the two lanes overlap, so that the
  * workgroups of one fill the CUs the last round of the other leaves idle.
  * The copy stream is not used.
+ * Slots mode uses Alg. 1's streams and events but interleaves the copy stream
+ * with the attentions: the copy stream packs chunks 0 and 1, then, for every
+ * c, waits E_c^attn, unpacks c and packs c + 2 (recording E_{c+2}^pack), so
+ * that chunk c + 2 can reuse chunk c's workspace slot (the input layout of one
+ * chunk and the output layout of another beside a chunk's attention,
+ * Sec. 3.5).  The host issues every record before any wait on it.
  * With one chunk the inline and lanes plans are the serial plan.
  *   ops : host array of `cap` entries, or NULL to query the count.
  * Returns the number of ops (>= 0), HCMS_ERR_CHUNKS (n_chunks < 1),
@@ -342,6 +349,28 @@ HCMS_API int hcms_forward(hcms_ctx *ctx,
                  int P, int S, int H, int d, float scale,
                  const int *chunk_sizes, int n_chunks, int dtype, int mode,
                  void *main_stream, void *copy_stream, void *compute_stream);
+
+/*
+ * hcms_forward with two chunk slots instead of full head-major workspaces
+ * (the memory reduction of the chunked pipeline: only the chunks in flight
+ * need a head-major copy).  q_slots, k_slots, v_slots, o_slots are device
+ * buffers of [2][slot_heads][S][d] each; chunk c uses slot c % 2 (its heads
+ * at the slot's start), so slot_heads must be at least every chunk size.
+ * Modes: HCMS_MODE_SERIAL, HCMS_MODE_LANES, HCMS_MODE_SLOTS and HCMS_MODE_AUTO
+ * (lanes when hcms_auto_mode picks lanes, else serial).  Pipelined and inline
+ * modes would pack chunk c + 2 into chunk c's slot while its attention may
+ * still run, and are rejected with HCMS_ERR_ARG.  No lse output: the backward
+ * needs every head's head-major tensors.  o_seq is bit-identical to
+ * hcms_forward's for the same inputs, whatever the mode and chunking.
+ * Errors: as hcms_forward, plus CHUNKS (slot_heads < 1 or below a chunk size)
+ * and ARG (mode).
+ */
+HCMS_API int hcms_forward_slots(hcms_ctx *ctx, const void *q_seq, const void *k_seq,
+                                const void *v_seq, void *o_seq, void *q_slots, void *k_slots,
+                                void *v_slots, void *o_slots, int slot_heads, int P, int S, int H,
+                                int d, float scale, const int *chunk_sizes, int n_chunks, int dtype,
+                                int mode, void *main_stream, void *copy_stream,
+                                void *compute_stream);
 
 /*
  * The backward of hcms_forward, for training: the reverse pipeline of the

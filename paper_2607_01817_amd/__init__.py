@@ -22,7 +22,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhcms.so")
 
 BF16, FP32 = 0, 1
-MODE_SERIAL, MODE_PIPELINED, MODE_INLINE, MODE_LANES, MODE_AUTO = 0, 1, 2, 3, 4
+MODE_SERIAL, MODE_PIPELINED, MODE_INLINE, MODE_LANES, MODE_AUTO, MODE_SLOTS = 0, 1, 2, 3, 4, 5
 OP_RECORD, OP_WAIT, OP_PACK, OP_ATTENTION, OP_UNPACK = 0, 1, 2, 3, 4
 STREAM_MAIN, STREAM_COPY, STREAM_COMPUTE = 0, 1, 2
 
@@ -84,6 +84,8 @@ def load():
                           vp, vp, vp], i),
         "hcms_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i,
                            f, ip, i, i, i, vp, vp, vp], i),
+        "hcms_forward_slots": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, f, ip, i, i, i,
+                                vp, vp, vp], i),
         "hcms_linear": ([vp, vp, vp, i, i, i, i, vp], i),
         "hcms_rope_table_entries": ([ip, ip, i], i),
         "hcms_rope_table": ([vp, ip, ip, i, d, vp], i),
@@ -465,6 +467,45 @@ class Context:
             self._h, q_seq.data_ptr(), k_seq.data_ptr(), v_seq.data_ptr(), out.data_ptr(),
             ws[0].data_ptr(), ws[1].data_ptr(), ws[2].data_ptr(), ws[3].data_ptr(), lse_p,
             P, S, H, d, float(scale), sizes, n, _dtype(q_seq), int(mode), main,
+            ctypes.c_void_p(self.copy_stream.cuda_stream),
+            ctypes.c_void_p(self.compute_stream.cuda_stream)))
+        return out
+
+    def slot_workspaces(self, S: int, slot_heads: int, d: int, dtype: torch.dtype):
+        """Four two-slot head-major workspaces, [2][slot_heads][S][d] each."""
+        key = (S, slot_heads, d, dtype)
+        if getattr(self, "_sws_key", None) != key:
+            self._sws = [torch.empty((2, slot_heads, S, d), dtype=dtype,
+                                     device=f"cuda:{self.device}") for _ in range(4)]
+            self._sws_key = key
+        return self._sws
+
+    def forward_slots(self, q_seq: torch.Tensor, k_seq: torch.Tensor, v_seq: torch.Tensor, P: int,
+                      scale: float, chunk_sizes, mode: int = MODE_AUTO,
+                      out: torch.Tensor | None = None, slots=None, main_stream=None) -> torch.Tensor:
+        """:meth:`forward` with two chunk slots (``slots``: four
+        [2][slot_heads][S][d] buffers, slot_heads >= every chunk) instead of
+        full head-major workspaces; modes serial, lanes, slots or auto."""
+        for t, n in ((q_seq, "q_seq"), (k_seq, "k_seq"), (v_seq, "v_seq")):
+            _dev(t, n)
+        if not (q_seq.shape == k_seq.shape == v_seq.shape) or q_seq.dim() != 3:
+            raise ValueError("q_seq, k_seq, v_seq must all be [S][H][d]")
+        S, H, d = q_seq.shape
+        if out is None:
+            out = torch.empty_like(q_seq)
+        _dev(out, "out")
+        if slots is None:
+            slots = self.slot_workspaces(S, max(int(c) for c in chunk_sizes), d, q_seq.dtype)
+        slot_heads = slots[0].shape[1]
+        for t in slots:
+            _dev(t, "slot workspace")
+            if t.shape != (2, slot_heads, S, d) or t.dtype != q_seq.dtype:
+                raise ValueError("slot workspaces must be [2][slot_heads][S][d] of the input dtype")
+        sizes, n = _ints(chunk_sizes)
+        _check(load().hcms_forward_slots(
+            self._h, q_seq.data_ptr(), k_seq.data_ptr(), v_seq.data_ptr(), out.data_ptr(),
+            *[t.data_ptr() for t in slots], slot_heads, P, S, H, d, float(scale), sizes, n,
+            _dtype(q_seq), int(mode), _stream(main_stream),
             ctypes.c_void_p(self.copy_stream.cuda_stream),
             ctypes.c_void_p(self.compute_stream.cuda_stream)))
         return out

@@ -245,24 +245,60 @@ void lanes_plan(int C, PlanWriter &w) {
     w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
 }
 
+// The copy stream interleaved with the attentions, for chunk slots that are
+// reused: Alg. 1's streams and events, but after attention c the copy stream
+// unpacks c and then packs c + 2 (which reuses chunk c's slot; attention c + 2
+// therefore also comes after unpack c, which freed the output slot).  This is
+// the overlap of Sec. 3.5 -- the input layout of one chunk and the output
+// layout of another beside a chunk's attention -- in an order that needs only
+// two chunks' worth of head-major workspace.  The host issues every record
+// before any wait on it: the compute stream's ops of chunk c come before the
+// copy stream's ops that follow attention c.
+void slots_plan(int C, PlanWriter &w) {
+    const int e_main = 0, e_done = 1 + 2 * C;
+    auto e_pack = [](int c) { return 1 + c; };
+    auto e_attn = [C](int c) { return 1 + C + c; };
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_MAIN, -1, e_main);
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COPY, -1, e_main);
+    for (int c = 0; c < C && c < 2; ++c) {
+        w.put(HCMS_OP_PACK, HCMS_STREAM_COPY, c, -1);
+        w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_pack(c));
+    }
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_COMPUTE, -1, e_main);
+    for (int c = 0; c < C; ++c) {
+        w.put(HCMS_OP_WAIT, HCMS_STREAM_COMPUTE, -1, e_pack(c));
+        w.put(HCMS_OP_ATTENTION, HCMS_STREAM_COMPUTE, c, -1);
+        w.put(HCMS_OP_RECORD, HCMS_STREAM_COMPUTE, -1, e_attn(c));
+        w.put(HCMS_OP_WAIT, HCMS_STREAM_COPY, -1, e_attn(c));
+        w.put(HCMS_OP_UNPACK, HCMS_STREAM_COPY, c, -1);
+        if (c + 2 < C) {
+            w.put(HCMS_OP_PACK, HCMS_STREAM_COPY, c + 2, -1);
+            w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_pack(c + 2));
+        }
+    }
+    w.put(HCMS_OP_RECORD, HCMS_STREAM_COPY, -1, e_done);
+    w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
+}
+
 // Modes with a fixed plan (hcms_plan); HCMS_MODE_AUTO resolves to one of
 // them per call.
 bool plan_mode(int mode) {
     return mode == HCMS_MODE_SERIAL || mode == HCMS_MODE_PIPELINED ||
-           mode == HCMS_MODE_INLINE || mode == HCMS_MODE_LANES;
+           mode == HCMS_MODE_INLINE || mode == HCMS_MODE_LANES || mode == HCMS_MODE_SLOTS;
 }
 
 int build_plan(int C, int mode, PlanWriter &w) {
     if (mode == HCMS_MODE_SERIAL) serial_plan(C, w);
     else if (mode == HCMS_MODE_PIPELINED) alg1_plan(C, w);
     else if (mode == HCMS_MODE_INLINE) inline_plan(C, w);
+    else if (mode == HCMS_MODE_SLOTS) slots_plan(C, w);
     else lanes_plan(C, w);
     return w.n;
 }
 
 int plan_size(int C, int mode) {
-    if (mode == HCMS_MODE_SERIAL || (C == 1 && mode != HCMS_MODE_PIPELINED)) return 3 * C;
-    if (mode == HCMS_MODE_PIPELINED) return 7 * C + 5;
+    if (mode == HCMS_MODE_PIPELINED || mode == HCMS_MODE_SLOTS) return 7 * C + 5;
+    if (mode == HCMS_MODE_SERIAL || C == 1) return 3 * C;
     return mode == HCMS_MODE_INLINE ? 3 * C + 8 : 3 * C + 4;
 }
 
@@ -359,12 +395,15 @@ namespace {
 // HCMS_MODE_AUTO into *mode and returns the row size's log2 unit count.
 int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const int *chunk_sizes,
                    int n_chunks, int dtype, int *mode, int *log2u, void *main_stream,
-                   void *copy_stream, void *compute_stream) {
+                   void *copy_stream, void *compute_stream, bool slotted = false) {
     int st;
     const int m = *mode;
     if (!plan_mode(m) && m != HCMS_MODE_AUTO)
-        return fail(HCMS_ERR_ARG, "mode %d is not serial (0), pipelined (1), inline (2), lanes (3) "
-                    "or auto (4)", m);
+        return fail(HCMS_ERR_ARG, "mode %d is not serial (0), pipelined (1), inline (2), lanes (3), "
+                    "auto (4) or slots (5)", m);
+    if (slotted && (m == HCMS_MODE_PIPELINED || m == HCMS_MODE_INLINE))
+        return fail(HCMS_ERR_ARG, "mode %d packs chunk c + 2 before chunk c's attention is done; "
+                    "with two chunk slots use serial, lanes, slots or auto", m);
     if ((st = check_dtype(dtype)) != HCMS_OK) return st;
     if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
     if ((st = row_log2_units(d, dtype, log2u)) != HCMS_OK) return st;
@@ -374,10 +413,13 @@ int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const
         return fail(HCMS_ERR_CHUNKS, "n_chunks=%d exceeds the context's max_chunks=%d", n_chunks,
                     ctx->max_chunks);
     if ((st = check_scale(scale)) != HCMS_OK) return st;
-    if (m == HCMS_MODE_PIPELINED &&
+    if ((m == HCMS_MODE_PIPELINED || m == HCMS_MODE_SLOTS) &&
         (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
-        return fail(HCMS_ERR_ARG, "pipelined mode needs three distinct streams");
-    const int r = m == HCMS_MODE_AUTO ? auto_mode(S, d, chunk_sizes, n_chunks, ctx->n_cu) : m;
+        return fail(HCMS_ERR_ARG, "pipelined and slots modes need three distinct streams");
+    int r = m == HCMS_MODE_AUTO ? auto_mode(S, d, chunk_sizes, n_chunks, ctx->n_cu) : m;
+    // With two chunk slots the one-lane plan with few synchronisations is not
+    // available; auto then runs the serial plan (lanes when it saves a round).
+    if (slotted && m == HCMS_MODE_AUTO && r == HCMS_MODE_INLINE) r = HCMS_MODE_SERIAL;
     if (r == HCMS_MODE_INLINE && copy_stream == main_stream)
         return fail(HCMS_ERR_ARG, "inline mode needs a copy stream distinct from the main stream");
     if (r == HCMS_MODE_LANES && compute_stream == main_stream)
@@ -393,7 +435,7 @@ int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const
 }
 
 // Issues the plan of `mode` (already resolved): RECORD / WAIT ops on the
-// context's events, kernel ops through launch(kind, h0, h_count, stream),
+// context's events, kernel ops through launch(kind, chunk, h0, h_count, stream),
 // each bracketed by timing events while the context records.
 template <typename Launch>
 int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *main_stream,
@@ -434,7 +476,7 @@ int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *m
         const size_t slot = (call * 3 + (op.kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
         if (timed && (e = hipEventRecord(ctx->t_begin[slot], s)) != hipSuccess)
             return hip_fail(e, "hipEventRecord");
-        if ((e = launch(op.kind, offs[c], chunk_sizes[c], s)) != hipSuccess)
+        if ((e = launch(op.kind, c, offs[c], chunk_sizes[c], s)) != hipSuccess)
             return hip_fail(e, "kernel launch");
         if (timed && (e = hipEventRecord(ctx->t_end[slot], s)) != hipSuccess)
             return hip_fail(e, "hipEventRecord");
@@ -454,6 +496,7 @@ struct ForwardArgs {
     const int *chunk_sizes;
     int n_chunks, dtype, mode;
     void *main_stream, *copy_stream, *compute_stream;
+    int slot_heads = 0;  // 0: workspaces of H heads; else two slots of slot_heads heads
 };
 
 // Everything hcms_forward validates; resolves the mode and the row unit.
@@ -464,17 +507,26 @@ int check_forward(const ForwardArgs &f, int *mode, int *log2u) {
                     !f.o_hm))
         return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
     if ((st = check_schedule(f.ctx, f.P, f.S, f.H, f.d, f.scale, f.chunk_sizes, f.n_chunks, f.dtype,
-                             mode, log2u, f.main_stream, f.copy_stream, f.compute_stream)) != HCMS_OK)
+                             mode, log2u, f.main_stream, f.copy_stream, f.compute_stream,
+                             f.slot_heads > 0)) != HCMS_OK)
         return st;
+    if (f.slot_heads > 0)
+        for (int c = 0; c < f.n_chunks; ++c)
+            if (f.chunk_sizes[c] > f.slot_heads)
+                return fail(HCMS_ERR_CHUNKS, "chunk %d has %d heads, a slot holds %d", c,
+                            f.chunk_sizes[c], f.slot_heads);
     const void *all[8] = {f.q_seq, f.k_seq, f.v_seq, f.o_seq, f.q_hm, f.k_hm, f.v_hm, f.o_hm};
     for (const void *p : all)
         if (f.S > 0 && !aligned16(p)) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");
     const int64_t bytes = static_cast<int64_t>(f.S) * f.H * f.d * elem_bytes(f.dtype);
+    const int64_t ws_bytes = f.slot_heads > 0
+        ? static_cast<int64_t>(2) * f.slot_heads * f.S * f.d * elem_bytes(f.dtype) : bytes;
     for (int i = 0; i < 8; ++i)
         for (int j = i + 1; j < 8; ++j) {
             // Inputs may alias each other (read-only); everything else must not.
             const bool both_inputs = i < 3 && j < 3;
-            if (!both_inputs && overlaps(all[i], bytes, all[j], bytes))
+            if (!both_inputs && overlaps(all[i], i < 4 ? bytes : ws_bytes, all[j],
+                                         j < 4 ? bytes : ws_bytes))
                 return fail(HCMS_ERR_ALIAS, "tensor %d overlaps tensor %d", i, j);
         }
     if (f.lse) {
@@ -492,19 +544,25 @@ int check_forward(const ForwardArgs &f, int *mode, int *log2u) {
 int issue_forward(const ForwardArgs &f, int mode, int log2u) {
     const int64_t head_bytes = static_cast<int64_t>(f.S) * f.d * elem_bytes(f.dtype);
     const float c_log2e = scale_log2e(f.scale);
-    auto at = [head_bytes](void *p, int h0) { return static_cast<char *>(p) + head_bytes * h0; };
-    auto launch = [&](int kind, int h0, int hc, hipStream_t s) -> hipError_t {
+    // Chunk c's head-major buffers: its heads of the full workspaces, or slot
+    // c % 2 of the two-slot ones.
+    const int slot_heads = f.slot_heads;
+    auto at = [head_bytes, slot_heads](void *p, int c, int h0) {
+        const int64_t first = slot_heads > 0 ? static_cast<int64_t>(c & 1) * slot_heads : h0;
+        return static_cast<char *>(p) + head_bytes * first;
+    };
+    auto launch = [&](int kind, int c, int h0, int hc, hipStream_t s) -> hipError_t {
         if (kind == HCMS_OP_PACK) {
             const void *src[3] = {f.q_seq, f.k_seq, f.v_seq};
-            void *dst[3] = {at(f.q_hm, h0), at(f.k_hm, h0), at(f.v_hm, h0)};
+            void *dst[3] = {at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0)};
             return hcms::launch_pack(src, dst, 3, f.S, f.H, h0, hc, log2u, s);
         }
         if (kind == HCMS_OP_ATTENTION)
-            return hcms::launch_attention(at(f.q_hm, h0), at(f.k_hm, h0), at(f.v_hm, h0),
-                                          at(f.o_hm, h0),
+            return hcms::launch_attention(at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0),
+                                          at(f.o_hm, c, h0),
                                           f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr,
                                           f.S, hc, f.d, c_log2e, f.dtype, s);
-        const void *src[1] = {at(f.o_hm, h0)};
+        const void *src[1] = {at(f.o_hm, c, h0)};
         void *dst[1] = {f.o_seq};
         return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, s);
     };
@@ -756,7 +814,7 @@ int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
     if (n_chunks < 1) return fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be >= 1", n_chunks);
     if (!plan_mode(mode))
         return fail(HCMS_ERR_ARG, "mode %d has no fixed plan (serial 0, pipelined 1, inline 2, "
-                    "lanes 3)", mode);
+                    "lanes 3, slots 5)", mode);
     const int need = plan_size(n_chunks, mode);
     if (ops == nullptr) {
         ok();
@@ -905,6 +963,22 @@ int hcms_forward(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void
     return issue_forward(f, resolved, log2u);
 }
 
+int hcms_forward_slots(hcms_ctx *ctx, const void *q_seq, const void *k_seq, const void *v_seq,
+                       void *o_seq, void *q_slots, void *k_slots, void *v_slots, void *o_slots,
+                       int slot_heads, int P, int S, int H, int d, float scale,
+                       const int *chunk_sizes, int n_chunks, int dtype, int mode,
+                       void *main_stream, void *copy_stream, void *compute_stream) {
+    if (slot_heads < 1) return fail(HCMS_ERR_CHUNKS, "slot_heads=%d must be >= 1", slot_heads);
+    ForwardArgs f{ctx, q_seq, k_seq, v_seq, o_seq, q_slots, k_slots, v_slots, o_slots, nullptr, P,
+                  S, H, d, scale, chunk_sizes, n_chunks, dtype, mode, main_stream, copy_stream,
+                  compute_stream};
+    f.slot_heads = slot_heads;
+    int st, log2u = 0, resolved = mode;
+    if ((st = check_forward(f, &resolved, &log2u)) != HCMS_OK) return st;
+    if (S == 0) return ok();
+    return issue_forward(f, resolved, log2u);
+}
+
 int hcms_linear(const void *x, const void *w, void *y, int M, int N, int K, int dtype,
                 void *stream) {
     int st;
@@ -1040,7 +1114,7 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
     auto at = [head_bytes](const void *p, int h0) {
         return const_cast<char *>(static_cast<const char *>(p)) + head_bytes * h0;
     };
-    auto launch = [&](int kind, int h0, int hc, hipStream_t s) -> hipError_t {
+    auto launch = [&](int kind, int /*chunk*/, int h0, int hc, hipStream_t s) -> hipError_t {
         if (kind == HCMS_OP_PACK) {
             const void *src[1] = {dout_seq};
             void *dst[1] = {at(do_hm, h0)};

@@ -239,7 +239,8 @@ def test_plan_errors(lib):
     assert lib.hcms_plan(0, 1, None, 0) == ECHUNKS
     assert lib.hcms_plan(2, 7, None, 0) == EARG
     assert lib.hcms_plan(2, hcms.MODE_AUTO, None, 0) == EARG   # no fixed plan
-    assert lib.hcms_plan(2, 5, None, 0) == EARG
+    assert lib.hcms_plan(2, 6, None, 0) == EARG
+    assert lib.hcms_plan(2, hcms.MODE_SLOTS, None, 0) == 19
     assert lib.hcms_plan(2, hcms.MODE_INLINE, None, 0) == 14
     assert lib.hcms_plan(2, hcms.MODE_LANES, None, 0) == 10
     ops = (hcms.Op * 3)()
@@ -456,3 +457,57 @@ def test_layer_forward_validation(lib):
     assert call() == ENULL                      # no context
     assert call(grid=(4, 6, 11)) == ESHAPE      # checked before the context
     assert call(D=100) == ESHAPE
+
+
+# ---------------------------------------------------------------------------
+# Two chunk slots: the slots plan and hcms_forward_slots
+# ---------------------------------------------------------------------------
+def check_slot_reuse(ops, C):
+    """Chunk c + 2 reuses chunk c's slot: its pack must come after attention c
+    (which reads the Q, K, V slot) and its attention after unpack c (which
+    reads the O slot)."""
+    reach = happens_before(ops)
+    pk, at, up = (kernel_ops(ops, k) for k in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK))
+    for c in range(C - 2):
+        assert pk[c + 2] in reach[at[c]], f"pack {c + 2} may overwrite slot {c % 2} under attention {c}"
+        assert at[c + 2] in reach[up[c]], f"attention {c + 2} may overwrite O slot {c % 2} under unpack {c}"
+
+
+@pytest.mark.parametrize("C", [1, 2, 3, 5, 10])
+def test_slots_plan_orders_every_dependency_and_slot_reuse(lib, C):
+    ops = hcms.plan(C, hcms.MODE_SLOTS)
+    assert len(ops) == 7 * C + 5
+    pk, at, up = check_pipelined_dependencies(ops, C, hcms.STREAM_COMPUTE)
+    for c in range(C):
+        assert ops[pk[c]][1] == ops[up[c]][1] == hcms.STREAM_COPY
+    check_slot_reuse(ops, C)
+    reach = happens_before(ops)
+    # The copy stream still overlaps: pack c + 1 and unpack c - 1 are not
+    # ordered against attention c.
+    for c in range(1, C - 1):
+        assert at[c] not in reach[pk[c + 1]] and pk[c + 1] not in reach[at[c]]
+        assert at[c] not in reach[up[c - 1]] and up[c - 1] not in reach[at[c]]
+
+
+@pytest.mark.parametrize("mode", ["serial", "lanes"])
+@pytest.mark.parametrize("C", [2, 3, 5, 10])
+def test_serial_and_lanes_plans_allow_slot_reuse(lib, mode, C):
+    check_slot_reuse(hcms.plan(C, getattr(hcms, "MODE_" + mode.upper())), C)
+
+
+@pytest.mark.parametrize("mode", ["pipelined", "inline"])
+def test_pipelined_and_inline_plans_do_not_allow_slot_reuse(lib, mode):
+    with pytest.raises(AssertionError):
+        check_slot_reuse(hcms.plan(5, getattr(hcms, "MODE_" + mode.upper())), 5)
+
+
+def test_forward_slots_validation(lib):
+    sizes = (ctypes.c_int * 3)(3, 3, 2)
+
+    def call(slot_heads=3, mode=hcms.MODE_SLOTS):
+        return lib.hcms_forward_slots(None, A, B, C_, D_, A + 2**24, B + 2**24, C_ + 2**24,
+                                      D_ + 2**24, slot_heads, 8, 4096, 8, 128, 0.088, sizes, 3, 0,
+                                      mode, None, None, None)
+
+    assert call(slot_heads=0) == ECHUNKS
+    assert call() == ENULL          # no context (checked after slot_heads)

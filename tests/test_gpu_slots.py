@@ -1,0 +1,85 @@
+"""hcms_forward with two chunk slots on the GPU, through the C ABI: the
+output is bit-identical to the full-workspace forward in every allowed mode
+and chunking, and the slot reuse is ordered even when a stream is delayed."""
+import pytest
+import torch
+
+from paper_2607_01817_amd import inputs
+from tests.gpu_util import bits, log, workload_inputs
+from tests.test_gpu_parity import _delay, _fill_bits
+
+pytestmark = pytest.mark.gpu
+
+SLOT_MODES = ("serial", "lanes", "slots", "auto")
+
+
+def _mode(hcms, name):
+    return getattr(hcms, "MODE_" + name.upper())
+
+
+@pytest.mark.parametrize("name", ["small", "wan_p8"])
+def test_forward_slots_bitwise_equals_full_workspaces(hcms, name):
+    w = inputs.WORKLOADS[name]
+    q, k, v = (x.cuda() for x in workload_inputs(name))
+    ctx = hcms.Context(max_chunks=16)
+    ref = bits(ctx.forward(q, k, v, w.P, w.scale, (w.H,), mode=hcms.MODE_SERIAL).cpu())
+    chunkings = w.chunkings if name == "small" else ((2, 2, 1), (1, 1, 1, 1, 1))
+    for sizes in chunkings:
+        for m in SLOT_MODES if name == "small" else ("slots", "auto"):
+            log(f"[slots] {name} chunks={sizes} mode={m}")
+            out = ctx.forward_slots(q, k, v, w.P, w.scale, sizes, mode=_mode(hcms, m))
+            torch.cuda.synchronize()
+            assert torch.equal(bits(out.cpu()), ref), (sizes, m)
+        # the slots plan on full workspaces too
+        out = ctx.forward(q, k, v, w.P, w.scale, sizes, mode=hcms.MODE_SLOTS)
+        torch.cuda.synchronize()
+        assert torch.equal(bits(out.cpu()), ref), (sizes, "slots plan, full workspaces")
+    ctx.close()
+
+
+def test_forward_slots_rejects_modes_that_break_slot_reuse(hcms):
+    w = inputs.WORKLOADS["small"]
+    q, k, v = (x.cuda() for x in workload_inputs("small"))
+    ctx = hcms.Context(max_chunks=8)
+    for m in (hcms.MODE_PIPELINED, hcms.MODE_INLINE):
+        with pytest.raises(hcms.HcmsError):
+            ctx.forward_slots(q, k, v, w.P, w.scale, (3, 3, 2), mode=m)
+    small = [torch.empty((2, 2, w.S, w.d), dtype=q.dtype, device="cuda") for _ in range(4)]
+    with pytest.raises(hcms.HcmsError):   # a slot of 2 heads cannot hold a chunk of 3
+        ctx.forward_slots(q, k, v, w.P, w.scale, (3, 3, 2), slots=small)
+    torch.cuda.synchronize()
+    ctx.close()
+
+
+@pytest.mark.parametrize("mode", ["slots", "lanes"])
+@pytest.mark.parametrize("late", ["copy", "compute", "main"])
+def test_forward_slots_respects_slot_reuse_under_delay(hcms, late, mode):
+    """Poison the slots and the output, delay one stream with a bounded spin
+    kernel, and read the output on the main stream right after the call.  A
+    missing wait (including the slot-reuse orderings pack c+2 after attention
+    c and attention c+2 after unpack c) would corrupt the output."""
+    w = inputs.WORKLOADS["small"]
+    q, k, v = (x.cuda() for x in workload_inputs("small"))
+    ctx = hcms.Context(max_chunks=8)
+    sizes = (2, 2, 2, 2)
+    ref = ctx.forward(q, k, v, w.P, w.scale, sizes, mode=hcms.MODE_SERIAL).clone()
+    torch.cuda.synchronize()
+    slots = ctx.slot_workspaces(w.S, 2, w.d, q.dtype)
+    out = torch.empty_like(q)
+    for t in (*slots, out):
+        _fill_bits(t)
+    q_in = q
+    if late == "main":
+        q_in = torch.empty_like(q)
+        _fill_bits(q_in)
+        torch.cuda.synchronize()
+        _delay(torch.cuda.current_stream())
+        q_in.copy_(q)
+    else:
+        torch.cuda.synchronize()
+        _delay(ctx.copy_stream if late == "copy" else ctx.compute_stream)
+    ctx.forward_slots(q_in, k, v, w.P, w.scale, sizes, mode=_mode(hcms, mode), out=out, slots=slots)
+    seen = out.clone()
+    torch.cuda.synchronize()
+    assert torch.equal(bits(seen), bits(ref)), (late, mode)
+    ctx.close()
