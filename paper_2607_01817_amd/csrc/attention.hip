@@ -14,10 +14,13 @@
 //     exactly one workgroup per CU, so a workgroup dispatched while other
 //     kernels occupy part of the GPU can never be queued behind two running
 //     ones on the same CU, and every staged K/V block feeds 256 queries;
-//   * K and V blocks are staged in LDS by all threads (global -> registers ->
-//     LDS), K one block ahead of V, each double-buffered.  With bf16 storage
-//     two register sets alternate, so each block's global loads are issued a
-//     whole step before its LDS stores and their latency is hidden;
+//   * K and V blocks are staged in LDS by all threads, K one block ahead of
+//     V.  With d = 128 and bf16 storage (attention_dma_kernel) the blocks go
+//     from global memory straight into LDS, three steps ahead of their use,
+//     through four LDS buffers per tensor.  Otherwise they pass through
+//     registers (global -> registers -> LDS) into double buffers; with bf16
+//     storage two register sets alternate, so each block's global loads are
+//     issued a whole step before its LDS stores;
 //   * scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: keys are the M dimension and queries the N
 //     dimension.  In the accumulator layout each lane then holds one query
@@ -446,10 +449,358 @@ __global__ __launch_bounds__(64 * WAVES, PER_CU * WAVES / 4) void attention_kern
     }
 }
 
+// ---------------------------------------------------------------------------
+// d = 128 with bf16 storage: K and V blocks go from global memory straight
+// into LDS (buffer_load_dwordx4 ... lds), several blocks ahead of their use,
+// without passing through registers.
+//
+// LDS holds kNB buffers of K blocks and kNB of V blocks, each 64 keys x 256
+// bytes row-major.  One DMA instruction of a wave writes 1 KiB of LDS
+// contiguously (lane l at byte 16 l), i.e. four key rows; every lane chooses
+// which 16-byte chunk of its row it fetches, so the chunks are stored
+// XOR-swizzled:
+//   K: chunk c of row r at position c ^ (r & 15), so the 16-byte score operand
+//      reads of 16 consecutive rows hit 16 different groups of 4 banks;
+//   V: chunk c of row r at position c ^ 4 (r & 3), so the transposing reads
+//      below (4 rows x 64 bytes per 32 lanes) hit 16 different groups.
+// The V^T operand of O^T += V^T P^T (lane (li, g) needs V[key][32 dt + li] for
+// the keys 4g + {0..3} and 8 + 4g + {0..3} of a 16-key group, the order in
+// which the score accumulator rows arrive) comes from two ds_read_b64_tr_b16.
+// Within each group of 16 lanes that instruction hands lane t element t mod 4
+// of the 8 bytes read by lanes 4r + t / 4, r = 0..3.  So lane 4r + q of the
+// group reads row key_base + r at columns d_base + 4q .. 4q + 3, and lane t
+// receives column d_base + t of the four rows.
+// The compiler does not see these loads (inline asm; with the intrinsic it
+// would wait for all of them before every LDS read).  The key loop issues no
+// other vector memory instruction, and the kernel waits for its loads itself
+// (s_waitcnt vmcnt) before each step's barrier.  The operand values and the
+// MFMA order are those of attention_kernel, so both give identical results.
+namespace dma {
+
+constexpr int kD = 128;
+constexpr int kWaves = 8;
+constexpr int kRowB = kD * 2;                          // bytes per key row
+constexpr int kTileB = kBC * kRowB;                    // one 64-key block: 16 KiB
+constexpr int kNB = 4;                                 // LDS buffers per tensor
+constexpr int kPerWave = kTileB / (64 * 16) / kWaves;  // DMA instructions per wave and block
+#ifndef HCMS_ATTN_DIST
+#define HCMS_ATTN_DIST 3
+#endif
+// Steps between a block's load and the step that reads it.
+constexpr int kDist = HCMS_ATTN_DIST;
+static_assert(kDist >= 1 && kDist + 1 <= kNB, "more blocks in flight than LDS buffers");
+static_assert(kPerWave == 2, "the wait counts below assume two DMA instructions per block");
+
+// One wave's 1 KiB of a block: lane l's 16 bytes at `voff` (plus the block
+// offset `soff`, which the buffer range check includes) land at LDS byte
+// lds_addr + 16 l.  Out-of-range reads land as zeros.
+// M0 is written here and read by nothing else in the kernel.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ inline void load_lds(unsigned lds_addr, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(lds_addr), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N of this wave's vector memory instructions are pending.
+template <int N>
+__device__ inline void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+// Score operands: S^T[i & 1] += K rows 32 (i & 1) + li, chunk 2 (i >> 1) + g,
+// times Q^T; `k_rd[i >> 1]` is the lane's byte offset of its row and chunk.
+__device__ inline void qk(f32x16 (&sacc)[2], const char *kb, const unsigned (&k_rd)[kD / 16],
+                          const bf16x8 (&qreg)[kD / 16]) {
+    constexpr int N = 2 * (kD / 16);
+    constexpr int AHEAD = 4;
+    auto rd = [&](int n) {
+        return *reinterpret_cast<const bf16x8 *>(kb + k_rd[n >> 1] + (n & 1) * 32 * kRowB);
+    };
+    bf16x8 a[N];
+#pragma unroll
+    for (int i = 0; i < AHEAD; ++i) a[i] = rd(i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        if (i + AHEAD < N) a[i + AHEAD] = rd(i + AHEAD);
+        sacc[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], qreg[i >> 1],
+                                                              i < 2 ? f32x16{} : sacc[i & 1], 0, 0, 0);
+    }
+}
+
+// V^T operand i = (ks, dt) = (i / 4, i % 4): keys 16 ks + 4g + {0..3} and
+// 16 ks + 8 + 4g + {0..3} of column 32 dt + li.
+__device__ inline bf16x8 vt(const char *vb, const unsigned (&v_rd)[kD / 32], int i) {
+    typedef __attribute__((address_space(3))) bf16x4 LdsV4;
+    const char *p = vb + v_rd[i % (kD / 32)] + (i / (kD / 32)) * 16 * kRowB;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p + 8 * kRowB));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+__device__ inline void pv_prefetch(bf16x8 (&pre)[kPvAhead], const char *vb, const unsigned (&v_rd)[kD / 32]) {
+#pragma unroll
+    for (int i = 0; i < kPvAhead; ++i) pre[i] = vt(vb, v_rd, i);
+}
+
+// O^T[i % 4] += V^T operand i times P^T[i / 4], in the order of pv_mfma.
+__device__ inline void pv(f32x16 (&oacc)[kD / 32], const bf16x8 (&pb)[4], const char *vb,
+                          const unsigned (&v_rd)[kD / 32], const bf16x8 (&pre)[kPvAhead]) {
+    constexpr int DT = kD / 32, N = 4 * DT;
+    bf16x8 a[N];
+#pragma unroll
+    for (int i = 0; i < kPvAhead; ++i) a[i] = pre[i];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        if (i + kPvAhead < N) a[i + kPvAhead] = vt(vb, v_rd, i + kPvAhead);
+        oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], pb[i / DT], oacc[i % DT], 0, 0, 0);
+    }
+}
+
+// Scheduling hints, as interleave_qk_exp and interleave_pv_stage; a V operand
+// takes two LDS reads and there are no LDS stores.
+__device__ inline void interleave_qk() {
+    constexpr int N = 2 * (kD / 16), AHEAD = 4;
+    __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);  // DS read
+    __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);     // VALU
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
+        if (i + AHEAD < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPvAhead, 0);  // V operand prefetch
+}
+
+__device__ inline void interleave_pv() {
+    constexpr int N = 4 * (kD / 32);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
+        if (i + kPvAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS read
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);                           // VALU
+    }
+}
+
+template <int P>
+struct Phase {
+    static constexpr int value = P;
+};
+
+}  // namespace dma
+
+__global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_dma_kernel(
+    const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
+    __bf16 *__restrict__ o, float *__restrict__ lse, int S, int n_qtiles, float c) {
+    using namespace dma;
+    constexpr int D = kD, KK = D / 16, DT = D / 32;
+    __shared__ __attribute__((aligned(1024))) char lds[2 * kNB * kTileB];
+    const char *const kbase = lds;                  // K buffer b at kbase + b * kTileB
+    const char *const vbase = lds + kNB * kTileB;   // V buffer b at vbase + b * kTileB
+
+    // XCD-aware tile order, as in attention_kernel.
+    const int nb = gridDim.x, b = blockIdx.x;
+    const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
+    const int logical = xcd * per + min(xcd, rem) + (b >> 3);
+    const int head = logical / n_qtiles;
+    const int qtile = logical - head * n_qtiles;
+
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * 2;
+    const __amdgpu_buffer_rsrc_t qr = head_rsrc(q + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t vr = head_rsrc(v + hoff, hbytes);
+    __bf16 *oh = o + hoff;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 31;
+    const int g = lane >> 5;
+    const int q0 = (qtile * kWaves + wave) * kQW;
+
+    bf16x8 qreg[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        qreg[kk] = __builtin_bit_cast(
+            bf16x8, load8<__bf16>(qr, static_cast<unsigned>((q0 + li) * D + kk * 16 + g * 8) * 2));
+
+    // Lane offsets: DMA sources (row r = 4 (2 wave + i) + lane / 16 of the
+    // block, chunk at position lane % 16), score operand reads and transposing
+    // V reads (lane t = lane % 16 of group G = lane / 16).
+    unsigned k_src[kPerWave], v_src[kPerWave];
+#pragma unroll
+    for (int i = 0; i < kPerWave; ++i) {
+        const unsigned r = 4 * (kPerWave * wave + i) + (lane >> 4), p = lane & 15;
+        k_src[i] = r * kRowB + ((p ^ (r & 15)) << 4);
+        v_src[i] = r * kRowB + ((p ^ ((r & 3) << 2)) << 4);
+    }
+    unsigned k_rd[KK];
+#pragma unroll
+    for (int qq = 0; qq < KK; ++qq) k_rd[qq] = li * kRowB + (((2 * qq + g) ^ (li & 15)) << 4);
+    unsigned v_rd[DT];
+    {
+        const unsigned G = lane >> 4, t = lane & 15;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+            v_rd[dt] = (4 * (G >> 1) + (t >> 2)) * kRowB +
+                       ((((dt ^ (t >> 2)) << 2) + 2 * (G & 1) + ((t >> 1) & 1)) << 4) + ((t & 1) << 3);
+    }
+    // Opaque to the compiler: with the offsets' known bits it turns base +
+    // constant into an OR, which the transposing read's immediate offset does
+    // not take.
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(v_rd[dt]));
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<uintptr_t>(lds));
+    const unsigned wave_dst = lds0 + kPerWave * wave * 1024;
+    auto issue_k = [&](int blk) {
+        const unsigned dst = wave_dst + (blk & (kNB - 1)) * kTileB;
+#pragma unroll
+        for (int i = 0; i < kPerWave; ++i) load_lds(dst + i * 1024, kr, k_src[i], blk * kTileB);
+    };
+    auto issue_v = [&](int blk) {
+        const unsigned dst = wave_dst + (kNB + (blk & (kNB - 1))) * kTileB;
+#pragma unroll
+        for (int i = 0; i < kPerWave; ++i) load_lds(dst + i * 1024, vr, v_src[i], blk * kTileB);
+    };
+
+    f32x16 oacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+    const int nkb = (S + kBC - 1) / kBC;
+
+    // Prologue: K_0, V_0, ..., K_{kDist-1}, V_{kDist-1}, K_kDist in flight;
+    // step j then issues K_{j+1+kDist} and V_{j+kDist} (blocks past the end
+    // read as zeros and are never used).
+#pragma unroll
+    for (int blk = 0; blk <= kDist; ++blk) {
+        issue_k(blk);
+        if (blk < kDist) issue_v(blk);
+    }
+    wait_vm<4 * kDist>();  // K_0 landed
+    __syncthreads();
+    f32x16 sa[2], sb[2];
+    qk(sa, kbase, k_rd, qreg);
+    wait_vm<4 * kDist - 4>();  // V_0 and K_1 landed
+    __syncthreads();           // and every wave is done with K_0's buffer
+
+    // Block 0 sets the running maximum; the lazy rescaling is that of
+    // attention_kernel.
+    float m, mc, lsum;
+    bf16x8 pb[4];
+    if (nkb == 1) mask_block(sa, g, S);
+    m = block_max(sa);
+    mc = m * c;
+    lsum = exp_block(sa, c, mc, pb);
+
+    bf16x8 vpre[kPvAhead];
+    auto softmax = [&](const f32x16(&s)[2], const char *vb) {
+        float bsum = exp_block(s, c, mc, pb);
+        pv_prefetch(vpre, vb, v_rd);
+        interleave_qk();
+        const bool up = halves_sum(bsum) > kRaiseBound;
+        if (__any(up)) {
+            const float mx = block_max(s);
+            const float m_new = up ? mx : m;
+            const float alpha = up ? __builtin_amdgcn_exp2f((m - mx) * c) : 1.0f;
+            m = m_new;
+            mc = m_new * c;
+            bsum = exp_block(s, c, mc, pb);
+            lsum *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+        }
+        lsum += bsum;
+    };
+
+    if (nkb > 1) {
+        // Block 0's PV and block 1's scores.
+        issue_k(1 + kDist);
+        issue_v(kDist);
+        qk(sb, kbase + 1 * kTileB, k_rd, qreg);
+        pv_prefetch(vpre, vbase, v_rd);
+        pv(oacc, pb, vbase, v_rd, vpre);
+        wait_vm<4 * (kDist - 1)>();
+        __syncthreads();
+    }
+
+    // Step j: K_{j+1} is in buffer (j + 1) % kNB, V_j in buffer j % kNB.
+    auto step = [&](int j, auto ph, f32x16(&scur)[2], f32x16(&snext)[2]) {
+        constexpr int P = decltype(ph)::value;
+        issue_k(j + 1 + kDist);
+        issue_v(j + kDist);
+        qk(snext, kbase + ((P + 1) % kNB) * kTileB, k_rd, qreg);
+        softmax(scur, vbase + P * kTileB);
+        pv(oacc, pb, vbase + P * kTileB, v_rd, vpre);
+        interleave_pv();
+        wait_vm<4 * (kDist - 1)>();  // K_{j+2} and V_{j+1} landed
+        __syncthreads();
+    };
+    int j = 1;
+    if (nkb > 1) {
+        for (; j + 4 < nkb; j += 4) {
+            step(j, Phase<1>{}, sb, sa);
+            step(j + 1, Phase<2>{}, sa, sb);
+            step(j + 2, Phase<3>{}, sb, sa);
+            step(j + 3, Phase<0>{}, sa, sb);
+        }
+        if (j + 1 < nkb) {
+            step(j, Phase<1>{}, sb, sa);
+            ++j;
+            if (j + 1 < nkb) {
+                step(j, Phase<2>{}, sa, sb);
+                ++j;
+                if (j + 1 < nkb) {
+                    step(j, Phase<3>{}, sb, sa);
+                    ++j;
+                }
+            }
+        }
+        // Last block (j = nkb - 1): its scores are in sa when j is even.
+        if ((j & 1) == 0) {
+            sb[0] = sa[0];
+            sb[1] = sa[1];
+        }
+        mask_block(sb, g, S - j * kBC);
+        softmax(sb, vbase + (j % kNB) * kTileB);
+        pv(oacc, pb, vbase + (j % kNB) * kTileB, v_rd, vpre);
+    } else {
+        pv_prefetch(vpre, vbase, v_rd);
+        pv(oacc, pb, vbase, v_rd, vpre);
+    }
+    wait_vm<0>();  // no load into LDS is pending when the workgroup ends
+
+    const int qi = q0 + li;
+    const float l = halves_sum(lsum);
+    const float inv = 1.0f / l;
+    if (lse != nullptr && g == 0 && qi < S)
+        lse[static_cast<int64_t>(head) * S + qi] = mc + __builtin_amdgcn_logf(l);
+    if (qi < S) {
+        __bf16 *orow = oh + static_cast<int64_t>(qi) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 x = {oacc[dt][rb * 4 + 0] * inv, oacc[dt][rb * 4 + 1] * inv,
+                                 oacc[dt][rb * 4 + 2] * inv, oacc[dt][rb * 4 + 3] * inv};
+                store4(orow + dt * 32 + rb * 8 + g * 4, x);
+            }
+    }
+}
+
 // Launch shape per head dimension: WAVES waves per workgroup, NT tiles of 32
 // queries per wave, 256 queries per workgroup.  d = 128: four waves of 64
 // queries, one wave per SIMD (every K and V operand read from LDS feeds two
 // MFMAs); d = 64: four waves of 32 queries, two workgroups per CU.
+#ifndef HCMS_ATTN_LDS_DMA
+#define HCMS_ATTN_LDS_DMA 1
+#endif
+// d = 128 with bf16 storage runs attention_dma_kernel.
+constexpr bool kLdsDma = HCMS_ATTN_LDS_DMA != 0;
+
 template <int D>
 struct Shape {
     static constexpr int NT = D == 128 ? HCMS_ATTN_NT128 : 1;
@@ -465,9 +816,16 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, fl
     const int n_qtiles = (S + Sh::BR - 1) / Sh::BR;
     const int64_t blocks = static_cast<int64_t>(n_qtiles) * n_heads;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    attention_kernel<D, T, Sh::WAVES, Sh::NT, Sh::PER_CU><<<static_cast<unsigned>(blocks), 64 * Sh::WAVES, 0, stream>>>(
-        static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
-        static_cast<T *>(o), lse, S, n_qtiles, c);
+    if constexpr (D == dma::kD && sizeof(T) == 2 && kLdsDma) {
+        static_assert(Sh::NT == 1 && Sh::WAVES == dma::kWaves, "the DMA kernel covers 256 queries in 8 waves");
+        attention_dma_kernel<<<static_cast<unsigned>(blocks), 64 * dma::kWaves, 0, stream>>>(
+            static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
+            static_cast<__bf16 *>(o), lse, S, n_qtiles, c);
+    } else {
+        attention_kernel<D, T, Sh::WAVES, Sh::NT, Sh::PER_CU><<<static_cast<unsigned>(blocks), 64 * Sh::WAVES, 0, stream>>>(
+            static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
+            static_cast<T *>(o), lse, S, n_qtiles, c);
+    }
     return hipGetLastError();
 }
 
