@@ -246,6 +246,29 @@ __device__ inline float exp_block(const f32x16 (&s)[2], float c, float mc, bf16x
     return sum;
 }
 
+// The exponentials of one 32-key tile mt of a block (exp_block's pb[2 mt] and
+// pb[2 mt + 1]) in p0 and p1, continuing the row sum `sum` in exp_block's
+// order: exp_half of tile 0 from 0, then of tile 1 from that sum, gives
+// exp_block's values and sum bit for bit.
+__device__ inline float exp_half(const f32x16 &s, float c, float mc, bf16x8 &p0, bf16x8 &p1,
+                                 float sum) {
+    const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        f32x8 p;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[h * 8 + r], c, -mc));
+        const bf16x8 pbf = __builtin_convertvector(p, bf16x8);
+        (h == 0 ? p0 : p1) = pbf;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const bf16x2 pair = {pbf[2 * r], pbf[2 * r + 1]};
+            sum = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, sum, false);
+        }
+    }
+    return sum;
+}
+
 template <int D, typename T, int WAVES, int NT, int PER_CU>
 __global__ __launch_bounds__(64 * WAVES, PER_CU * WAVES / 4) void attention_kernel(
     const T *__restrict__ q, const T *__restrict__ k, const T *__restrict__ v, T *__restrict__ o,
@@ -511,10 +534,19 @@ __device__ inline void wait_vm() {
 
 // Score operands: S^T[i & 1] += K rows 32 (i & 1) + li, chunk 2 (i >> 1) + g,
 // times Q^T; `k_rd[i >> 1]` is the lane's byte offset of its row and chunk.
+#ifndef HCMS_ATTN_KAHEAD
+#define HCMS_ATTN_KAHEAD 4
+#endif
+#ifndef HCMS_ATTN_VAHEAD
+#define HCMS_ATTN_VAHEAD 2
+#endif
+constexpr int kKAhead = HCMS_ATTN_KAHEAD;  // score operand reads in flight
+constexpr int kVAhead = HCMS_ATTN_VAHEAD;  // V^T operands read ahead of their MFMA
+
 __device__ inline void qk(f32x16 (&sacc)[2], const char *kb, const unsigned (&k_rd)[kD / 16],
                           const bf16x8 (&qreg)[kD / 16]) {
     constexpr int N = 2 * (kD / 16);
-    constexpr int AHEAD = 4;
+    constexpr int AHEAD = kKAhead;
     auto rd = [&](int n) {
         return *reinterpret_cast<const bf16x8 *>(kb + k_rd[n >> 1] + (n & 1) * 32 * kRowB);
     };
@@ -539,47 +571,52 @@ __device__ inline bf16x8 vt(const char *vb, const unsigned (&v_rd)[kD / 32], int
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
-__device__ inline void pv_prefetch(bf16x8 (&pre)[kPvAhead], const char *vb, const unsigned (&v_rd)[kD / 32]) {
+__device__ inline void pv_prefetch(bf16x8 (&pre)[kVAhead], const char *vb, const unsigned (&v_rd)[kD / 32]) {
 #pragma unroll
-    for (int i = 0; i < kPvAhead; ++i) pre[i] = vt(vb, v_rd, i);
+    for (int i = 0; i < kVAhead; ++i) pre[i] = vt(vb, v_rd, i);
 }
 
-// O^T[i % 4] += V^T operand i times P^T[i / 4], in the order of pv_mfma.
-__device__ inline void pv(f32x16 (&oacc)[kD / 32], const bf16x8 (&pb)[4], const char *vb,
-                          const unsigned (&v_rd)[kD / 32], const bf16x8 (&pre)[kPvAhead]) {
+// O^T[i % 4] += V^T operand i times P^T[i / 4], in the order of pv_mfma; P^T
+// comes as its keys 0-31 (lo) and 32-63 (hi).
+__device__ inline void pv(f32x16 (&oacc)[kD / 32], const bf16x8 (&lo)[2], const bf16x8 (&hi)[2],
+                          const char *vb, const unsigned (&v_rd)[kD / 32], const bf16x8 (&pre)[kVAhead]) {
     constexpr int DT = kD / 32, N = 4 * DT;
     bf16x8 a[N];
 #pragma unroll
-    for (int i = 0; i < kPvAhead; ++i) a[i] = pre[i];
+    for (int i = 0; i < kVAhead; ++i) a[i] = pre[i];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        if (i + kPvAhead < N) a[i + kPvAhead] = vt(vb, v_rd, i + kPvAhead);
-        oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], pb[i / DT], oacc[i % DT], 0, 0, 0);
+        if (i + kVAhead < N) a[i + kVAhead] = vt(vb, v_rd, i + kVAhead);
+        const int ks = i / DT;
+        oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], ks < 2 ? lo[ks] : hi[ks - 2],
+                                                               oacc[i % DT], 0, 0, 0);
     }
 }
 
-// Scheduling hints, as interleave_qk_exp and interleave_pv_stage; a V operand
-// takes two LDS reads and there are no LDS stores.
+// Scheduling hints.  Each phase of a step holds half of the softmax VALU work
+// (the exponentials of 32 keys: FMA, v_exp_f32, conversion, row sum): about
+// three VALU instructions between consecutive MFMAs in both the score phase
+// and the PV phase.  A V operand takes two LDS reads.
 __device__ inline void interleave_qk() {
-    constexpr int N = 2 * (kD / 16), AHEAD = 4;
+    constexpr int N = 2 * (kD / 16), AHEAD = kKAhead;
     __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);  // DS read
-    __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);     // VALU
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);      // VALU
 #pragma unroll
     for (int i = 0; i < N; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
         if (i + AHEAD < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPvAhead, 0);  // V operand prefetch
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kVAhead, 0);  // V operand prefetch
 }
 
 __device__ inline void interleave_pv() {
     constexpr int N = 4 * (kD / 32);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
-        if (i + kPvAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS read
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);                           // VALU
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
+        if (i + kVAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);                        // VALU
     }
 }
 
@@ -686,17 +723,24 @@ __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_d
     __syncthreads();           // and every wave is done with K_0's buffer
 
     // Block 0 sets the running maximum; the lazy rescaling is that of
-    // attention_kernel.
-    float m, mc, lsum;
-    bf16x8 pb[4];
+    // attention_kernel.  The exponentials of block j are split over two
+    // steps: keys 0-31 (tile 0) during the PV of block j - 1, keys 32-63
+    // (tile 1) during the scores of block j + 1, followed by the overflow test
+    // of block j.  So both phases of a step carry half of the VALU work next to
+    // their 16 MFMAs.  lo[j & 1] holds tile 0 of block j's P, hi tile 1; s0 the
+    // row sum over tile 0 (continued by tile 1 in exp_block's order).
+    float m, mc, lsum, s0 = 0.f;
+    bf16x8 lo[2][2], hi[2];
     if (nkb == 1) mask_block(sa, g, S);
     m = block_max(sa);
     mc = m * c;
-    lsum = exp_block(sa, c, mc, pb);
+    lsum = exp_half(sa[1], c, mc, hi[0], hi[1], exp_half(sa[0], c, mc, lo[0][0], lo[0][1], 0.f));
 
-    bf16x8 vpre[kPvAhead];
-    auto softmax = [&](const f32x16(&s)[2], const char *vb) {
-        float bsum = exp_block(s, c, mc, pb);
+    bf16x8 vpre[kVAhead];
+    // Tile 1 of block j (scores s, tile 0 already in lo_j with sum s0), the
+    // overflow test and, when some query needs it, the recompute branch.
+    auto finish = [&](const f32x16(&s)[2], bf16x8(&lo_j)[2], const char *vb) {
+        float bsum = exp_half(s[1], c, mc, hi[0], hi[1], s0);
         pv_prefetch(vpre, vb, v_rd);
         interleave_qk();
         const bool up = halves_sum(bsum) > kRaiseBound;
@@ -706,7 +750,7 @@ __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_d
             const float alpha = up ? __builtin_amdgcn_exp2f((m - mx) * c) : 1.0f;
             m = m_new;
             mc = m_new * c;
-            bsum = exp_block(s, c, mc, pb);
+            bsum = exp_half(s[1], c, mc, hi[0], hi[1], exp_half(s[0], c, mc, lo_j[0], lo_j[1], 0.f));
             lsum *= alpha;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
@@ -715,61 +759,86 @@ __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_d
         }
         lsum += bsum;
     };
-
-    if (nkb > 1) {
-        // Block 0's PV and block 1's scores.
-        issue_k(1 + kDist);
-        issue_v(kDist);
-        qk(sb, kbase + 1 * kTileB, k_rd, qreg);
-        pv_prefetch(vpre, vbase, v_rd);
-        pv(oacc, pb, vbase, v_rd, vpre);
-        wait_vm<4 * (kDist - 1)>();
-        __syncthreads();
-    }
+    // PV of block j beside tile 0 of block j + 1 (scores sn, already masked
+    // when block j + 1 is the last one).
+    auto pv_next = [&](const bf16x8(&lo_j)[2], const char *vb, f32x16(&sn)[2], bf16x8(&lo_n)[2]) {
+        pv(oacc, lo_j, hi, vb, v_rd, vpre);
+        s0 = exp_half(sn[0], c, mc, lo_n[0], lo_n[1], 0.f);
+        interleave_pv();
+    };
 
     // Step j: K_{j+1} is in buffer (j + 1) % kNB, V_j in buffer j % kNB.
-    auto step = [&](int j, auto ph, f32x16(&scur)[2], f32x16(&snext)[2]) {
+    // Block j + 1 is masked when it is the last one; the steady-state steps
+    // (all but the last) never are, so they carry no masking code.
+    auto step = [&](int j, auto ph, auto first, auto last, f32x16(&scur)[2], f32x16(&snext)[2],
+                    bf16x8(&lo_j)[2], bf16x8(&lo_n)[2]) {
+        // P: j % kNB, or -1 when only known at run time (one step per workgroup);
+        // step 0 has no exponentials left to finish (block 0 took them all).
         constexpr int P = decltype(ph)::value;
+        const int kb = P >= 0 ? (P + 1) % kNB : (j + 1) % kNB;
+        const int vb = P >= 0 ? P : j % kNB;
         issue_k(j + 1 + kDist);
         issue_v(j + kDist);
-        qk(snext, kbase + ((P + 1) % kNB) * kTileB, k_rd, qreg);
-        softmax(scur, vbase + P * kTileB);
-        pv(oacc, pb, vbase + P * kTileB, v_rd, vpre);
-        interleave_pv();
+        qk(snext, kbase + kb * kTileB, k_rd, qreg);
+        if constexpr (decltype(first)::value) pv_prefetch(vpre, vbase, v_rd);
+        else finish(scur, lo_j, vbase + vb * kTileB);
+        if constexpr (decltype(last)::value) mask_block(snext, g, S - (j + 1) * kBC);
+        pv_next(lo_j, vbase + vb * kTileB, snext, lo_n);
         wait_vm<4 * (kDist - 1)>();  // K_{j+2} and V_{j+1} landed
         __syncthreads();
     };
-    int j = 1;
+    using Last = std::true_type;
+    using NotLast = std::false_type;
+    using First = std::true_type;
+    using Next = std::false_type;
     if (nkb > 1) {
-        for (; j + 4 < nkb; j += 4) {
-            step(j, Phase<1>{}, sb, sa);
-            step(j + 1, Phase<2>{}, sa, sb);
-            step(j + 2, Phase<3>{}, sb, sa);
-            step(j + 3, Phase<0>{}, sa, sb);
+        // Step 0: block 0's PV and block 1's scores.
+        if (nkb == 2) step(0, Phase<0>{}, First{}, Last{}, sa, sb, lo[0], lo[1]);
+        else step(0, Phase<0>{}, First{}, NotLast{}, sa, sb, lo[0], lo[1]);
+        int j = 1;
+        for (; j + 5 < nkb; j += 4) {
+            step(j, Phase<1>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
+            step(j + 1, Phase<2>{}, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
+            step(j + 2, Phase<3>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
+            step(j + 3, Phase<0>{}, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
         }
-        if (j + 1 < nkb) {
-            step(j, Phase<1>{}, sb, sa);
+        if (j + 2 < nkb) {
+            step(j, Phase<1>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
             ++j;
-            if (j + 1 < nkb) {
-                step(j, Phase<2>{}, sa, sb);
+            if (j + 2 < nkb) {
+                step(j, Phase<2>{}, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
                 ++j;
-                if (j + 1 < nkb) {
-                    step(j, Phase<3>{}, sb, sa);
+                if (j + 2 < nkb) {
+                    step(j, Phase<3>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
                     ++j;
                 }
             }
         }
-        // Last block (j = nkb - 1): its scores are in sa when j is even.
-        if ((j & 1) == 0) {
-            sb[0] = sa[0];
-            sb[1] = sa[1];
+        // Block j's scores and tile 0 are in sa and lo[0] when j is even.
+        auto to_odd = [&]() {
+            if ((j & 1) == 0) {
+                sb[0] = sa[0];
+                sb[1] = sa[1];
+                lo[1][0] = lo[0][0];
+                lo[1][1] = lo[0][1];
+            }
+        };
+        if (nkb > 2) {
+            // The step of the last scores (j = nkb - 2), then the last block
+            // (masked), whose scores and tile 0 it leaves in sa and lo[0].
+            to_odd();
+            step(j, Phase<-1>{}, Next{}, Last{}, sb, sa, lo[1], lo[0]);
+            ++j;
+            finish(sa, lo[0], vbase + (j % kNB) * kTileB);
+            pv(oacc, lo[0], hi, vbase + (j % kNB) * kTileB, v_rd, vpre);
+        } else {
+            // nkb = 2: step 0 left block 1 (masked) in sb and lo[1].
+            finish(sb, lo[1], vbase + kTileB);
+            pv(oacc, lo[1], hi, vbase + kTileB, v_rd, vpre);
         }
-        mask_block(sb, g, S - j * kBC);
-        softmax(sb, vbase + (j % kNB) * kTileB);
-        pv(oacc, pb, vbase + (j % kNB) * kTileB, v_rd, vpre);
     } else {
         pv_prefetch(vpre, vbase, v_rd);
-        pv(oacc, pb, vbase, v_rd, vpre);
+        pv(oacc, lo[0], hi, vbase, v_rd, vpre);
     }
     wait_vm<0>();  // no load into LDS is pending when the workgroup ends
 
