@@ -246,12 +246,31 @@ __device__ inline float exp_block(const f32x16 (&s)[2], float c, float mc, bf16x
     return sum;
 }
 
-// The exponentials of one 32-key tile mt of a block (exp_block's pb[2 mt] and
-// pb[2 mt + 1]) in p0 and p1, continuing the row sum `sum` in exp_block's
-// order: exp_half of tile 0 from 0, then of tile 1 from that sum, gives
-// exp_block's values and sum bit for bit.
+#ifndef HCMS_ATTN_FP32_SUM
+#define HCMS_ATTN_FP32_SUM 0
+#endif
+// The exponentials of one 32-key tile of a block (exp_block's pb[2 mt] and
+// pb[2 mt + 1] for tile mt) in p0 and p1; returns sum plus this lane's sum of
+// the tile's 16 weights.  That sum adds the fp32 weights before their
+// rounding to bf16, in a fixed order with v_add_f32: unlike
+// v_dot2c_f32_bf16, which does not issue while the matrix core is busy, an
+// add issues beside the MFMAs.  l is then the sum of the unrounded weights
+// while V is multiplied by their bf16 roundings, a relative difference below
+// 2^-9 that averages out over the keys.
 __device__ inline float exp_half(const f32x16 &s, float c, float mc, bf16x8 &p0, bf16x8 &p1,
                                  float sum) {
+#if HCMS_ATTN_FP32_SUM
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        f32x8 p;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[h * 8 + r], c, -mc));
+        (h == 0 ? p0 : p1) = __builtin_convertvector(p, bf16x8);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) sum += p[r];
+    }
+    return sum;
+#else
     const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -267,6 +286,7 @@ __device__ inline float exp_half(const f32x16 &s, float c, float mc, bf16x8 &p0,
         }
     }
     return sum;
+#endif
 }
 
 template <int D, typename T, int WAVES, int NT, int PER_CU>
@@ -823,19 +843,20 @@ __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_d
                 lo[1][1] = lo[0][1];
             }
         };
-        if (nkb > 2) {
-            // The step of the last scores (j = nkb - 2), then the last block
-            // (masked), whose scores and tile 0 it leaves in sa and lo[0].
+        if (j + 1 < nkb) {
+            // The step of the last scores (j = nkb - 2); it leaves the last
+            // block's scores and tile 0 in sa and lo[0].
             to_odd();
             step(j, Phase<-1>{}, Next{}, Last{}, sb, sa, lo[1], lo[0]);
             ++j;
-            finish(sa, lo[0], vbase + (j % kNB) * kTileB);
-            pv(oacc, lo[0], hi, vbase + (j % kNB) * kTileB, v_rd, vpre);
-        } else {
-            // nkb = 2: step 0 left block 1 (masked) in sb and lo[1].
-            finish(sb, lo[1], vbase + kTileB);
-            pv(oacc, lo[1], hi, vbase + kTileB, v_rd, vpre);
+            sb[0] = sa[0];
+            sb[1] = sa[1];
+            lo[1][0] = lo[0][0];
+            lo[1][1] = lo[0][1];
         }
+        // Last block (j = nkb - 1, masked) in sb and lo[1].
+        finish(sb, lo[1], vbase + (j % kNB) * kTileB);
+        pv(oacc, lo[1], hi, vbase + (j % kNB) * kTileB, v_rd, vpre);
     } else {
         pv_prefetch(vpre, vbase, v_rd);
         pv(oacc, lo[0], hi, vbase, v_rd, vpre);
