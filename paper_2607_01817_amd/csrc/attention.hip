@@ -246,8 +246,10 @@ __device__ inline float exp_block(const f32x16 (&s)[2], float c, float mc, bf16x
     return sum;
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
 #ifndef HCMS_ATTN_FP32_SUM
-#define HCMS_ATTN_FP32_SUM 0
+#define HCMS_ATTN_FP32_SUM 1
 #endif
 // The exponentials of one 32-key tile of a block (exp_block's pb[2 mt] and
 // pb[2 mt + 1] for tile mt) in p0 and p1; returns sum plus this lane's sum of
@@ -262,12 +264,17 @@ __device__ inline float exp_half(const f32x16 &s, float c, float mc, bf16x8 &p0,
 #if HCMS_ATTN_FP32_SUM
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        f32x8 p;
+        bf16x8 pbf;
 #pragma unroll
-        for (int r = 0; r < 8; ++r) p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[h * 8 + r], c, -mc));
-        (h == 0 ? p0 : p1) = __builtin_convertvector(p, bf16x8);
-#pragma unroll
-        for (int r = 0; r < 8; ++r) sum += p[r];
+        for (int r = 0; r < 8; r += 2) {
+            const float a = __builtin_amdgcn_exp2f(__builtin_fmaf(s[h * 8 + r], c, -mc));
+            const float b = __builtin_amdgcn_exp2f(__builtin_fmaf(s[h * 8 + r + 1], c, -mc));
+            const bf16x2 ab = __builtin_convertvector((f32x2){a, b}, bf16x2);
+            pbf[r] = ab[0];
+            pbf[r + 1] = ab[1];
+            sum += a + b;
+        }
+        (h == 0 ? p0 : p1) = pbf;
     }
     return sum;
 #else
