@@ -465,7 +465,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
             "traffic": measured_traffic(w.name, sizes),
-            "kernel": "attention_kernel<128, bf16>",
+            "kernel": "attention_dma_kernel (d = 128, bf16)",
             "per_launch": f"4*S^2*H_c*d FLOP per chunk launch; avg launch {avg_attn_ms:.4f} ms "
                           f"over {len(attn_ms)} launches, events on the launching stream, in "
                           f"a second pass of the {args.steps} steps "

@@ -33,7 +33,8 @@
 //     swapped) to match the order in which the accumulator rows arrive;
 //   * software pipeline: while the VALU computes the exponentials of block j,
 //     the MFMA unit already computes the scores of block j + 1 (no dependency
-//     between the two), then O^T += V_j^T P_j^T.  K operands are read from
+//     between the two), then O^T += V_j^T P_j^T (attention_dma_kernel splits
+//     each block's exponentials over both halves of a step).  K operands are read from
 //     LDS four MFMAs ahead and V operands two (the first two before the
 //     overflow test below); scheduling hints spread the exponentials between the score
 //     MFMAs and the next blocks' LDS stores between the PV MFMAs.  The loop is
@@ -47,10 +48,11 @@
 //     rescaled.  So the common path computes no maximum at all, every
 //     exponential used is at most 2^8 (bf16 and fp32 hold it exactly in
 //     range), and the final O / l is unchanged;
-//   * P is rounded to bf16 (nearest-even, v_cvt_pk_bf16_f32) for the PV MFMA;
-//     the row sum l adds exactly these rounded values (v_dot2c_f32_bf16 with a
-//     (1, 1) pair), so the weights that multiply V are normalised exactly; all
-//     accumulation (scores, O, l) is fp32;
+//   * P is rounded to bf16 (nearest-even, v_cvt_pk_bf16_f32) for the PV MFMA.
+//     attention_kernel's row sum l adds exactly these rounded values
+//     (v_dot2c_f32_bf16 with a (1, 1) pair); attention_dma_kernel's adds the
+//     fp32 weights before rounding (v_add_f32, which issues beside the
+//     MFMAs).  All accumulation (scores, O, l) is fp32;
 //   * the grid is remapped so that the 8 XCDs each take a contiguous range of
 //     (head, query tile) pairs, so concurrent workgroups of an XCD stream the
 //     same K/V blocks through that XCD's L2.
@@ -524,7 +526,7 @@ __global__ __launch_bounds__(64 * WAVES, PER_CU * WAVES / 4) void attention_kern
 // would wait for all of them before every LDS read).  The key loop issues no
 // other vector memory instruction, and the kernel waits for its loads itself
 // (s_waitcnt vmcnt) before each step's barrier.  The operand values and the
-// MFMA order are those of attention_kernel, so both give identical results.
+// MFMA order are those of attention_kernel; the row sum differs (exp_half).
 namespace dma {
 
 constexpr int kD = 128;
