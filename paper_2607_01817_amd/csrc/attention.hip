@@ -623,17 +623,29 @@ __device__ inline void pv(f32x16 (&oacc)[kD / 32], const bf16x8 (&lo)[2], const 
 }
 
 // Scheduling hints.  Each phase of a step holds half of the softmax VALU work
-// (the exponentials of 32 keys: FMA, v_exp_f32, conversion, row sum): about
-// three VALU instructions between consecutive MFMAs in both the score phase
-// and the PV phase.  A V operand takes two LDS reads.
+// (the exponentials of 32 keys: FMA, v_exp_f32, conversion, row sum), about
+// three VALU instructions per MFMA.  The hints pin two of them after each
+// score MFMA and each PV MFMA and leave the rest to the scheduler, which
+// measured faster than pinning all three.  A V operand takes two LDS reads.
+#ifndef HCMS_ATTN_QK_VALU
+#define HCMS_ATTN_QK_VALU 2
+#endif
+#ifndef HCMS_ATTN_PV_VALU
+#define HCMS_ATTN_PV_VALU 2
+#endif
+#ifndef HCMS_ATTN_QK_VALU0
+#define HCMS_ATTN_QK_VALU0 4
+#endif
+constexpr int kQkValu = HCMS_ATTN_QK_VALU;   // VALU instructions after each score MFMA
+constexpr int kPvValu = HCMS_ATTN_PV_VALU;   // VALU instructions after each PV MFMA
 __device__ inline void interleave_qk() {
     constexpr int N = 2 * (kD / 16), AHEAD = kKAhead;
     __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);  // DS read
-    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);      // VALU
+    __builtin_amdgcn_sched_group_barrier(0x002, HCMS_ATTN_QK_VALU0, 0);  // VALU
 #pragma unroll
     for (int i = 0; i < N; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
+        __builtin_amdgcn_sched_group_barrier(0x002, kQkValu, 0);  // VALU
         if (i + AHEAD < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * kVAhead, 0);  // V operand prefetch
@@ -645,7 +657,7 @@ __device__ inline void interleave_pv() {
     for (int i = 0; i < N; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
         if (i + kVAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);                        // VALU
+        __builtin_amdgcn_sched_group_barrier(0x002, kPvValu, 0);                  // VALU
     }
 }
 
