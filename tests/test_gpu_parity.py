@@ -158,6 +158,30 @@ def test_attention_ragged_shapes(hcms, oracle_mod, S, H, d, dtype):
         assert torch.equal(torch.from_numpy(out).to(dtype), v)
 
 
+@pytest.mark.parametrize("nkb", range(1, 14))
+@pytest.mark.parametrize("tail", [0, 7])
+def test_attention_every_key_block_count(hcms, oracle_mod, nkb, tail):
+    """d = 128, bf16: the key loop is unrolled by four after its first step,
+    with up to three more steps, a peeled step for the last scores (which
+    masks the last block) and the last block, so each count of 64-key blocks
+    from 1 to 13 takes a different path.  Odd counts use logits of std 16,
+    which take the recompute branch in those last steps as well."""
+    S, H, d = 64 * nkb - tail, 2, 128
+    if S < 1:
+        pytest.skip("no keys")
+    sigma = 4.0 if nkb % 2 else 0.5
+    log(f"[key blocks] nkb={nkb} S={S} sigma={sigma}")
+    g = torch.Generator().manual_seed(1000 + S)
+    q, k, v = (torch.randn(H, S, d, generator=g) * s for s in (sigma, sigma, 1.0))
+    q, k, v = (x.to(torch.bfloat16) for x in (q, k, v))
+    scale = d ** -0.5
+    out = hcms.attention(q.cuda(), k.cuda(), v.cuda(), scale).double().cpu().numpy()
+    for h in range(H):
+        want = oracle_mod.attention_head(q[h].double().numpy(), k[h].double().numpy(),
+                                         v[h].double().numpy(), scale)
+        check_attention_rows(out[h], want, f"nkb={nkb} S={S} h={h}")
+
+
 def test_attention_large_logits_and_rescaling(hcms, oracle_mod):
     """Q, K ~ N(0, 4^2): logits with std 16 keep raising the running maximum,
     exercising the lazy rescale path; also all-equal keys (uniform weights)."""
