@@ -543,24 +543,6 @@ constexpr int kDist = HCMS_ATTN_DIST;
 static_assert(kDist >= 1 && kDist + 1 <= kNB, "more blocks in flight than LDS buffers");
 static_assert(kPerWave == 2, "the wait counts below assume two DMA instructions per block");
 
-// One wave's 1 KiB of a block: lane l's 16 bytes at `voff` (plus the block
-// offset `soff`, which the buffer range check includes) land at LDS byte
-// lds_addr + 16 l.  Out-of-range reads land as zeros.
-// M0 is written here and read by nothing else in the kernel.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ inline void load_lds(unsigned lds_addr, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                 :: "s"(lds_addr), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// Wait until at most N of this wave's vector memory instructions are pending.
-template <int N>
-__device__ inline void wait_vm() {
-    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
-}
-
 // Score operands: S^T[i & 1] += K rows 32 (i & 1) + li, chunk 2 (i >> 1) + g,
 // times Q^T; `k_rd[i >> 1]` is the lane's byte offset of its row and chunk.
 #ifndef HCMS_ATTN_KAHEAD

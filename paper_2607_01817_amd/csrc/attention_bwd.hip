@@ -34,6 +34,16 @@
 // and V in LDS in the second keep each wave within 256 registers, so one
 // wave's MFMAs overlap the other's exponentials and LDS reads.
 //
+// At d = 128 with bf16 storage the two launches run DMA forms of these kernels
+// (attention_dq_dma_kernel, attention_dkdv_dma_kernel): the streamed tiles (K
+// and V, or Q, dO, L and D) go from global memory straight into LDS, three
+// blocks ahead through four buffers, instead of through registers, and the
+// transposed operands come from the row-major tiles by ds_read_b64_tr_b16.
+// A 16-byte chunk c of tile row r sits at chunk position c ^ f(r), with
+// f(r) = 4 (r mod 4) + (r / 4 mod 4), which keeps both the 16-byte row reads
+// and the transposing reads free of bank conflicts.  They use the same
+// operand values and MFMA order, so they give the same bits.
+//
 // Tails: loads go through buffer resources bounded by the head's tensor (rows
 // >= S read as zeros); keys or queries past S get P = 0 and are not stored.
 #include "attention_tiles.h"
@@ -215,6 +225,201 @@ __global__ __launch_bounds__(QTile<D>::threads, QTile<D>::per_cu) void attention
     }
 }
 
+// dQ for d = 128 with bf16 storage: K and V blocks go from global memory
+// straight into LDS (load_lds), three steps ahead, through four buffers each;
+// K^T operands come from the row-major K tile by ds_read_b64_tr_b16 (see
+// attention_dma_kernel for the instruction's lane layout).  Both tiles are
+// 64 keys x 256 bytes with chunk c of row r at position c ^ swz(r),
+// swz(r) = 4 (r mod 4) + (r / 4) mod 4: 16 consecutive rows of one chunk land
+// in 16 different groups of 4 banks (the 16-byte row reads of S^T = K Q^T and
+// dP^T = V dO^T), and so do 4 rows x 4 chunks (the transposing reads).  The
+// operand values and the MFMA order are those of attention_dq_kernel.
+namespace bdma {
+
+constexpr int kD = 128;
+constexpr int kWaves = 8;
+constexpr int kRowB = kD * 2;
+constexpr int kTileB = kBC * kRowB;                    // 16 KiB
+constexpr int kNB = 4;                                 // LDS buffers per tensor
+constexpr int kDist = 3;                               // steps between a block's load and its use
+constexpr int kPerWave = kTileB / (64 * 16) / kWaves;  // DMA instructions per wave and block
+static_assert(kPerWave == 2 && kDist + 1 <= kNB, "wait counts below assume this");
+
+__device__ inline unsigned swz(unsigned r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+template <int P>
+struct Phase {
+    static constexpr int value = P;
+};
+
+}  // namespace bdma
+
+__global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention_dq_dma_kernel(
+    const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
+    const __bf16 *__restrict__ o, const __bf16 *__restrict__ dout, const float *__restrict__ lse,
+    __bf16 *__restrict__ dq, float *__restrict__ delta, int S, int n_qtiles, float c, float scale) {
+    using namespace bdma;
+    constexpr int D = kD, KK = D / 16, DT = D / 32;
+    __shared__ __attribute__((aligned(1024))) char lds[2 * kNB * kTileB];
+    const char *const kbase = lds;                 // K buffer b at kbase + b * kTileB
+    const char *const vbase = lds + kNB * kTileB;  // V buffer b at vbase + b * kTileB
+
+    const int logical = xcd_logical(blockIdx.x, gridDim.x);
+    const int head = logical / n_qtiles;
+    const int qtile = logical - head * n_qtiles;
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * 2;
+    const __amdgpu_buffer_rsrc_t qr = head_rsrc(q + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t vr = head_rsrc(v + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t or_ = head_rsrc(o + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t dr = head_rsrc(dout + hoff, hbytes);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 31, g = lane >> 5;
+    const int qi = qtile * (kQW * kWaves) + wave * kQW + li;
+
+    bf16x8 qreg[KK], doreg[KK];
+    float dpart = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        const unsigned off = static_cast<unsigned>(qi * D + kk * 16 + g * 8) * 2;
+        qreg[kk] = __builtin_bit_cast(bf16x8, load8<__bf16>(qr, off));
+        doreg[kk] = __builtin_bit_cast(bf16x8, load8<__bf16>(dr, off));
+        const bf16x8 ov = __builtin_bit_cast(bf16x8, load8<__bf16>(or_, off));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bf16x2 a = {doreg[kk][2 * e], doreg[kk][2 * e + 1]};
+            const bf16x2 b = {ov[2 * e], ov[2 * e + 1]};
+            dpart = __builtin_amdgcn_fdot2_f32_bf16(a, b, dpart, false);
+        }
+    }
+    const float Di = swap_halves_sum(dpart);
+    const float Li = qi < S ? lse[static_cast<int64_t>(head) * S + qi] : 0.f;
+    if (g == 0 && qi < S) delta[static_cast<int64_t>(head) * S + qi] = Di;
+
+    // Lane offsets: DMA sources (row r = 4 (2 wave + i) + lane / 16, chunk at
+    // position lane % 16), 16-byte row reads (row li of a 32-key half, chunk
+    // 2 kk + g) and transposing K^T reads (lane t = lane % 16 of group
+    // G = lane / 16; second read 8 rows on, whose swizzle differs).
+    unsigned src[kPerWave];
+#pragma unroll
+    for (int i = 0; i < kPerWave; ++i) {
+        const unsigned r = 4 * (kPerWave * wave + i) + (lane >> 4), p = lane & 15;
+        src[i] = r * kRowB + ((p ^ swz(r)) << 4);
+    }
+    unsigned row_rd[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) row_rd[kk] = li * kRowB + (((2 * kk + g) ^ swz(li)) << 4);
+    unsigned tr_rd[2][DT];
+    {
+        const unsigned G = lane >> 4, t = lane & 15;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const unsigned r = 4 * (G >> 1) + (t >> 2) + 8 * hh;  // key row within a 16-key step
+                const unsigned col = dt * 32 + 16 * (G & 1) + 4 * (t & 3);
+                tr_rd[hh][dt] = r * kRowB + (((col >> 3) ^ swz(r)) << 4) + ((col & 7) << 1);
+            }
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(tr_rd[hh][dt]));
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<uintptr_t>(lds));
+    const unsigned wave_dst = lds0 + kPerWave * wave * 1024;
+    auto issue = [&](int blk) {
+        const unsigned kd = wave_dst + (blk & (kNB - 1)) * kTileB;
+#pragma unroll
+        for (int i = 0; i < kPerWave; ++i) load_lds(kd + i * 1024, kr, src[i], blk * kTileB);
+#pragma unroll
+        for (int i = 0; i < kPerWave; ++i) load_lds(kd + kNB * kTileB + i * 1024, vr, src[i], blk * kTileB);
+    };
+
+    f32x16 dqacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) dqacc[dt] = f32x16{};
+    const int nkb = (S + kBC - 1) / kBC;
+
+    // Prologue: blocks 0..kDist-1 in flight; step j issues block j + kDist.
+#pragma unroll
+    for (int blk = 0; blk < kDist; ++blk) issue(blk);
+    wait_vm<4 * (kDist - 1)>();  // block 0 landed
+    __syncthreads();
+
+    typedef __attribute__((address_space(3))) bf16x4 LdsV4;
+    // Block j in buffer P (P = j % kNB, or -1 when known only at run time).
+    auto step = [&](int j, auto ph) {
+        constexpr int P = decltype(ph)::value;
+        const int bi = P >= 0 ? P : j % kNB;
+        const char *kb = kbase + bi * kTileB;
+        const char *vb = vbase + bi * kTileB;
+        issue(j + kDist);
+        const int kvalid = S - j * kBC;
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+            f32x16 sacc = {}, dpacc = {};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kb + row_rd[kk] + mt * 32 * kRowB);
+                const bf16x8 va = *reinterpret_cast<const bf16x8 *>(vb + row_rd[kk] + mt * 32 * kRowB);
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
+            }
+            bf16x8 dsb[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                f32x8 x;
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const int rr = h * 8 + r;
+                    const int key = mt * 32 + (rr >> 2) * 8 + g * 4 + (rr & 3);
+                    const float p = key < kvalid
+                        ? __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rr], c, -Li)) : 0.f;
+                    x[r] = p * (dpacc[rr] - Di);
+                }
+                dsb[h] = __builtin_convertvector(x, bf16x8);
+            }
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int ks = mt * 2 + h;
+                    const char *p0 = kb + ks * 16 * kRowB;
+                    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p0 + tr_rd[0][dt]));
+                    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p0 + tr_rd[1][dt]));
+                    const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                    dqacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[h], dqacc[dt], 0, 0, 0);
+                }
+        }
+        wait_vm<4 * (kDist - 1)>();  // block j + 1 landed
+        __syncthreads();
+    };
+    int j = 0;
+    for (; j + 4 <= nkb; j += 4) {
+        step(j, Phase<0>{});
+        step(j + 1, Phase<1>{});
+        step(j + 2, Phase<2>{});
+        step(j + 3, Phase<3>{});
+    }
+    for (; j < nkb; ++j) step(j, Phase<-1>{});
+    wait_vm<0>();  // no load into LDS is pending when the workgroup ends
+
+    if (qi < S) {
+        __bf16 *row = dq + hoff + static_cast<int64_t>(qi) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 x = {dqacc[dt][rb * 4 + 0] * scale, dqacc[dt][rb * 4 + 1] * scale,
+                                 dqacc[dt][rb * 4 + 2] * scale, dqacc[dt][rb * 4 + 3] * scale};
+                store4(row + dt * 32 + rb * 8 + g * 4, x);
+            }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // dK, dV: key-parallel
 // ---------------------------------------------------------------------------
@@ -278,6 +483,198 @@ struct QStage {
         if (tid < 16) *reinterpret_cast<f32x4 *>((tid < 8 ? ls : ds) + (tid & 7) * 4) = stat;
     }
 };
+
+// dK, dV for d = 128 with bf16 storage: the blocks of 32 queries (Q, dO, L,
+// D) go from global memory straight into LDS, three blocks ahead, through four
+// buffers each; Q and dO tiles are 32 x 256 bytes with the swizzle of
+// attention_dq_dma_kernel, read as 16-byte rows (S = Q K^T, dP = dO V^T) and
+// transposed by ds_read_b64_tr_b16 (dV^T += dO^T P, dK^T += Q^T dS).  Waves
+// 0 and 1 also load L and D (4 bytes per lane), so they count one more load
+// per block.  The operand values and the MFMA order are those of
+// attention_dkdv_kernel.
+__global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention_dkdv_dma_kernel(
+    const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
+    const __bf16 *__restrict__ dout, const float *__restrict__ lse, const float *__restrict__ delta,
+    __bf16 *__restrict__ dk, __bf16 *__restrict__ dv, int S, int n_ktiles, float c, float scale) {
+    using namespace bdma;
+    constexpr int D = kD, KK = D / 16, DT = D / 32, NT = 64 * kWaves, KEYS = kQW * kWaves;
+    constexpr int QTB = kQB * kRowB;  // one block of 32 queries: 8 KiB
+    constexpr int STB = 64 * 4;       // one statistics load: 64 floats
+    static_assert(QTB == 1024 * kWaves, "one DMA instruction per wave and tensor");
+    __shared__ __attribute__((aligned(16))) __bf16 vrows[KEYS * QLds<D>::RS];
+    __shared__ __attribute__((aligned(1024))) char lds[kNB * (2 * QTB + 2 * STB)];
+    const char *const qbase = lds;                  // Q block buffer b at qbase + b * QTB
+    const char *const dbase = lds + kNB * QTB;      // dO
+    const char *const lbase = lds + 2 * kNB * QTB;  // L (STB bytes per buffer)
+    const char *const ebase = lbase + kNB * STB;    // D
+
+    const int logical = xcd_logical(blockIdx.x, gridDim.x);
+    const int head = logical / n_ktiles;
+    const int ktile = logical - head * n_ktiles;
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * 2;
+    const __amdgpu_buffer_rsrc_t qr = head_rsrc(q + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t vr = head_rsrc(v + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t dr = head_rsrc(dout + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t lr = head_rsrc(lse + static_cast<int64_t>(head) * S, int64_t{S} * 4);
+    const __amdgpu_buffer_rsrc_t er = head_rsrc(delta + static_cast<int64_t>(head) * S, int64_t{S} * 4);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 31, g = lane >> 5;
+    const int key0 = ktile * KEYS;
+    const int kj = key0 + wave * kQW + li;
+
+    bf16x8 kreg[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        kreg[kk] = __builtin_bit_cast(
+            bf16x8, load8<__bf16>(kr, static_cast<unsigned>(kj * D + kk * 16 + g * 8) * 2));
+    constexpr int CH = D / 8;
+#pragma unroll
+    for (int i = 0; i < KEYS * CH / NT; ++i) {
+        const int u = tid + i * NT, row = u / CH, ch = u % CH;
+        *reinterpret_cast<u32x4 *>(vrows + row * QLds<D>::RS + ch * 8) =
+            load8<__bf16>(vr, static_cast<unsigned>((key0 + row) * D + ch * 8) * 2);
+    }
+    f32x16 dkacc[DT], dvacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        dkacc[dt] = f32x16{};
+        dvacc[dt] = f32x16{};
+    }
+    const int nqb = (S + kQB - 1) / kQB;
+    const __bf16 *vmine = vrows + (wave * kQW + li) * QLds<D>::RS + g * 8;
+
+    // Lane offsets: DMA source (row 4 wave + lane / 16, chunk at position
+    // lane % 16), 16-byte row reads (query li, chunk 2 kk + g) and the two
+    // transposing reads of each 16-query step.
+    unsigned src;
+    {
+        const unsigned r = 4 * wave + (lane >> 4), p = lane & 15;
+        src = r * kRowB + ((p ^ swz(r)) << 4);
+    }
+    unsigned row_rd[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) row_rd[kk] = li * kRowB + (((2 * kk + g) ^ swz(li)) << 4);
+    unsigned tr_rd[2][DT];
+    {
+        const unsigned G = lane >> 4, t = lane & 15;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const unsigned r = 4 * (G >> 1) + (t >> 2) + 8 * hh;
+                const unsigned col = dt * 32 + 16 * (G & 1) + 4 * (t & 3);
+                tr_rd[hh][dt] = r * kRowB + (((col >> 3) ^ swz(r)) << 4) + ((col & 7) << 1);
+            }
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(tr_rd[hh][dt]));
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<uintptr_t>(lds));
+    auto issue = [&](int blk) {
+        const unsigned b = blk & (kNB - 1);
+        load_lds(lds0 + b * QTB + wave * 1024, qr, src, blk * QTB);
+        load_lds(lds0 + kNB * QTB + b * QTB + wave * 1024, dr, src, blk * QTB);
+        if (wave == 0) load_lds_b32(lds0 + 2 * kNB * QTB + b * STB, lr, lane * 4, blk * kQB * 4);
+        if (wave == 1) load_lds_b32(lds0 + 2 * kNB * QTB + kNB * STB + b * STB, er, lane * 4, blk * kQB * 4);
+    };
+    // All but the latest (kDist - 1) blocks' loads of this wave landed.
+    auto wait_blocks = [&]() {
+        if (wave < 2) wait_vm<3 * (kDist - 1)>();
+        else wait_vm<2 * (kDist - 1)>();
+    };
+
+#pragma unroll
+    for (int blk = 0; blk < kDist; ++blk) issue(blk);
+    wait_blocks();  // block 0 landed (and the V rows were stored)
+    __syncthreads();
+
+    typedef __attribute__((address_space(3))) bf16x4 LdsV4;
+    auto step = [&](int i, auto ph) {
+        constexpr int P = decltype(ph)::value;
+        const int bi = P >= 0 ? P : i % kNB;
+        const char *qb = qbase + bi * QTB;
+        const char *db = dbase + bi * QTB;
+        const float *lb = reinterpret_cast<const float *>(lbase + bi * STB);
+        const float *eb = reinterpret_cast<const float *>(ebase + bi * STB);
+        issue(i + kDist);
+        f32x16 s = {}, dp = {};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8 qa = *reinterpret_cast<const bf16x8 *>(qb + row_rd[kk]);
+            const bf16x8 da = *reinterpret_cast<const bf16x8 *>(db + row_rd[kk]);
+            const bf16x8 vb = *reinterpret_cast<const bf16x8 *>(vmine + kk * 16);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], s, 0, 0, 0);
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
+        }
+        const int qvalid = S - i * kQB;
+        bf16x8 pb[2], dsb[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const f32x4 l0 = *reinterpret_cast<const f32x4 *>(lb + h * 16 + g * 4);
+            const f32x4 l1 = *reinterpret_cast<const f32x4 *>(lb + h * 16 + 8 + g * 4);
+            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(eb + h * 16 + g * 4);
+            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(eb + h * 16 + 8 + g * 4);
+            f32x8 p, ds;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int rr = h * 8 + r;
+                const int qrow = (rr >> 2) * 8 + g * 4 + (rr & 3);
+                const float Lr = (r < 4) ? l0[r & 3] : l1[r & 3];
+                const float Dr = (r < 4) ? e0[r & 3] : e1[r & 3];
+                p[r] = qrow < qvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[rr], c, -Lr)) : 0.f;
+                ds[r] = p[r] * (dp[rr] - Dr);
+            }
+            pb[h] = __builtin_convertvector(p, bf16x8);
+            dsb[h] = __builtin_convertvector(ds, bf16x8);
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int qs = 0; qs < 2; ++qs) {
+                const char *d0 = db + qs * 16 * kRowB, *q0p = qb + qs * 16 * kRowB;
+                const bf16x4 dlo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(d0 + tr_rd[0][dt]));
+                const bf16x4 dhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(d0 + tr_rd[1][dt]));
+                const bf16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(q0p + tr_rd[0][dt]));
+                const bf16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(q0p + tr_rd[1][dt]));
+                const bf16x8 da = __builtin_shufflevector(dlo, dhi, 0, 1, 2, 3, 4, 5, 6, 7);
+                const bf16x8 qa = __builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7);
+                dvacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, pb[qs], dvacc[dt], 0, 0, 0);
+                dkacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, dsb[qs], dkacc[dt], 0, 0, 0);
+            }
+        wait_blocks();  // block i + 1 landed
+        __syncthreads();
+    };
+    int i = 0;
+    for (; i + 4 <= nqb; i += 4) {
+        step(i, Phase<0>{});
+        step(i + 1, Phase<1>{});
+        step(i + 2, Phase<2>{});
+        step(i + 3, Phase<3>{});
+    }
+    for (; i < nqb; ++i) step(i, Phase<-1>{});
+    wait_vm<0>();
+
+    if (kj < S) {
+        __bf16 *krow = dk + hoff + static_cast<int64_t>(kj) * D;
+        __bf16 *vrow = dv + hoff + static_cast<int64_t>(kj) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 xk = {dkacc[dt][rb * 4 + 0] * scale, dkacc[dt][rb * 4 + 1] * scale,
+                                  dkacc[dt][rb * 4 + 2] * scale, dkacc[dt][rb * 4 + 3] * scale};
+                const f32x4 xv = {dvacc[dt][rb * 4 + 0], dvacc[dt][rb * 4 + 1], dvacc[dt][rb * 4 + 2],
+                                  dvacc[dt][rb * 4 + 3]};
+                store4(krow + dt * 32 + rb * 8 + g * 4, xk);
+                store4(vrow + dt * 32 + rb * 8 + g * 4, xv);
+            }
+    }
+}
 
 template <int D, typename T>
 __global__ __launch_bounds__(KTile<D>::threads, KTile<D>::per_cu) void attention_dkdv_kernel(
@@ -405,6 +802,17 @@ __global__ __launch_bounds__(KTile<D>::threads, KTile<D>::per_cu) void attention
     }
 }
 
+#ifndef HCMS_BWD_DQ_DMA
+#define HCMS_BWD_DQ_DMA 1
+#endif
+// d = 128 with bf16 storage runs attention_dq_dma_kernel.
+constexpr bool kDqDma = HCMS_BWD_DQ_DMA != 0;
+#ifndef HCMS_BWD_DKDV_DMA
+#define HCMS_BWD_DKDV_DMA 1
+#endif
+// d = 128 with bf16 storage runs attention_dkdv_dma_kernel.
+constexpr bool kDkdvDma = HCMS_BWD_DKDV_DMA != 0;
+
 template <int D, typename T>
 hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const void *o,
                             const void *dout, const float *lse, void *dq, void *dk, void *dv,
@@ -415,16 +823,32 @@ hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const v
     const int n_tiles = (S + KTile<D>::keys - 1) / KTile<D>::keys;
     const int64_t blocks = static_cast<int64_t>(n_tiles) * n_heads;
     if (blocks > 0x7fffffff || qblocks > 0x7fffffff) return hipErrorInvalidValue;
-    attention_dq_kernel<D, T><<<static_cast<unsigned>(qblocks), QTile<D>::threads, 0, stream>>>(
-        static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
-        static_cast<const T *>(o), static_cast<const T *>(dout), lse, static_cast<T *>(dq), delta, S,
-        n_qt, c, scale);
+    if constexpr (D == bdma::kD && sizeof(T) == 2 && kDqDma) {
+        static_assert(QTile<D>::waves == bdma::kWaves, "the DMA kernel covers 256 queries in 8 waves");
+        attention_dq_dma_kernel<<<static_cast<unsigned>(qblocks), QTile<D>::threads, 0, stream>>>(
+            static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
+            static_cast<const __bf16 *>(o), static_cast<const __bf16 *>(dout), lse,
+            static_cast<__bf16 *>(dq), delta, S, n_qt, c, scale);
+    } else {
+        attention_dq_kernel<D, T><<<static_cast<unsigned>(qblocks), QTile<D>::threads, 0, stream>>>(
+            static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
+            static_cast<const T *>(o), static_cast<const T *>(dout), lse, static_cast<T *>(dq), delta, S,
+            n_qt, c, scale);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    attention_dkdv_kernel<D, T><<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
-        static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
-        static_cast<const T *>(dout), lse, delta, static_cast<T *>(dk), static_cast<T *>(dv), S,
-        n_tiles, c, scale);
+    if constexpr (D == bdma::kD && sizeof(T) == 2 && kDkdvDma) {
+        static_assert(KTile<D>::waves == bdma::kWaves, "the DMA kernel covers 256 keys in 8 waves");
+        attention_dkdv_dma_kernel<<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
+            static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
+            static_cast<const __bf16 *>(dout), lse, delta, static_cast<__bf16 *>(dk),
+            static_cast<__bf16 *>(dv), S, n_tiles, c, scale);
+    } else {
+        attention_dkdv_kernel<D, T><<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
+            static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
+            static_cast<const T *>(dout), lse, delta, static_cast<T *>(dk), static_cast<T *>(dv), S,
+            n_tiles, c, scale);
+    }
     return hipGetLastError();
 }
 

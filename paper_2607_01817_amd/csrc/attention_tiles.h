@@ -53,6 +53,32 @@ __device__ inline void store4(__bf16 *p, f32x4 x) {
 }
 __device__ inline void store4(float *p, f32x4 x) { *reinterpret_cast<f32x4 *>(p) = x; }
 
+// One wave's 1 KiB of a block loaded straight into LDS (gfx950
+// buffer_load_dwordx4 ... lds): lane l's 16 bytes at `voff` plus the block
+// offset `soff` (the buffer range check covers both; out-of-range lanes write
+// zeros) land at LDS byte lds_addr + 16 l.  Inline asm: with the intrinsic the
+// compiler waits for every such load before any later LDS read, so the
+// kernels count these loads themselves (wait_vm).  M0 is written here and read
+// by nothing else in the kernels.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ inline void load_lds(unsigned lds_addr, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(lds_addr), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+// The same with 4 bytes per lane (lane l at LDS byte lds_addr + 4 l).
+__device__ inline void load_lds_b32(unsigned lds_addr, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+                 :: "s"(lds_addr), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N of this wave's vector memory instructions are pending.
+template <int N>
+__device__ inline void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
 // Position of key `k` (0..63) inside a transposed V row: bits 2 and 3 swapped.
 __device__ inline int vt_pos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
 
