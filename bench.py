@@ -288,7 +288,7 @@ def training_step(ctx, w, chunks, reps: int, dev):
     res["backward_roofline"] = {
         "bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
         "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-        "kernels": "attention_dq_kernel<128, bf16> + attention_dkdv_kernel<128, bf16>",
+        "kernels": "attention_dq_dma_kernel + attention_dkdv_dma_kernel (d = 128, bf16)",
         "per_launch": f"10*S^2*H_c*d FLOP per chunk (executed: 14*S^2*H_c*d, Q K^T and dO V^T "
                       f"are computed in both launches); avg {statistics.mean(attn_ms):.4f} ms over "
                       f"{len(attn_ms)} chunk backward launches, serial schedule"}
