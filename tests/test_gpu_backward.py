@@ -75,6 +75,25 @@ def test_backward_matches_oracle(hcms, oracle_mod, S, H, d, dtype, sigma):
         assert torch.equal(dv.cpu(), do)
 
 
+@pytest.mark.parametrize("n", range(1, 10))
+@pytest.mark.parametrize("ragged", [False, True])
+def test_backward_every_block_count(hcms, oracle_mod, n, ragged):
+    """d = 128 bf16: every count of 64-key blocks from 1 to 9 (the dQ kernel's
+    key loop, four blocks per pass plus a remainder of 0 to 3) and of 32-query
+    blocks from 1 to 18 (the dK/dV kernel's query loop), ragged (S = 64 n - 41:
+    n key blocks, 2 n - 1 query blocks, both tails partial) and exact (S = 64 n)."""
+    S = 64 * n - 41 if ragged else 64 * n
+    log(f"[backward blocks] S={S} (key blocks {n}, query blocks {(S + 31) // 32})")
+    q, k, v, do = _data(S, 2, 128, torch.bfloat16, 1000 + S, 1.5)
+    scale = 128 ** -0.5
+    out, lse, dq, dk, dv = _run(hcms, q, k, v, do, scale)
+    for h in range(2):
+        Q, K, V, G = (x[h].double().numpy() for x in (q, k, v, do))
+        rq, rk, rv = oracle_mod.attention_backward_head(Q, K, V, G, scale)
+        for name, got, want in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+            _check_grad(got[h].double().cpu().numpy(), want, f"{name} head {h}")
+
+
 def test_training_forward_output_equals_inference_forward(hcms):
     q, k, v, _ = _data(3000, 3, 128, torch.bfloat16, 11)
     qd, kd, vd = (x.cuda() for x in (q, k, v))
