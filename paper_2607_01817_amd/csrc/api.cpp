@@ -540,6 +540,23 @@ int check_forward(const ForwardArgs &f, int *mode, int *log2u) {
     return HCMS_OK;
 }
 
+// LDS reservation of a chunk's copy.  In the inline schedule the copy
+// stream's packs (chunks 1..C-1) run beside attention 0 and its unpacks
+// (chunks 0..C-2) beside attention C-1.  They hold kCopyBesideAttentionLds,
+// which keeps them off the CUs the attention workgroups occupy: they take the
+// CUs those launches' last rounds leave idle (or wait for the launch to end)
+// instead of taking issue slots from attention waves.  In the other
+// schedules a copy becomes ready when a launch starts (an unpack after the
+// previous chunk's attention, a lane's pack), and a reserved copy that takes
+// a CU first keeps the launch's workgroup off it, so they reserve nothing.
+auto copy_lds_reserve(int mode, int C) {
+    return [mode, C](int kind, int c) -> unsigned {
+        if (mode != HCMS_MODE_INLINE) return 0;
+        if ((kind == HCMS_OP_PACK && c == 0) || (kind == HCMS_OP_UNPACK && c == C - 1)) return 0;
+        return hcms::kCopyBesideAttentionLds;
+    };
+}
+
 // Issues a validated hcms_forward (S > 0) in the resolved mode.
 int issue_forward(const ForwardArgs &f, int mode, int log2u) {
     const int64_t head_bytes = static_cast<int64_t>(f.S) * f.d * elem_bytes(f.dtype);
@@ -551,11 +568,12 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
         const int64_t first = slot_heads > 0 ? static_cast<int64_t>(c & 1) * slot_heads : h0;
         return static_cast<char *>(p) + head_bytes * first;
     };
+    const auto beside = copy_lds_reserve(mode, f.n_chunks);
     auto launch = [&](int kind, int c, int h0, int hc, hipStream_t s) -> hipError_t {
         if (kind == HCMS_OP_PACK) {
             const void *src[3] = {f.q_seq, f.k_seq, f.v_seq};
             void *dst[3] = {at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0)};
-            return hcms::launch_pack(src, dst, 3, f.S, f.H, h0, hc, log2u, s);
+            return hcms::launch_pack(src, dst, 3, f.S, f.H, h0, hc, log2u, beside(kind, c), s);
         }
         if (kind == HCMS_OP_ATTENTION)
             return hcms::launch_attention(at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0),
@@ -564,7 +582,7 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
                                           f.S, hc, f.d, c_log2e, f.dtype, s);
         const void *src[1] = {at(f.o_hm, c, h0)};
         void *dst[1] = {f.o_seq};
-        return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, s);
+        return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, beside(kind, c), s);
     };
     return execute_plan(f.ctx, mode, f.chunk_sizes, f.n_chunks, f.main_stream, f.copy_stream,
                         f.compute_stream, launch);
@@ -712,7 +730,7 @@ int hcms_pack(const void *src_seq, void *dst_hm, int P, int S, int H, int d, int
     if (st != HCMS_OK) return st;
     const void *src[1] = {src_seq};
     void *dst[1] = {dst_hm};
-    const hipError_t e = hcms::launch_pack(src, dst, 1, S, H, h_begin, h_count, log2u,
+    const hipError_t e = hcms::launch_pack(src, dst, 1, S, H, h_begin, h_count, log2u, 0,
                                            static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "pack launch");
     return ok();
@@ -725,7 +743,7 @@ int hcms_unpack(const void *src_hm, void *dst_seq, int P, int S, int H, int d, i
     if (st != HCMS_OK) return st;
     const void *src[1] = {src_hm};
     void *dst[1] = {dst_seq};
-    const hipError_t e = hcms::launch_unpack(src, dst, 1, S, H, h_begin, h_count, log2u,
+    const hipError_t e = hcms::launch_unpack(src, dst, 1, S, H, h_begin, h_count, log2u, 0,
                                              static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "unpack launch");
     return ok();
@@ -1114,11 +1132,12 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
     auto at = [head_bytes](const void *p, int h0) {
         return const_cast<char *>(static_cast<const char *>(p)) + head_bytes * h0;
     };
-    auto launch = [&](int kind, int /*chunk*/, int h0, int hc, hipStream_t s) -> hipError_t {
+    const auto beside = copy_lds_reserve(mode, n_chunks);
+    auto launch = [&](int kind, int c, int h0, int hc, hipStream_t s) -> hipError_t {
         if (kind == HCMS_OP_PACK) {
             const void *src[1] = {dout_seq};
             void *dst[1] = {at(do_hm, h0)};
-            return hcms::launch_pack(src, dst, 1, S, H, h0, hc, log2u, s);
+            return hcms::launch_pack(src, dst, 1, S, H, h0, hc, log2u, beside(kind, c), s);
         }
         if (kind == HCMS_OP_ATTENTION) {
             const int64_t so = static_cast<int64_t>(h0) * S;
@@ -1129,7 +1148,7 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
         }
         const void *src[3] = {at(dq_hm, h0), at(dk_hm, h0), at(dv_hm, h0)};
         void *dst[3] = {dq_seq, dk_seq, dv_seq};
-        return hcms::launch_unpack(src, dst, 3, S, H, h0, hc, log2u, s);
+        return hcms::launch_unpack(src, dst, 3, S, H, h0, hc, log2u, beside(kind, c), s);
     };
     return execute_plan(ctx, mode, chunk_sizes, n_chunks, main_stream, copy_stream, compute_stream,
                         launch);

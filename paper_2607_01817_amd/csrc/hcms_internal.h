@@ -16,13 +16,24 @@ const char *last_error();
 // Copy `n_tensors` (1..3) head chunks at once.  Each tensor z moves
 //   dst[z][j][t][:] = src[z][t][h0 + j][:]   (pack)
 // for t < S, j < hc, where a row ([:]) is 16 << log2_units bytes.
+// lds_reserve (at most 64 KiB): LDS bytes every workgroup holds unused.  The
+// kernels need none; a reservation larger than the LDS an attention
+// workgroup leaves free on its CU (kCopyBesideAttentionLds) keeps the copy's
+// workgroups off CUs that run attention, so a copy issued beside an attention
+// launch runs on the CUs its last round leaves idle instead of taking issue
+// slots from the attention waves.
 hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors,
                        int64_t S, int64_t H, int64_t h0, int64_t hc, int log2_units,
-                       hipStream_t stream);
+                       unsigned lds_reserve, hipStream_t stream);
 
 // Each tensor z moves  dst[z][t][h0 + j][:] = src[z][j][t][:]   (unpack)
 hipError_t launch_unpack(const void *const *src, void *const *dst, int n_tensors, int64_t S,
-                         int64_t H, int64_t h0, int64_t hc, int log2_units, hipStream_t stream);
+                         int64_t H, int64_t h0, int64_t hc, int log2_units, unsigned lds_reserve,
+                         hipStream_t stream);
+
+// The d = 128 bf16 attention kernels hold 128 KiB or more of a CU's 160 KiB
+// of LDS; a copy workgroup holding 40 KiB therefore never shares a CU with one.
+inline constexpr unsigned kCopyBesideAttentionLds = 40 * 1024;
 
 // Attention of `n_heads` consecutive heads, head-major [n_heads][S][d]
 // buffers starting at the chunk's first head.  scale_log2e = scale * log2(e).

@@ -34,6 +34,7 @@ namespace {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
+constexpr unsigned kMaxLdsReserve = 64 * 1024;  // at most 64 KiB per workgroup
 constexpr int kUnroll = 3;
 constexpr int kUnitsPerBlock = kThreads * kUnroll;  // 16-byte units per workgroup
 constexpr int kNonTemporal = 2;                     // cache-policy bit of a streaming load
@@ -123,16 +124,18 @@ dim3 grid_for(int64_t S, int64_t hc, int log2_units, int n_tensors) {
                 static_cast<unsigned>(hc), static_cast<unsigned>(n_tensors));
 }
 
+// lds_reserve: bytes of LDS each workgroup holds without using them (see
+// launch_pack).
 template <int LOG2U>
 void pack_dispatch(const PackPtrs &p, int n_tensors, int64_t S, int64_t H, int64_t h0,
-                   int64_t hc, hipStream_t stream) {
-    pack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, n_tensors), kThreads, 0, stream>>>(p, S, H, h0);
+                   int64_t hc, unsigned lds_reserve, hipStream_t stream) {
+    pack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, n_tensors), kThreads, lds_reserve, stream>>>(p, S, H, h0);
 }
 
 template <int LOG2U>
 void unpack_dispatch(const PackPtrs &p, int n_tensors, int64_t S, int64_t H, int64_t h0,
-                     int64_t hc, hipStream_t stream) {
-    unpack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, n_tensors), kThreads, 0, stream>>>(p, S, H, h0);
+                     int64_t hc, unsigned lds_reserve, hipStream_t stream) {
+    unpack_kernel<LOG2U><<<grid_for(S, hc, LOG2U, n_tensors), kThreads, lds_reserve, stream>>>(p, S, H, h0);
 }
 
 // Lane offsets on the strided side are 32-bit: a workgroup spans at most
@@ -142,8 +145,10 @@ bool strided_span_fits(int64_t H) { return H > 0 && H * (int64_t{kUnitsPerBlock}
 }  // namespace
 
 hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, int64_t S,
-                       int64_t H, int64_t h0, int64_t hc, int log2_units, hipStream_t stream) {
+                       int64_t H, int64_t h0, int64_t hc, int log2_units, unsigned lds_reserve,
+                       hipStream_t stream) {
     if (S == 0 || hc == 0) return hipSuccess;
+    if (lds_reserve > kMaxLdsReserve) return hipErrorInvalidValue;
     if (!strided_span_fits(H) || n_tensors < 1 || n_tensors > 3) return hipErrorInvalidValue;
     PackPtrs p{};
     for (int z = 0; z < n_tensors; ++z) {
@@ -151,21 +156,23 @@ hipError_t launch_pack(const void *const *src, void *const *dst, int n_tensors, 
         p.dst[z] = static_cast<char *>(dst[z]);
     }
     switch (log2_units) {
-        case 0: pack_dispatch<0>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 1: pack_dispatch<1>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 2: pack_dispatch<2>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 3: pack_dispatch<3>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 4: pack_dispatch<4>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 5: pack_dispatch<5>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 6: pack_dispatch<6>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 0: pack_dispatch<0>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 1: pack_dispatch<1>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 2: pack_dispatch<2>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 3: pack_dispatch<3>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 4: pack_dispatch<4>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 5: pack_dispatch<5>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 6: pack_dispatch<6>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_unpack(const void *const *src, void *const *dst, int n_tensors, int64_t S,
-                         int64_t H, int64_t h0, int64_t hc, int log2_units, hipStream_t stream) {
+                         int64_t H, int64_t h0, int64_t hc, int log2_units, unsigned lds_reserve,
+                         hipStream_t stream) {
     if (S == 0 || hc == 0) return hipSuccess;
+    if (lds_reserve > kMaxLdsReserve) return hipErrorInvalidValue;
     if (!strided_span_fits(H) || n_tensors < 1 || n_tensors > 3) return hipErrorInvalidValue;
     PackPtrs p{};
     for (int z = 0; z < n_tensors; ++z) {
@@ -173,13 +180,13 @@ hipError_t launch_unpack(const void *const *src, void *const *dst, int n_tensors
         p.dst[z] = static_cast<char *>(dst[z]);
     }
     switch (log2_units) {
-        case 0: unpack_dispatch<0>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 1: unpack_dispatch<1>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 2: unpack_dispatch<2>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 3: unpack_dispatch<3>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 4: unpack_dispatch<4>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 5: unpack_dispatch<5>(p, n_tensors, S, H, h0, hc, stream); break;
-        case 6: unpack_dispatch<6>(p, n_tensors, S, H, h0, hc, stream); break;
+        case 0: unpack_dispatch<0>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 1: unpack_dispatch<1>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 2: unpack_dispatch<2>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 3: unpack_dispatch<3>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 4: unpack_dispatch<4>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 5: unpack_dispatch<5>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
+        case 6: unpack_dispatch<6>(p, n_tensors, S, H, h0, hc, lds_reserve, stream); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
