@@ -10,8 +10,8 @@ tokens (36 latent frames x 1560), H = 5 local heads, d = 128, bf16, chunks
 
 Printed: one JSON line with the metric (attention TFLOP/s, 4 S^2 H d per step
 over the step time), the roofline of the dominant kernel (attention, bf16
-MFMA), the layout kernels' HBM rates, the serial, Alg. 1, inline and lanes
-schedules side by side, and the oracle timed on the host cores on a bounded
+MFMA), the layout kernels' HBM rates, the serial, Alg. 1, inline, lanes,
+fused and two-slot schedules side by side, and the oracle timed on the host cores on a bounded
 sample of the same workload.
 """
 from __future__ import annotations
@@ -135,7 +135,8 @@ def cpu_baseline(w, q, k, v, seconds: float):
 
 
 MODES = {"serial": hcms.MODE_SERIAL, "pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE,
-         "lanes": hcms.MODE_LANES, "auto": hcms.MODE_AUTO, "slots": hcms.MODE_SLOTS}
+         "lanes": hcms.MODE_LANES, "auto": hcms.MODE_AUTO, "slots": hcms.MODE_SLOTS,
+         "fused": hcms.MODE_FUSED}
 MODE_NAMES = {v: k for k, v in MODES.items()}
 
 
@@ -145,14 +146,14 @@ def quartiles(xs):
 
 
 def compare_modes(ctx, w, chunks, reps: int, dev):
-    """Serial, Alg. 1, inline and lanes schedules of one workload, interleaved
+    """Serial, Alg. 1, inline, lanes, fused and two-slot schedules of one workload, interleaved
     (order reversed every other rep to cancel clock drift), step time from
     events on the main stream."""
     q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
     out = torch.empty_like(q)
     ws = ctx.workspaces(w.S, w.H, w.d, q.dtype)
     slots = ctx.slot_workspaces(w.S, max(chunks), w.d, q.dtype)
-    modes = ["serial", "pipelined", "inline", "lanes", "slots_two_slot"]
+    modes = ["serial", "pipelined", "inline", "lanes", "fused", "slots_two_slot"]
 
     def run(m):
         if m == "slots_two_slot":   # the slots plan on two chunk slots
@@ -465,7 +466,10 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
             "traffic": measured_traffic(w.name, sizes),
-            "kernel": "attention_dma_kernel (d = 128, bf16)",
+            "kernel": "attention_dma_kernel (d = 128, bf16)" + (
+                "; in the fused plan each launch also carries the neighbouring chunks' copies "
+                "on the CUs its last round leaves idle (attention_dma_kernel<true>)"
+                if plan == "fused" else ""),
             "per_launch": f"4*S^2*H_c*d FLOP per chunk launch; avg launch {avg_attn_ms:.4f} ms "
                           f"over {len(attn_ms)} launches, events on the launching stream, in "
                           f"a second pass of the {args.steps} steps "
@@ -477,8 +481,19 @@ def main():
         es = w.elem_bytes
         pk_bytes = [3 * 2 * w.S * sizes[i % C] * w.d * es for i in range(len(pack_ms))]
         up_bytes = [2 * w.S * sizes[i % C] * w.d * es for i in range(len(unpack_ms))]
-        pipe = {"pack_in_step_GBps": round(sum(pk_bytes) / (sum(pack_ms) * 1e-3) / 1e9, 1),
-                "unpack_in_step_GBps": round(sum(up_bytes) / (sum(unpack_ms) * 1e-3) / 1e9, 1)}
+        # In the fused plan a copy that rides in an attention launch reports
+        # that launch's time; the rates then cover the copies that ran alone
+        # (chunk 0's pack, the last chunk's unpack).
+        own_pk = [i for i in range(len(pack_ms)) if plan != "fused" or i % C == 0]
+        own_up = [i for i in range(len(unpack_ms)) if plan != "fused" or i % C == C - 1]
+        pipe = {"pack_in_step_GBps": round(sum(pk_bytes[i] for i in own_pk) /
+                                           (sum(pack_ms[i] for i in own_pk) * 1e-3) / 1e9, 1),
+                "unpack_in_step_GBps": round(sum(up_bytes[i] for i in own_up) /
+                                             (sum(unpack_ms[i] for i in own_up) * 1e-3) / 1e9, 1)}
+        if plan == "fused":
+            pipe["in_step_note"] = ("fused plan: rates of the copies that ran as launches of "
+                                    "their own (chunk 0's pack, the last unpack); the others "
+                                    "rode in the attention launches")
 
         # ---- layout kernels alone on the Wan-P4, Wan-P8 and Stress shapes:
         # cold (MALL flushed) and warm.  A byte move does not depend on the
@@ -514,7 +529,7 @@ def main():
         res.update(pipe)
         result["layout"] = res
 
-        # ---- the schedules side by side: serial, Alg. 1, inline, lanes ----
+        # ---- the schedules side by side: serial, Alg. 1, inline, lanes, fused ----
         torch.cuda.synchronize()
         reps = max(20, args.steps // 2)
         cmp = [compare_modes(ctx, w, sizes, reps, dev), compare_modes(ctx, w, (w.H,), reps, dev)]

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define HCMS_ABI_VERSION 1
+#define HCMS_ABI_VERSION 2
 
 #if defined(__GNUC__)
 #define HCMS_API __attribute__((visibility("default")))
@@ -181,8 +181,9 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
 #define HCMS_MODE_PIPELINED 1  /* Alg. 1: copy stream + compute stream + events */
 #define HCMS_MODE_INLINE 2     /* one lane, four synchronisations (see hcms_plan) */
 #define HCMS_MODE_LANES 3      /* chunks alternate between two streams (see hcms_plan) */
-#define HCMS_MODE_AUTO 4       /* hcms_forward only: inline or lanes, per hcms_auto_mode */
+#define HCMS_MODE_AUTO 4       /* hcms_forward only: fused, inline or lanes, per hcms_auto_mode */
 #define HCMS_MODE_SLOTS 5      /* Alg. 1's streams, copies interleaved so slots can be reused */
+#define HCMS_MODE_FUSED 6      /* one stream; neighbouring copies ride in each attention launch */
 
 /* Op kinds, streams and event ids of a plan (hcms_plan). */
 #define HCMS_OP_RECORD 0     /* record event `event` on `stream` */
@@ -194,6 +195,7 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
 #define HCMS_STREAM_MAIN 0
 #define HCMS_STREAM_COPY 1
 #define HCMS_STREAM_COMPUTE 2
+#define HCMS_STREAM_IN_ATTENTION 3  /* runs inside the next ATTENTION op's launch (fused mode) */
 
 typedef struct hcms_op {
     int kind;    /* HCMS_OP_* */
@@ -237,7 +239,19 @@ typedef struct hcms_op {
  * that chunk c + 2 can reuse chunk c's workspace slot (the input layout of one
  * chunk and the output layout of another beside a chunk's attention,
  * Sec. 3.5).  The host issues every record before any wait on it.
- * With one chunk the inline and lanes plans are the serial plan.
+ * Fused mode runs on the main stream alone, with no events: it packs chunk
+ * 0; then, for every c, the pack of chunk c + 1 (c + 1 < C) and the unpack of
+ * chunk c - 1 (c >= 1) are issued on HCMS_STREAM_IN_ATTENTION, which means
+ * that they run inside the launch of the ATTENTION op that follows them, as
+ * workgroups dispatched after all of that launch's attention workgroups, on
+ * the CUs its last round leaves idle; after the last attention the main
+ * stream unpacks chunk C-1.  An op on HCMS_STREAM_IN_ATTENTION is ordered
+ * after every main-stream op before that attention and before every one
+ * after it, and overlaps the attention itself (it touches other heads'
+ * buffers).  Where a launch cannot carry them (not d = 128 bf16, or its last
+ * round leaves fewer than n_cu / 8 CUs idle) hcms_forward runs them right
+ * after that attention on the main stream instead.
+ * With one chunk the inline, lanes and fused plans are the serial plan.
  *   ops : host array of `cap` entries, or NULL to query the count.
  * Returns the number of ops (>= 0), HCMS_ERR_CHUNKS (n_chunks < 1),
  * HCMS_ERR_ARG (mode, or HCMS_MODE_AUTO, which has no fixed plan) or
@@ -252,11 +266,14 @@ HCMS_API int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap);
  * per CU for d = 128, 128 and two for d = 64).  One lane takes
  * sum_c ceil(W_c / (n_cu * B)) rounds of workgroups; two lanes pool them,
  * ceil(sum_c W_c / (n_cu * B)).  Returns HCMS_MODE_LANES when pooling saves a
- * round, HCMS_MODE_INLINE otherwise, HCMS_MODE_SERIAL for one chunk; or
- * HCMS_ERR_SHAPE (S < 0, d), HCMS_ERR_ARG (n_cu < 1), HCMS_ERR_NULL or
- * HCMS_ERR_CHUNKS.  Host only.
+ * round; otherwise HCMS_MODE_FUSED for d = 128 with bf16 storage (the launches
+ * that can carry the neighbouring chunks' copies) and HCMS_MODE_INLINE for the
+ * rest; HCMS_MODE_SERIAL for one chunk.  Errors: HCMS_ERR_SHAPE (S < 0, d),
+ * HCMS_ERR_DTYPE, HCMS_ERR_ARG (n_cu < 1), HCMS_ERR_NULL or HCMS_ERR_CHUNKS.
+ * Host only.
  */
-HCMS_API int hcms_auto_mode(int S, int d, const int *chunk_sizes, int n_chunks, int n_cu);
+HCMS_API int hcms_auto_mode(int S, int d, int dtype, const int *chunk_sizes, int n_chunks,
+                            int n_cu);
 
 /*
  * Time model of HCMS (Sec. 3.7, Theorem of the optimal chunk count; appendix
@@ -313,7 +330,8 @@ HCMS_API int hcms_ctx_destroy(hcms_ctx *ctx);
  * runs it (events are created here, once; later calls are not timed);
  * max_calls = 0 turns timing off.  Each call resets the record.
  * hcms_ctx_kernel_ms waits for the recorded events and writes the durations in
- * milliseconds, call by call and chunk by chunk, in issue order.
+ * milliseconds, call by call and chunk by chunk, in issue order.  In fused
+ * mode a copy that rides in an attention launch reports that launch's time.
  *   kind : HCMS_OP_PACK, HCMS_OP_ATTENTION or HCMS_OP_UNPACK
  * Returns the number of durations written, HCMS_ERR_ARG (timing off / bad
  * kind / max_calls < 0), HCMS_ERR_CAPACITY or HCMS_ERR_HIP.
@@ -339,7 +357,8 @@ HCMS_API int hcms_ctx_kernel_ms(hcms_ctx *ctx, int kind, float *ms_out, int cap)
  *   copy_stream, compute_stream: used in pipelined mode; must be distinct from
  *                                each other and from main_stream.  Inline mode
  *                                uses copy_stream only, lanes mode
- *                                compute_stream only (distinct from main).
+ *                                compute_stream only (distinct from main);
+ *                                fused mode uses neither.
  * Errors: as hcms_pack and hcms_attention, plus ARG (mode, stream reuse,
  * context of another device) and CHUNKS (n_chunks > the context's max_chunks).
  */
@@ -356,8 +375,8 @@ HCMS_API int hcms_forward(hcms_ctx *ctx,
  * need a head-major copy).  q_slots, k_slots, v_slots, o_slots are device
  * buffers of [2][slot_heads][S][d] each; chunk c uses slot c % 2 (its heads
  * at the slot's start), so slot_heads must be at least every chunk size.
- * Modes: HCMS_MODE_SERIAL, HCMS_MODE_LANES, HCMS_MODE_SLOTS and HCMS_MODE_AUTO
- * (lanes when hcms_auto_mode picks lanes, else serial).  Pipelined and inline
+ * Modes: HCMS_MODE_SERIAL, HCMS_MODE_LANES, HCMS_MODE_SLOTS, HCMS_MODE_FUSED and
+ * HCMS_MODE_AUTO (the mode hcms_auto_mode picks, serial in place of inline).  Pipelined and inline
  * modes would pack chunk c + 2 into chunk c's slot while its attention may
  * still run, and are rejected with HCMS_ERR_ARG.  No lse output: the backward
  * needs every head's head-major tensors.  o_seq is bit-identical to
@@ -389,8 +408,9 @@ HCMS_API int hcms_forward_slots(hcms_ctx *ctx, const void *q_seq, const void *k_
  *   dq_seq, dk_seq, dv_seq : outputs, [P][S/P][H][d]
  *   do_hm, dq_hm, dk_hm, dv_hm : device workspaces, [H][S][d] each
  *   delta            : device workspace, [H][S] fp32
- * Streams and modes as hcms_forward.  Every mode and chunking gives
- * bit-identical gradients.  Errors: as hcms_forward and
+ * Streams and modes as hcms_forward; in fused mode the copies run right after
+ * each chunk's backward launches (these carry none).  Every mode and chunking
+ * gives bit-identical gradients.  Errors: as hcms_forward and
  * hcms_attention_backward.
  */
 HCMS_API int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_seq,

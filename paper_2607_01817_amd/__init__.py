@@ -22,9 +22,10 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhcms.so")
 
 BF16, FP32 = 0, 1
-MODE_SERIAL, MODE_PIPELINED, MODE_INLINE, MODE_LANES, MODE_AUTO, MODE_SLOTS = 0, 1, 2, 3, 4, 5
+MODE_SERIAL, MODE_PIPELINED, MODE_INLINE, MODE_LANES, MODE_AUTO, MODE_SLOTS, MODE_FUSED = (
+    0, 1, 2, 3, 4, 5, 6)
 OP_RECORD, OP_WAIT, OP_PACK, OP_ATTENTION, OP_UNPACK = 0, 1, 2, 3, 4
-STREAM_MAIN, STREAM_COPY, STREAM_COMPUTE = 0, 1, 2
+STREAM_MAIN, STREAM_COPY, STREAM_COMPUTE, STREAM_IN_ATTENTION = 0, 1, 2, 3
 
 _DTYPES = {torch.bfloat16: BF16, torch.float32: FP32}
 _lib = None
@@ -69,7 +70,7 @@ def load():
         "hcms_attention_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, f, ip, i, i,
                                      vp], i),
         "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
-        "hcms_auto_mode": ([i, i, ip, i, i], i),
+        "hcms_auto_mode": ([i, i, i, ip, i, i], i),
         "hcms_ctx_last_mode": ([vp], i),
         "hcms_model_time": ([d, d, d, d, i, dp], i),
         "hcms_model_optimal_chunks": ([d, d, i, dp], i),
@@ -153,10 +154,10 @@ def plan(n_chunks: int, mode: int = MODE_PIPELINED) -> list[tuple[int, int, int,
     return [(o.kind, o.stream, o.chunk, o.event) for o in ops]
 
 
-def auto_mode(S: int, d: int, chunk_sizes, n_cu: int) -> int:
+def auto_mode(S: int, d: int, chunk_sizes, n_cu: int, dtype: int = BF16) -> int:
     """The plan mode MODE_AUTO runs for these chunks on n_cu compute units."""
     sizes, n = _ints(chunk_sizes)
-    return _check(load().hcms_auto_mode(S, d, sizes, n, n_cu))
+    return _check(load().hcms_auto_mode(S, d, dtype, sizes, n, n_cu))
 
 
 def model_time(t0: float, t_comm: float, t_attn: float, beta: float, n_chunks: int) -> float:

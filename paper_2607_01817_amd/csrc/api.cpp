@@ -280,11 +280,33 @@ void slots_plan(int C, PlanWriter &w) {
     w.put(HCMS_OP_WAIT, HCMS_STREAM_MAIN, -1, e_done);
 }
 
+// One stream and no events, for one GPU.  The pack of chunk c + 1 and the
+// unpack of chunk c - 1 ride in the launch of attention c as extra
+// workgroups, dispatched after all of its attention workgroups, so they run
+// on the CUs the launch's last round leaves idle.  Stream order gives every
+// dependency of Alg. 1: pack c + 1 (in launch c) comes before attention c + 1
+// (launch c + 1), unpack c - 1 (in launch c) after attention c - 1 (launch
+// c - 1); and nothing in one launch touches the bytes of another op of the
+// same launch (chunk c's workspace heads, chunk c + 1's, chunk c - 1's output
+// rows).  Chunk 0's pack and the last unpack stay on the main stream.  The
+// copies a launch cannot carry run right after it (see hcms.h).
+void fused_plan(int C, PlanWriter &w) {
+    if (C == 1) return serial_plan(C, w);
+    w.put(HCMS_OP_PACK, HCMS_STREAM_MAIN, 0, -1);
+    for (int c = 0; c < C; ++c) {
+        if (c + 1 < C) w.put(HCMS_OP_PACK, HCMS_STREAM_IN_ATTENTION, c + 1, -1);
+        if (c >= 1) w.put(HCMS_OP_UNPACK, HCMS_STREAM_IN_ATTENTION, c - 1, -1);
+        w.put(HCMS_OP_ATTENTION, HCMS_STREAM_MAIN, c, -1);
+    }
+    w.put(HCMS_OP_UNPACK, HCMS_STREAM_MAIN, C - 1, -1);
+}
+
 // Modes with a fixed plan (hcms_plan); HCMS_MODE_AUTO resolves to one of
 // them per call.
 bool plan_mode(int mode) {
     return mode == HCMS_MODE_SERIAL || mode == HCMS_MODE_PIPELINED ||
-           mode == HCMS_MODE_INLINE || mode == HCMS_MODE_LANES || mode == HCMS_MODE_SLOTS;
+           mode == HCMS_MODE_INLINE || mode == HCMS_MODE_LANES || mode == HCMS_MODE_SLOTS ||
+           mode == HCMS_MODE_FUSED;
 }
 
 int build_plan(int C, int mode, PlanWriter &w) {
@@ -292,19 +314,23 @@ int build_plan(int C, int mode, PlanWriter &w) {
     else if (mode == HCMS_MODE_PIPELINED) alg1_plan(C, w);
     else if (mode == HCMS_MODE_INLINE) inline_plan(C, w);
     else if (mode == HCMS_MODE_SLOTS) slots_plan(C, w);
+    else if (mode == HCMS_MODE_FUSED) fused_plan(C, w);
     else lanes_plan(C, w);
     return w.n;
 }
 
 int plan_size(int C, int mode) {
     if (mode == HCMS_MODE_PIPELINED || mode == HCMS_MODE_SLOTS) return 7 * C + 5;
-    if (mode == HCMS_MODE_SERIAL || C == 1) return 3 * C;
+    if (mode == HCMS_MODE_SERIAL || mode == HCMS_MODE_FUSED || C == 1) return 3 * C;
     return mode == HCMS_MODE_INLINE ? 3 * C + 8 : 3 * C + 4;
 }
 
 // Rounds of attention workgroups: a launch of W workgroups on `slots`
 // concurrent slots takes ceil(W / slots) rounds; two lanes pool the chunks.
-int auto_mode(int S, int d, const int *sizes, int C, int n_cu) {
+// When pooling saves no round, the launches that can carry the neighbouring
+// chunks' copies (d = 128, bf16 storage) run the fused plan, the others the
+// inline one.
+int auto_mode(int S, int d, int dtype, const int *sizes, int C, int n_cu) {
     if (C == 1) return HCMS_MODE_SERIAL;
     const int64_t br = hcms::attention_queries_per_block(d);
     const int64_t slots = static_cast<int64_t>(n_cu) * hcms::attention_blocks_per_cu(d);
@@ -315,7 +341,8 @@ int auto_mode(int S, int d, const int *sizes, int C, int n_cu) {
         rounds += (wc + slots - 1) / slots;
         total += wc;
     }
-    return rounds > (total + slots - 1) / slots ? HCMS_MODE_LANES : HCMS_MODE_INLINE;
+    if (rounds > (total + slots - 1) / slots) return HCMS_MODE_LANES;
+    return d == 128 && dtype == HCMS_BF16 ? HCMS_MODE_FUSED : HCMS_MODE_INLINE;
 }
 
 // Saves the current device, switches to `dev`, restores on scope exit.
@@ -400,10 +427,10 @@ int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const
     const int m = *mode;
     if (!plan_mode(m) && m != HCMS_MODE_AUTO)
         return fail(HCMS_ERR_ARG, "mode %d is not serial (0), pipelined (1), inline (2), lanes (3), "
-                    "auto (4) or slots (5)", m);
+                    "auto (4), slots (5) or fused (6)", m);
     if (slotted && (m == HCMS_MODE_PIPELINED || m == HCMS_MODE_INLINE))
         return fail(HCMS_ERR_ARG, "mode %d packs chunk c + 2 before chunk c's attention is done; "
-                    "with two chunk slots use serial, lanes, slots or auto", m);
+                    "with two chunk slots use serial, lanes, slots, fused or auto", m);
     if ((st = check_dtype(dtype)) != HCMS_OK) return st;
     if ((st = check_dims(P, S, H, d, dtype)) != HCMS_OK) return st;
     if ((st = row_log2_units(d, dtype, log2u)) != HCMS_OK) return st;
@@ -416,7 +443,7 @@ int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const
     if ((m == HCMS_MODE_PIPELINED || m == HCMS_MODE_SLOTS) &&
         (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
         return fail(HCMS_ERR_ARG, "pipelined and slots modes need three distinct streams");
-    int r = m == HCMS_MODE_AUTO ? auto_mode(S, d, chunk_sizes, n_chunks, ctx->n_cu) : m;
+    int r = m == HCMS_MODE_AUTO ? auto_mode(S, d, dtype, chunk_sizes, n_chunks, ctx->n_cu) : m;
     // With two chunk slots the one-lane plan with few synchronisations is not
     // available; auto then runs the serial plan (lanes when it saves a round).
     if (slotted && m == HCMS_MODE_AUTO && r == HCMS_MODE_INLINE) r = HCMS_MODE_SERIAL;
@@ -434,12 +461,21 @@ int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const
     return HCMS_OK;
 }
 
+// A copy op of the fused plan waiting for the attention launch it rides in.
+struct RiderOp {
+    int kind, chunk, h0, hc;
+};
+
 // Issues the plan of `mode` (already resolved): RECORD / WAIT ops on the
 // context's events, kernel ops through launch(kind, chunk, h0, h_count, stream),
-// each bracketed by timing events while the context records.
-template <typename Launch>
+// each bracketed by timing events while the context records.  Ops on
+// HCMS_STREAM_IN_ATTENTION are collected and handed to the next ATTENTION op
+// through ride(chunk, h0, h_count, stream, riders, n, &riding); when that
+// launch cannot carry them (riding false) they are launched right after it.
+// A copy that rides reports the time of the launch it rode in.
+template <typename Launch, typename Ride>
 int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *main_stream,
-                 void *copy_stream, void *compute_stream, Launch &&launch) {
+                 void *copy_stream, void *compute_stream, Launch &&launch, Ride &&ride) {
     PlanWriter w{ctx->plan.data(), static_cast<int>(ctx->plan.size())};
     const int n_ops = build_plan(C, mode, w);
     ctx->last_mode = mode;
@@ -459,8 +495,18 @@ int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *m
     const bool timed = static_cast<int>(ctx->timed_chunks.size()) < ctx->timing_calls;
     const size_t call = ctx->timed_chunks.size();
     hipError_t e;
+    auto slot_of = [&](int kind, int c) {
+        return (call * 3 + (kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
+    };
+    RiderOp riders[2];
+    int n_riders = 0;
     for (int i = 0; i < n_ops; ++i) {
         const hcms_op &op = ctx->plan[i];
+        if (op.stream == HCMS_STREAM_IN_ATTENTION) {
+            if (n_riders == 2) return fail(HCMS_ERR_ARG, "more than two copies ride in one launch");
+            riders[n_riders++] = RiderOp{op.kind, op.chunk, offs[op.chunk], chunk_sizes[op.chunk]};
+            continue;
+        }
         hipStream_t s = streams[op.stream];
         if (op.kind == HCMS_OP_RECORD) {
             if ((e = hipEventRecord(event_of(op.event), s)) != hipSuccess)
@@ -473,14 +519,39 @@ int execute_plan(hcms_ctx *ctx, int mode, const int *chunk_sizes, int C, void *m
             continue;
         }
         const int c = op.chunk;
-        const size_t slot = (call * 3 + (op.kind - HCMS_OP_PACK)) * ctx->max_chunks + c;
-        if (timed && (e = hipEventRecord(ctx->t_begin[slot], s)) != hipSuccess)
-            return hip_fail(e, "hipEventRecord");
-        if ((e = launch(op.kind, c, offs[c], chunk_sizes[c], s)) != hipSuccess)
-            return hip_fail(e, "kernel launch");
-        if (timed && (e = hipEventRecord(ctx->t_end[slot], s)) != hipSuccess)
-            return hip_fail(e, "hipEventRecord");
+        const int n_ride = op.kind == HCMS_OP_ATTENTION ? n_riders : 0;
+        if (timed) {
+            if ((e = hipEventRecord(ctx->t_begin[slot_of(op.kind, c)], s)) != hipSuccess)
+                return hip_fail(e, "hipEventRecord");
+            for (int r = 0; r < n_ride; ++r)
+                if ((e = hipEventRecord(ctx->t_begin[slot_of(riders[r].kind, riders[r].chunk)], s)) !=
+                    hipSuccess)
+                    return hip_fail(e, "hipEventRecord");
+        }
+        bool riding = false;
+        if (n_ride > 0) e = ride(c, offs[c], chunk_sizes[c], s, riders, n_ride, &riding);
+        else e = launch(op.kind, c, offs[c], chunk_sizes[c], s);
+        if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        if (timed) {
+            if ((e = hipEventRecord(ctx->t_end[slot_of(op.kind, c)], s)) != hipSuccess)
+                return hip_fail(e, "hipEventRecord");
+            for (int r = 0; riding && r < n_ride; ++r)
+                if ((e = hipEventRecord(ctx->t_end[slot_of(riders[r].kind, riders[r].chunk)], s)) !=
+                    hipSuccess)
+                    return hip_fail(e, "hipEventRecord");
+        }
+        for (int r = 0; !riding && r < n_ride; ++r) {
+            const RiderOp &ro = riders[r];
+            if (timed && (e = hipEventRecord(ctx->t_begin[slot_of(ro.kind, ro.chunk)], s)) != hipSuccess)
+                return hip_fail(e, "hipEventRecord");
+            if ((e = launch(ro.kind, ro.chunk, ro.h0, ro.hc, s)) != hipSuccess)
+                return hip_fail(e, "kernel launch");
+            if (timed && (e = hipEventRecord(ctx->t_end[slot_of(ro.kind, ro.chunk)], s)) != hipSuccess)
+                return hip_fail(e, "hipEventRecord");
+        }
+        if (op.kind == HCMS_OP_ATTENTION) n_riders = 0;
     }
+    if (n_riders != 0) return fail(HCMS_ERR_ARG, "a riding copy has no attention launch after it");
     if (timed) ctx->timed_chunks.push_back(C);
     return ok();
 }
@@ -584,8 +655,38 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
         void *dst[1] = {f.o_seq};
         return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, beside(kind, c), s);
     };
+    auto ride = [&](int c, int h0, int hc, hipStream_t s, const RiderOp *riders, int n,
+                    bool *riding) -> hipError_t {
+        hcms::RidingCopy cp[2];
+        for (int r = 0; r < n; ++r) {
+            const RiderOp &ro = riders[r];
+            cp[r] = hcms::RidingCopy{};
+            cp[r].h0 = ro.h0;
+            cp[r].hc = ro.hc;
+            if (ro.kind == HCMS_OP_PACK) {
+                cp[r].n_tensors = 3;
+                cp[r].unpack = false;
+                const void *src[3] = {f.q_seq, f.k_seq, f.v_seq};
+                void *dst[3] = {at(f.q_hm, ro.chunk, ro.h0), at(f.k_hm, ro.chunk, ro.h0),
+                                at(f.v_hm, ro.chunk, ro.h0)};
+                for (int z = 0; z < 3; ++z) {
+                    cp[r].src[z] = src[z];
+                    cp[r].dst[z] = dst[z];
+                }
+            } else {
+                cp[r].n_tensors = 1;
+                cp[r].unpack = true;
+                cp[r].src[0] = at(f.o_hm, ro.chunk, ro.h0);
+                cp[r].dst[0] = f.o_seq;
+            }
+        }
+        return hcms::launch_attention_riding(
+            at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0), at(f.o_hm, c, h0),
+            f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr, f.S, hc, f.d, c_log2e,
+            f.dtype, cp, n, f.H, f.ctx->n_cu, riding, s);
+    };
     return execute_plan(f.ctx, mode, f.chunk_sizes, f.n_chunks, f.main_stream, f.copy_stream,
-                        f.compute_stream, launch);
+                        f.compute_stream, launch, ride);
 }
 
 // ---------------------------------------------------------------------------
@@ -832,7 +933,7 @@ int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
     if (n_chunks < 1) return fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be >= 1", n_chunks);
     if (!plan_mode(mode))
         return fail(HCMS_ERR_ARG, "mode %d has no fixed plan (serial 0, pipelined 1, inline 2, "
-                    "lanes 3, slots 5)", mode);
+                    "lanes 3, slots 5, fused 6)", mode);
     const int need = plan_size(n_chunks, mode);
     if (ops == nullptr) {
         ok();
@@ -845,8 +946,10 @@ int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
     return n;
 }
 
-int hcms_auto_mode(int S, int d, const int *chunk_sizes, int n_chunks, int n_cu) {
+int hcms_auto_mode(int S, int d, int dtype, const int *chunk_sizes, int n_chunks, int n_cu) {
     if (S < 0) return fail(HCMS_ERR_SHAPE, "S=%d must be >= 0", S);
+    const int st_dtype = check_dtype(dtype);
+    if (st_dtype != HCMS_OK) return st_dtype;
     if (d != 64 && d != 128) return fail(HCMS_ERR_SHAPE, "attention supports d = 64 or 128 (got %d)", d);
     if (n_cu < 1) return fail(HCMS_ERR_ARG, "n_cu=%d must be >= 1", n_cu);
     if (!chunk_sizes) return fail(HCMS_ERR_NULL, "chunk_sizes is NULL");
@@ -859,7 +962,7 @@ int hcms_auto_mode(int S, int d, const int *chunk_sizes, int n_chunks, int n_cu)
     int st = check_chunks(H, chunk_sizes, n_chunks);
     if (st != HCMS_OK) return st;
     ok();
-    return auto_mode(S, d, chunk_sizes, n_chunks, n_cu);
+    return auto_mode(S, d, dtype, chunk_sizes, n_chunks, n_cu);
 }
 
 int hcms_ctx_last_mode(const hcms_ctx *ctx) {
@@ -1150,8 +1253,15 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
         void *dst[3] = {dq_seq, dk_seq, dv_seq};
         return hcms::launch_unpack(src, dst, 3, S, H, h0, hc, log2u, beside(kind, c), s);
     };
+    // The backward launches carry no copies: the fused plan's copies run
+    // right after each chunk's backward launches.
+    auto ride = [&](int c, int h0, int hc, hipStream_t s, const RiderOp *, int,
+                    bool *riding) -> hipError_t {
+        *riding = false;
+        return launch(HCMS_OP_ATTENTION, c, h0, hc, s);
+    };
     return execute_plan(ctx, mode, chunk_sizes, n_chunks, main_stream, copy_stream, compute_stream,
-                        launch);
+                        launch, ride);
 }
 
 }  // extern "C"

@@ -60,7 +60,10 @@
 // Tails: loads go through buffer resources bounded by the head's tensor, so
 // query and key rows >= S read as zeros; such queries are not stored and such
 // keys get score -inf in the last block only.
+#include <algorithm>
+
 #include "attention_tiles.h"
+#include "copy_tiles.h"
 #include "hcms_internal.h"
 
 #ifndef HCMS_ATTN_NT128
@@ -650,17 +653,68 @@ struct Phase {
 
 }  // namespace dma
 
+// Copies that ride in an attention launch.  A launch of W attention
+// workgroups on n_cu CUs, one workgroup per CU, ends in a round that leaves
+// n_cu * ceil(W / n_cu) - W CUs idle.  The fused schedule appends that many
+// workgroups after the attention workgroups; the dispatcher hands them out
+// once every attention workgroup has a CU, so they fill the idle CUs of the
+// last round, and they move a neighbouring chunk's head rows (the next
+// chunk's pack, the previous chunk's unpack) meanwhile.  Rider workgroup r of
+// R takes copy blocks 2 r + half, 2 r + half + 2 R, ... over the jobs in
+// order, each half of its 512 threads one copy block at a time.
+struct RiderJob {
+    copy::PackPtrs p;
+    int64_t h0;
+    unsigned hc, n_tensors, blocks;  // blocks = copy::blocks_x * hc * n_tensors
+    int unpack;
+};
+
+struct Riders {
+    RiderJob job[2];
+    int64_t S, H;
+    unsigned n_jobs, bx;  // bx = copy::blocks_x(S, 4)
+    unsigned n_attn;      // attention workgroups in front of the riders
+};
+
+// Rows of d = 128 bf16 elements: 256 bytes = 16 units of 16 bytes.
+constexpr int kRiderLog2U = 4;
+static_assert((dma::kD * 2) >> 4 == 1 << kRiderLog2U, "rider rows are the attention rows");
+
+__device__ inline void run_riders(const Riders &r, unsigned rider, unsigned n_riders) {
+    const unsigned half = threadIdx.x >> 8, t = threadIdx.x & 255;
+    const unsigned total = r.job[0].blocks + (r.n_jobs > 1 ? r.job[1].blocks : 0u);
+    for (unsigned v = 2 * rider + half; v < total; v += 2 * n_riders) {
+        const bool second = v >= r.job[0].blocks;
+        const RiderJob &jb = second ? r.job[1] : r.job[0];
+        const unsigned w = second ? v - r.job[0].blocks : v;
+        const unsigned x = w % r.bx, rest = w / r.bx;
+        const unsigned j = rest % jb.hc, z = rest / jb.hc;
+        if (jb.unpack)
+            copy::copy_block<kRiderLog2U, true>(jb.p, r.S, r.H, jb.h0, x, j, z, t);
+        else
+            copy::copy_block<kRiderLog2U, false>(jb.p, r.S, r.H, jb.h0, x, j, z, t);
+    }
+}
+
+template <bool kRiders>
 __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_dma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
-    __bf16 *__restrict__ o, float *__restrict__ lse, int S, int n_qtiles, float c) {
+    __bf16 *__restrict__ o, float *__restrict__ lse, int S, int n_qtiles, float c, Riders riders) {
     using namespace dma;
+    if constexpr (kRiders) {
+        if (blockIdx.x >= riders.n_attn) {
+            run_riders(riders, blockIdx.x - riders.n_attn, gridDim.x - riders.n_attn);
+            return;
+        }
+    }
     constexpr int D = kD, KK = D / 16, DT = D / 32;
     __shared__ __attribute__((aligned(1024))) char lds[2 * kNB * kTileB];
     const char *const kbase = lds;                  // K buffer b at kbase + b * kTileB
     const char *const vbase = lds + kNB * kTileB;   // V buffer b at vbase + b * kTileB
 
     // XCD-aware tile order, as in attention_kernel.
-    const int nb = gridDim.x, b = blockIdx.x;
+    const int nb = kRiders ? static_cast<int>(riders.n_attn) : static_cast<int>(gridDim.x);
+    const int b = blockIdx.x;
     const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
     const int logical = xcd * per + min(xcd, rem) + (b >> 3);
     const int head = logical / n_qtiles;
@@ -911,9 +965,9 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, fl
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     if constexpr (D == dma::kD && sizeof(T) == 2 && kLdsDma) {
         static_assert(Sh::NT == 1 && Sh::WAVES == dma::kWaves, "the DMA kernel covers 256 queries in 8 waves");
-        attention_dma_kernel<<<static_cast<unsigned>(blocks), 64 * dma::kWaves, 0, stream>>>(
+        attention_dma_kernel<false><<<static_cast<unsigned>(blocks), 64 * dma::kWaves, 0, stream>>>(
             static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
-            static_cast<__bf16 *>(o), lse, S, n_qtiles, c);
+            static_cast<__bf16 *>(o), lse, S, n_qtiles, c, Riders{});
     } else {
         attention_kernel<D, T, Sh::WAVES, Sh::NT, Sh::PER_CU><<<static_cast<unsigned>(blocks), 64 * Sh::WAVES, 0, stream>>>(
             static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
@@ -939,6 +993,56 @@ hipError_t launch_attention(const void *q, const void *k, const void *v, void *o
     if (d == 64 && dtype == 1)
         return launch_typed<64, float>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_attention_riding(const void *q, const void *k, const void *v, void *o, float *lse,
+                                   int S, int n_heads, int d, float scale_log2e, int dtype,
+                                   const RidingCopy *copies, int n_copies, int64_t H, int n_cu,
+                                   bool *riding, hipStream_t stream) {
+    *riding = false;
+    const bool can = kLdsDma && d == dma::kD && dtype == 0 && S > 0 && n_heads > 0 && copies &&
+                     n_copies >= 1 && n_copies <= 2 && n_cu > 0 && copy::strided_span_fits(H);
+    if (!can) return launch_attention(q, k, v, o, lse, S, n_heads, d, scale_log2e, dtype, stream);
+    using Sh = Shape<dma::kD>;
+    const int64_t n_qtiles = (S + Sh::BR - 1) / Sh::BR;
+    const int64_t n_attn = n_qtiles * n_heads;
+    const int64_t idle = (n_cu - n_attn % n_cu) % n_cu;
+    Riders r{};
+    r.S = S;
+    r.H = H;
+    r.n_jobs = static_cast<unsigned>(n_copies);
+    const int64_t bx = copy::blocks_x(S, kRiderLog2U);
+    r.bx = static_cast<unsigned>(bx);
+    int64_t total = 0;
+    for (int i = 0; i < n_copies; ++i) {
+        const RidingCopy &cp = copies[i];
+        if (cp.n_tensors < 1 || cp.n_tensors > 3 || cp.hc < 1 || cp.h0 < 0 || cp.h0 + cp.hc > H)
+            return hipErrorInvalidValue;
+        RiderJob &jb = r.job[i];
+        for (int z = 0; z < cp.n_tensors; ++z) {
+            jb.p.src[z] = static_cast<const char *>(cp.src[z]);
+            jb.p.dst[z] = static_cast<char *>(cp.dst[z]);
+        }
+        jb.h0 = cp.h0;
+        jb.hc = static_cast<unsigned>(cp.hc);
+        jb.n_tensors = static_cast<unsigned>(cp.n_tensors);
+        jb.unpack = cp.unpack ? 1 : 0;
+        const int64_t blocks = bx * cp.hc * cp.n_tensors;
+        jb.blocks = static_cast<unsigned>(blocks);
+        total += blocks;
+    }
+    // Too few idle CUs, or more copy blocks than the 32-bit rider loop
+    // counts: the caller launches the copies itself.
+    if (idle < std::max(1, n_cu / 8) || total >= (int64_t{1} << 31) ||
+        n_attn + idle > 0x7fffffff)
+        return launch_attention(q, k, v, o, lse, S, n_heads, d, scale_log2e, dtype, stream);
+    r.n_attn = static_cast<unsigned>(n_attn);
+    attention_dma_kernel<true><<<static_cast<unsigned>(n_attn + idle), 64 * dma::kWaves, 0, stream>>>(
+        static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
+        static_cast<__bf16 *>(o), lse, S, static_cast<int>(n_qtiles), scale_log2e, r);
+    const hipError_t e = hipGetLastError();
+    if (e == hipSuccess) *riding = true;
+    return e;
 }
 
 }  // namespace hcms

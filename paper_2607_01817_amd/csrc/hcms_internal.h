@@ -49,6 +49,27 @@ hipError_t launch_attention(const void *q, const void *k, const void *v, void *o
                             int S, int n_heads, int d, float scale_log2e, int dtype,
                             hipStream_t stream);
 
+// A head-chunk copy that can ride in an attention launch: the arguments of
+// launch_pack (unpack = false) or launch_unpack (unpack = true) for rows of
+// d = 128 bf16 elements.
+struct RidingCopy {
+    const void *src[3];
+    void *dst[3];
+    int n_tensors;
+    bool unpack;
+    int64_t h0, hc;
+};
+// launch_attention, with up to two copies appended to the same launch as
+// extra workgroups after the attention workgroups, as many as the launch's
+// last round leaves CUs idle on n_cu CUs (H: heads of the [S][H][d] side).
+// Sets *riding when it did so; otherwise (not d = 128 bf16, fewer than
+// n_cu / 8 idle CUs, or copies too large) it launches only the attention and
+// the caller launches the copies after it.  A rider copy and the attention it
+// rides with must not touch the same bytes.
+hipError_t launch_attention_riding(const void *q, const void *k, const void *v, void *o, float *lse,
+                                   int S, int n_heads, int d, float scale_log2e, int dtype,
+                                   const RidingCopy *copies, int n_copies, int64_t H, int n_cu,
+                                   bool *riding, hipStream_t stream);
 // Backward of attention for `n_heads` consecutive heads (head-major buffers
 // starting at the chunk's first head; lse and delta [n_heads][S] fp32): one
 // query-parallel launch writing delta = <dO, O> and dq, then one key-parallel

@@ -43,7 +43,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert hcms.abi_version() == 1
+    assert hcms.abi_version() == 2
     names = {OK: "HCMS_OK", ENULL: "HCMS_ERR_NULL", ESHAPE: "HCMS_ERR_SHAPE",
              ECHUNKS: "HCMS_ERR_CHUNKS", EDTYPE: "HCMS_ERR_DTYPE", EALIGN: "HCMS_ERR_ALIGN",
              EHIP: "HCMS_ERR_HIP", EARG: "HCMS_ERR_ARG", EALIAS: "HCMS_ERR_ALIAS",
@@ -71,12 +71,27 @@ def test_default_chunks_matches_printed_table(lib):
 # ---------------------------------------------------------------------------
 def happens_before(ops):
     """Transitive happens-before over op indices from stream order and
-    record -> wait edges (a wait sees the latest record issued before it)."""
+    record -> wait edges (a wait sees the latest record issued before it).
+    An op on STREAM_IN_ATTENTION runs inside the launch of the next ATTENTION
+    op on the main stream: after the main-stream op before that launch and
+    before the main-stream op after it, unordered against the launch's
+    attention."""
     n = len(ops)
     edges = [set() for _ in range(n)]
     last_on_stream = {}
     last_record = {}
+    main = [i for i, op in enumerate(ops) if op[1] == hcms.STREAM_MAIN]
     for i, (kind, stream, chunk, event) in enumerate(ops):
+        if stream == hcms.STREAM_IN_ATTENTION:
+            host = next(j for j in main if j > i)
+            assert ops[host][0] == hcms.OP_ATTENTION, f"op {i} rides in no attention launch"
+            before = [j for j in main if j < host]
+            after = [j for j in main if j > host]
+            if before:
+                edges[before[-1]].add(i)
+            if after:
+                edges[i].add(after[0])
+            continue
         if stream in last_on_stream:
             edges[last_on_stream[stream]].add(i)
         last_on_stream[stream] = i
@@ -185,42 +200,75 @@ def test_lanes_plan_orders_every_dependency(lib, C):
     assert sum(op[0] in (hcms.OP_RECORD, hcms.OP_WAIT) for op in ops) == 4
 
 
+@pytest.mark.parametrize("C", [2, 3, 5, 10])
+def test_fused_plan_orders_every_dependency(lib, C):
+    ops = hcms.plan(C, hcms.MODE_FUSED)
+    assert len(ops) == 3 * C
+    pk, at, up = check_pipelined_dependencies(ops, C, hcms.STREAM_MAIN)
+    # One stream, no events.
+    assert all(op[0] not in (hcms.OP_RECORD, hcms.OP_WAIT) for op in ops)
+    assert {op[1] for op in ops} == {hcms.STREAM_MAIN, hcms.STREAM_IN_ATTENTION}
+    assert ops[pk[0]][1] == hcms.STREAM_MAIN and ops[up[C - 1]][1] == hcms.STREAM_MAIN
+    reach = happens_before(ops)
+    for c in range(C):
+        # Pack c + 1 and unpack c - 1 ride in attention c's launch: they
+        # overlap it and nothing else.
+        riders = [pk[c + 1]] if c + 1 < C else []
+        riders += [up[c - 1]] if c >= 1 else []
+        assert len(riders) == (c + 1 < C) + (c >= 1)
+        for r in riders:
+            assert ops[r][1] == hcms.STREAM_IN_ATTENTION
+            assert at[c] not in reach[r] and r not in reach[at[c]]
+            assert min(i for i in at.values() if i > r) == at[c]
+    # The two chunk slots can be reused.
+    check_slot_reuse(ops, C)
+
+
 def test_one_gpu_plans_with_one_chunk_are_serial(lib):
     assert hcms.plan(1, hcms.MODE_LANES) == hcms.plan(1, hcms.MODE_SERIAL)
     assert hcms.plan(1, hcms.MODE_INLINE) == hcms.plan(1, hcms.MODE_SERIAL)
+    assert hcms.plan(1, hcms.MODE_FUSED) == hcms.plan(1, hcms.MODE_SERIAL)
 
 
 # Rounds of attention workgroups, worked by hand for 256 CUs.  d = 128: 256
 # queries per workgroup, one per CU; d = 64: 128 queries, two per CU.
+# Where pooling saves no round, d = 128 bf16 runs the fused plan, the rest
+# the inline one.
 @pytest.mark.parametrize("S,d,sizes,want", [
-    (56160, 128, (2, 2, 1), "inline"),        # 220 tiles: 2+2+1 rounds = ceil(1100/256) = 5
-    (56160, 128, (1, 1, 1, 1, 1), "inline"),  # 5 x 1 = ceil(1100/256) = 5
+    (56160, 128, (2, 2, 1), "fused"),         # 220 tiles: 2+2+1 rounds = ceil(1100/256) = 5
+    (56160, 128, (1, 1, 1, 1, 1), "fused"),   # 5 x 1 = ceil(1100/256) = 5
     (32760, 128, (5, 5), "lanes"),            # 128 tiles: 3+3 = 6 > ceil(1280/256) = 5
     (32760, 128, (4, 3, 3), "lanes"),         # 2+2+2 = 6 > 5
     (100000, 128, (10, 10, 10, 10), "lanes"),  # 391 tiles: 4 x 16 = 64 > ceil(15640/256) = 62
-    (100000, 128, (14, 13, 13), "inline"),    # 22+20+20 = 62 = ceil(15640/256)
-    (65536, 128, (2, 2), "inline"),           # 256 tiles: 2+2 = 4 = ceil(1024/256)
+    (100000, 128, (14, 13, 13), "fused"),     # 22+20+20 = 62 = ceil(15640/256)
+    (65536, 128, (2, 2), "fused"),            # 256 tiles: 2+2 = 4 = ceil(1024/256)
     (4096, 128, (3, 3, 2), "lanes"),          # 16 tiles: 1+1+1 = 3 > ceil(128/256) = 1
     (4096, 64, (3, 3, 2), "lanes"),           # 32 tiles, 512 slots: 3 > 1
     (32768, 64, (4, 4), "inline"),            # 256 tiles, 512 slots: 2+2 = 4 = ceil(2048/512)
     (32768, 64, (3, 5), "lanes"),             # 2+3 = 5 > ceil(2048/512) = 4
     (56160, 128, (5,), "serial"),             # one chunk
-    (0, 128, (2, 2), "inline"),               # nothing to launch: 0 rounds either way
+    (0, 128, (2, 2), "fused"),                # nothing to launch: 0 rounds either way
 ])
 def test_auto_mode_by_rounds(lib, S, d, sizes, want):
-    modes = {"serial": hcms.MODE_SERIAL, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES}
+    modes = {"serial": hcms.MODE_SERIAL, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES,
+             "fused": hcms.MODE_FUSED}
     assert hcms.auto_mode(S, d, sizes, 256) == modes[want]
+    # fp32 storage takes the register-staged kernel, whose launches carry no
+    # copies: inline where bf16 would be fused.
+    fp32 = hcms.auto_mode(S, d, sizes, 256, dtype=hcms.FP32)
+    assert fp32 == (hcms.MODE_INLINE if want == "fused" else modes[want])
 
 
 def test_auto_mode_validation(lib):
     sizes = (ctypes.c_int * 2)(2, 2)
-    assert lib.hcms_auto_mode(-1, 128, sizes, 2, 256) == ESHAPE
-    assert lib.hcms_auto_mode(100, 96, sizes, 2, 256) == ESHAPE
-    assert lib.hcms_auto_mode(100, 128, sizes, 2, 0) == EARG
-    assert lib.hcms_auto_mode(100, 128, None, 2, 256) == ENULL
-    assert lib.hcms_auto_mode(100, 128, sizes, 0, 256) == ECHUNKS
+    assert lib.hcms_auto_mode(-1, 128, 0, sizes, 2, 256) == ESHAPE
+    assert lib.hcms_auto_mode(100, 96, 0, sizes, 2, 256) == ESHAPE
+    assert lib.hcms_auto_mode(100, 128, 2, sizes, 2, 256) == EDTYPE
+    assert lib.hcms_auto_mode(100, 128, 0, sizes, 2, 0) == EARG
+    assert lib.hcms_auto_mode(100, 128, 0, None, 2, 256) == ENULL
+    assert lib.hcms_auto_mode(100, 128, 0, sizes, 0, 256) == ECHUNKS
     bad = (ctypes.c_int * 2)(2, 0)
-    assert lib.hcms_auto_mode(100, 128, bad, 2, 256) == ECHUNKS
+    assert lib.hcms_auto_mode(100, 128, 0, bad, 2, 256) == ECHUNKS
     assert lib.hcms_ctx_last_mode(None) == ENULL
     assert lib.hcms_ctx_num_cu(None) == ENULL
 
@@ -239,7 +287,8 @@ def test_plan_errors(lib):
     assert lib.hcms_plan(0, 1, None, 0) == ECHUNKS
     assert lib.hcms_plan(2, 7, None, 0) == EARG
     assert lib.hcms_plan(2, hcms.MODE_AUTO, None, 0) == EARG   # no fixed plan
-    assert lib.hcms_plan(2, 6, None, 0) == EARG
+    assert lib.hcms_plan(2, 8, None, 0) == EARG
+    assert lib.hcms_plan(2, hcms.MODE_FUSED, None, 0) == 6
     assert lib.hcms_plan(2, hcms.MODE_SLOTS, None, 0) == 19
     assert lib.hcms_plan(2, hcms.MODE_INLINE, None, 0) == 14
     assert lib.hcms_plan(2, hcms.MODE_LANES, None, 0) == 10

@@ -173,7 +173,7 @@ def test_backward_pipeline_bitwise_across_modes_and_chunkings(hcms, name):
     ctx = hcms.Context(max_chunks=16)
     for sizes in w.chunkings:
         for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED, hcms.MODE_INLINE, hcms.MODE_LANES,
-                     hcms.MODE_AUTO):
+                     hcms.MODE_FUSED, hcms.MODE_AUTO):
             ws = [torch.empty_like(hm[0]) for _ in range(4)]
             lse2 = torch.empty_like(lse)
             o2 = ctx.forward(qs, ks, vs, w.P, w.scale, sizes, mode=mode, workspaces=ws, lse=lse2)

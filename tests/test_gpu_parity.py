@@ -244,7 +244,7 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
     ctx = hcms.Context(max_chunks=16)
     for sizes in _chunkings(w):
         for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED, hcms.MODE_INLINE, hcms.MODE_LANES,
-                     hcms.MODE_AUTO):
+                     hcms.MODE_FUSED, hcms.MODE_AUTO):
             out = ctx.forward(qd, kd, vd, w.P, w.scale, sizes, mode=mode)
             assert torch.equal(bits(out), bits(ref)), (name, sizes, mode)
     out = ctx.forward(qd, kd, vd, w.P, w.scale, w.chunkings[-1]).float().cpu()
@@ -254,6 +254,36 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
                                          head_major_np(v, h), w.scale, rows[h])
         got = out[torch.from_numpy(rows[h]), h].double().numpy()
         check_attention_rows(got, want, f"forward {name} head {h}")
+    ctx.close()
+
+
+@pytest.mark.parametrize("S,H,P,sizes_list", [
+    (1000, 6, 8, [(3, 2, 1), (1,) * 6, (2, 4)]),      # ragged: 4 query tiles, 16 key blocks
+    (4096, 8, 8, [(1,) * 8, (7, 1)]),                 # 16 tiles per head: many idle CUs
+    (56160, 5, 8, [(2, 2, 1), (1,) * 5, (4, 1)]),     # Wan-P8: 440 / 220 / 880 workgroups
+])
+def test_fused_forward_bitwise_equals_serial(hcms, S, H, P, sizes_list):
+    """The fused plan (the next chunk's pack and the previous chunk's unpack
+    riding in each attention launch) gives the serial plan's bits, with the
+    workspaces and the output poisoned first, so a copy in the wrong launch
+    would leave poison."""
+    g = torch.Generator().manual_seed(S + H)
+    q, k, v = (torch.randn(S, H, 128, generator=g).to(torch.bfloat16).cuda() for _ in range(3))
+    scale = 128 ** -0.5
+    ctx = hcms.Context(max_chunks=8)
+    ref = ctx.forward(q, k, v, P, scale, (H,), mode=hcms.MODE_SERIAL).clone()
+    for sizes in sizes_list:
+        log(f"[fused] S={S} H={H} chunks={sizes}")
+        ws = ctx.workspaces(S, H, 128, q.dtype)
+        out = torch.empty_like(q)
+        for t in (*ws, out):
+            _fill_bits(t)
+        torch.cuda.synchronize()
+        ctx.forward(q, k, v, P, scale, sizes, mode=hcms.MODE_FUSED, out=out, workspaces=ws)
+        seen = out.clone()
+        torch.cuda.synchronize()
+        assert ctx.last_mode == hcms.MODE_FUSED
+        assert torch.equal(bits(seen), bits(ref)), sizes
     ctx.close()
 
 
@@ -291,7 +321,7 @@ def _delay(stream, cycles=40_000_000):
         torch.cuda._sleep(cycles)
 
 
-@pytest.mark.parametrize("mode", ["pipelined", "inline", "lanes"])
+@pytest.mark.parametrize("mode", ["pipelined", "inline", "lanes", "fused"])
 @pytest.mark.parametrize("late", ["copy", "compute", "main"])
 def test_pipelined_respects_events_under_delay(hcms, late, mode):
     """Poison the workspaces and the output, delay one stream with a bounded
@@ -320,7 +350,8 @@ def test_pipelined_respects_events_under_delay(hcms, late, mode):
     else:
         torch.cuda.synchronize()
         _delay(ctx.copy_stream if late == "copy" else ctx.compute_stream)
-    m = {"pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES}[mode]
+    m = {"pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES,
+         "fused": hcms.MODE_FUSED}[mode]
     ctx.forward(q_in, k, v, w.P, w.scale, sizes, mode=m, out=out)
     seen = out.clone()            # on the main stream, no host sync in between
     torch.cuda.synchronize()
@@ -332,10 +363,11 @@ def test_timing_api_reports_every_chunk(hcms):
     w = inputs.WORKLOADS["small"]
     q, k, v = (x.cuda() for x in workload_inputs("small"))
     ctx = hcms.Context(max_chunks=8)
-    ctx.set_timing(2)
-    for _ in range(3):   # the third call is past the record and not timed
-        ctx.forward(q, k, v, w.P, w.scale, (3, 3, 2))
-    for kind in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK):
-        ms = ctx.kernel_ms(kind)
-        assert len(ms) == 6 and all(0 < x < 1000 for x in ms), (kind, ms)
+    for mode in (hcms.MODE_AUTO, hcms.MODE_FUSED):
+        ctx.set_timing(2)
+        for _ in range(3):   # the third call is past the record and not timed
+            ctx.forward(q, k, v, w.P, w.scale, (3, 3, 2), mode=mode)
+        for kind in (hcms.OP_PACK, hcms.OP_ATTENTION, hcms.OP_UNPACK):
+            ms = ctx.kernel_ms(kind)
+            assert len(ms) == 6 and all(0 < x < 1000 for x in ms), (mode, kind, ms)
     ctx.close()

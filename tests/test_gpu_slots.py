@@ -10,7 +10,7 @@ from tests.test_gpu_parity import _delay, _fill_bits
 
 pytestmark = pytest.mark.gpu
 
-SLOT_MODES = ("serial", "lanes", "slots", "auto")
+SLOT_MODES = ("serial", "lanes", "slots", "fused", "auto")
 
 
 def _mode(hcms, name):
@@ -25,7 +25,7 @@ def test_forward_slots_bitwise_equals_full_workspaces(hcms, name):
     ref = bits(ctx.forward(q, k, v, w.P, w.scale, (w.H,), mode=hcms.MODE_SERIAL).cpu())
     chunkings = w.chunkings if name == "small" else ((2, 2, 1), (1, 1, 1, 1, 1))
     for sizes in chunkings:
-        for m in SLOT_MODES if name == "small" else ("slots", "auto"):
+        for m in SLOT_MODES if name == "small" else ("slots", "fused", "auto"):
             log(f"[slots] {name} chunks={sizes} mode={m}")
             out = ctx.forward_slots(q, k, v, w.P, w.scale, sizes, mode=_mode(hcms, m))
             torch.cuda.synchronize()
@@ -51,7 +51,7 @@ def test_forward_slots_rejects_modes_that_break_slot_reuse(hcms):
     ctx.close()
 
 
-@pytest.mark.parametrize("mode", ["slots", "lanes"])
+@pytest.mark.parametrize("mode", ["slots", "lanes", "fused"])
 @pytest.mark.parametrize("late", ["copy", "compute", "main"])
 def test_forward_slots_respects_slot_reuse_under_delay(hcms, late, mode):
     """Poison the slots and the output, delay one stream with a bounded spin
