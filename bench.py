@@ -36,7 +36,8 @@ from paper_2607_01817_amd import inputs  # noqa: E402
 
 MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16: 256 CU x 2.4 GHz x 4096 FLOP/clk
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
-ATTENTION_SRC = os.path.join(ROOT, "paper_2607_01817_amd", "csrc", "attention.hip")
+ATTENTION_SRCS = [os.path.join(ROOT, "paper_2607_01817_amd", "csrc", f)
+                  for f in ("attention.hip", "copy_tiles.h")]
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attention_traffic_wan_p8.json")
 
 
@@ -70,23 +71,25 @@ def time_region(fn, reps: int, stream=None) -> list[float]:
     return out
 
 
-def measured_traffic(workload: str, chunks) -> float | None:
-    """HBM bytes per attention launch from the committed rocprofv3 counter
-    record (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or
-    None when there is no record for this workload or the kernel source has
-    changed since the counters were taken."""
+def measured_traffic(workload: str, chunks, plan: str) -> float | None:
+    """HBM bytes per attention launch of `plan` from the committed rocprofv3
+    counter record (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known
+    size), or None when there is no record for this workload and plan or the
+    kernel sources have changed since the counters were taken."""
     import hashlib
     try:
         with open(TRAFFIC_RECORD) as f:
             rec = json.load(f)
-        with open(ATTENTION_SRC, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
+        h = hashlib.sha256()
+        for src in ATTENTION_SRCS:
+            with open(src, "rb") as f:
+                h.update(f.read())
     except (OSError, ValueError):
         return None
-    if rec.get("attention_source_sha256") != sha or rec.get("workload") != workload \
-            or list(rec.get("chunks", [])) != list(chunks):
+    if rec.get("source_sha256") != h.hexdigest() or rec.get("workload") != workload \
+            or list(rec.get("chunks", [])) != list(chunks) or plan not in rec.get("plans", {}):
         return None
-    return float(rec["hbm_bytes_per_launch"])
+    return float(rec["plans"][plan]["hbm_bytes_per_launch"])
 
 
 def copy_calibration(dev):
@@ -465,7 +468,7 @@ def main():
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": measured_traffic(w.name, sizes),
+            "traffic": measured_traffic(w.name, sizes, plan),
             "kernel": "attention_dma_kernel (d = 128, bf16)" + (
                 "; in the fused plan each launch also carries the neighbouring chunks' copies "
                 "on the CUs its last round leaves idle (attention_dma_kernel<true>)"
