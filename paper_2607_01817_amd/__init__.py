@@ -486,7 +486,7 @@ class Context:
                       out: torch.Tensor | None = None, slots=None, main_stream=None) -> torch.Tensor:
         """:meth:`forward` with two chunk slots (``slots``: four
         [2][slot_heads][S][d] buffers, slot_heads >= every chunk) instead of
-        full head-major workspaces; modes serial, lanes, slots or auto."""
+        full head-major workspaces; modes serial, lanes, slots, fused or auto."""
         for t, n in ((q_seq, "q_seq"), (k_seq, "k_seq"), (v_seq, "v_seq")):
             _dev(t, n)
         if not (q_seq.shape == k_seq.shape == v_seq.shape) or q_seq.dim() != 3:
