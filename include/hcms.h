@@ -239,9 +239,12 @@ typedef struct hcms_op {
  * that chunk c + 2 can reuse chunk c's workspace slot (the input layout of one
  * chunk and the output layout of another beside a chunk's attention,
  * Sec. 3.5).  The host issues every record before any wait on it.
- * Fused mode runs on the main stream alone, with no events: it packs chunk
- * 0; then, for every c, the pack of chunk c + 1 (c + 1 < C) and the unpack of
- * chunk c - 1 (c >= 1) are issued on HCMS_STREAM_IN_ATTENTION, which means
+ * Fused mode is the overlap of Sec. 3.5 (the input layout of chunk c + 1 and
+ * the output layout of chunk c - 1 beside the attention of chunk c) with the
+ * dependencies of Alg. 1 kept by stream order alone, so it needs no events.
+ * It runs on the main stream: it packs chunk 0; then, for every c, the pack
+ * of chunk c + 1 (c + 1 < C) and the unpack of chunk c - 1 (c >= 1) are
+ * issued on HCMS_STREAM_IN_ATTENTION, which means
  * that they run inside the launch of the ATTENTION op that follows them, as
  * workgroups dispatched after all of that launch's attention workgroups, on
  * the CUs its last round leaves idle; after the last attention the main
