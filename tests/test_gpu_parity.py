@@ -261,7 +261,8 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
     (1000, 6, 8, [(3, 2, 1), (1,) * 6, (2, 4)]),      # ragged: 4 query tiles, 16 key blocks
     (4096, 8, 8, [(1,) * 8, (7, 1)]),                 # 16 tiles per head: many idle CUs
     (56160, 5, 8, [(2, 2, 1), (1,) * 5, (4, 1)]),     # Wan-P8: 440 / 220 / 880 workgroups
-])
+    (64000, 2, 8, [(1, 1)]),                          # 250 workgroups: 6 idle CUs, too few to
+])                                                    # carry the copies; they run after it
 def test_fused_forward_bitwise_equals_serial(hcms, S, H, P, sizes_list):
     """The fused plan (the next chunk's pack and the previous chunk's unpack
     riding in each attention launch) gives the serial plan's bits, with the
