@@ -437,6 +437,17 @@ def main():
     unpack_ms = ctx.kernel_ms(hcms.OP_UNPACK)
     ctx.set_timing(0)
 
+    # ---- under a plan whose launches also carry copies, the same steps once
+    # more in the serial plan: the attention launch on its own ----
+    plain_ms = None
+    if plan == "fused":
+        ctx.set_timing(args.steps)
+        for _ in range(args.steps):
+            step(m=hcms.MODE_SERIAL)
+        torch.cuda.synchronize()
+        plain_ms = ctx.kernel_ms(hcms.OP_ATTENTION)
+        ctx.set_timing(0)
+
     tflops = w.flops / (ms_per_step * 1e-3) / 1e12
     C = len(sizes)
     launch_flops = [4.0 * w.S * w.S * sizes[i % C] * w.d for i in range(len(attn_ms))]
@@ -479,6 +490,16 @@ def main():
                           f"({ms_per_step_events:.4f} ms per step with the events)",
         },
     }
+    if plain_ms:
+        plain = sum(launch_flops) / (sum(plain_ms) * 1e-3) / 1e12
+        result["roofline"]["plain_launch"] = {
+            "achieved": round(plain, 2),
+            "frac": round(plain / MFMA_BF16_PEAK_TFLOPS, 4),
+            "avg_launch_ms": round(statistics.mean(plain_ms), 4),
+            "note": "the same launches without riding copies (serial plan, a third pass of the "
+                    "steps): the attention kernel's own roofline; the copies riding in the fused "
+                    "launches take part of the power the attention would otherwise clock on",
+        }
 
     if not args.no_extras:
         es = w.elem_bytes
