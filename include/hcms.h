@@ -181,7 +181,9 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
 #define HCMS_MODE_PIPELINED 1  /* Alg. 1: copy stream + compute stream + events */
 #define HCMS_MODE_INLINE 2     /* one lane, four synchronisations (see hcms_plan) */
 #define HCMS_MODE_LANES 3      /* chunks alternate between two streams (see hcms_plan) */
-#define HCMS_MODE_AUTO 4       /* hcms_forward only: fused, inline or lanes, per hcms_auto_mode */
+#define HCMS_MODE_AUTO 4       /* the mode hcms_auto_mode picks (fused, inline, lanes or serial);
+                                  hcms_forward, hcms_forward_slots and hcms_backward take it,
+                                  hcms_plan does not (no fixed plan) */
 #define HCMS_MODE_SLOTS 5      /* Alg. 1's streams, copies interleaved so slots can be reused */
 #define HCMS_MODE_FUSED 6      /* one stream; neighbouring copies ride in each attention launch */
 

@@ -128,6 +128,30 @@ def _dev(t: torch.Tensor, name: str):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _expect(t: torch.Tensor, shape, dtype, name: str):
+    """Shape and dtype of a tensor the C ABI only sees as a pointer (the
+    callers check every size first and the devices after, so that a wrong
+    size never reaches a launch)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"{name} must be {list(shape)} of {dtype} "
+                         f"(got {list(t.shape)} of {t.dtype})")
+
+
+def _devs(named):
+    for t, n in named:
+        _dev(t, n)
+
+
+def _table_rows(grid, axis_pairs) -> int:
+    g, na = _ints(grid)
+    p, npairs = _ints(axis_pairs)
+    if na != npairs:
+        raise ValueError("one pair count per grid axis")
+    return _check(load().hcms_rope_table_entries(g, p, na))
+
+
 def _stream(s) -> ctypes.c_void_p:
     if s is None:
         s = torch.cuda.current_stream()
@@ -299,6 +323,7 @@ def attention_backward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: t
         sizes, n, _dtype(q), _stream(stream)))
     return dq, dk, dv
 
+
 def linear(x: torch.Tensor, w: torch.Tensor, out: torch.Tensor | None = None,
            stream=None) -> torch.Tensor:
     """Projection GEMM: x [M][K] times w [N][K] (weight stored [out][in]),
@@ -341,23 +366,27 @@ def qkv_projection(x: torch.Tensor, w_qkv: torch.Tensor, H: int, d: int,
     """x [S][D] times w_qkv [3 H d][D]: (q, k, v) [S][H][d] each, the query
     and key pairs rotated by ``table`` (from :func:`rope_table` on the same
     grid and axis_pairs) when it is given."""
-    _dev(x, "x")
-    _dev(w_qkv, "w_qkv")
+    if x.dim() != 2:
+        raise ValueError("x must be [S][D]")
     S, D = x.shape
+    _expect(x, (S, D), x.dtype, "x")
+    _expect(w_qkv, (3 * H * d, D), x.dtype, "w_qkv")
     if out is None:
         out = tuple(torch.empty((S, H, d), dtype=x.dtype, device=x.device) for _ in range(3))
-    for t in out:
-        _dev(t, "out")
-        if t.shape != (S, H, d) or t.dtype != x.dtype:
-            raise ValueError("outputs must be [S][H][d] of the input dtype")
+    if len(out) != 3:
+        raise ValueError("out must be three [S][H][d] tensors")
+    for t, n in zip(out, ("q_seq", "k_seq", "v_seq")):
+        _expect(t, (S, H, d), x.dtype, n)
     g = p = None
     na = 0
     tp = None
     if table is not None:
+        _expect(table, (_table_rows(grid, axis_pairs), 2), torch.float32, "table")
         _dev(table, "table")
         g, na = _ints(grid)
         p, _ = _ints(axis_pairs)
         tp = table.data_ptr()
+    _devs(((x, "x"), (w_qkv, "w_qkv"), *zip(out, ("q_seq", "k_seq", "v_seq"))))
     _check(load().hcms_qkv_projection(x.data_ptr(), w_qkv.data_ptr(), tp, g, p, na,
                                       out[0].data_ptr(), out[1].data_ptr(), out[2].data_ptr(),
                                       S, D, H, d, _dtype(x), _stream(stream)))
@@ -487,21 +516,23 @@ class Context:
         """:meth:`forward` with two chunk slots (``slots``: four
         [2][slot_heads][S][d] buffers, slot_heads >= every chunk) instead of
         full head-major workspaces; modes serial, lanes, slots, fused or auto."""
+        if q_seq.dim() != 3:
+            raise ValueError("q_seq must be [S][H][d]")
         for t, n in ((q_seq, "q_seq"), (k_seq, "k_seq"), (v_seq, "v_seq")):
-            _dev(t, n)
-        if not (q_seq.shape == k_seq.shape == v_seq.shape) or q_seq.dim() != 3:
-            raise ValueError("q_seq, k_seq, v_seq must all be [S][H][d]")
+            _expect(t, q_seq.shape, q_seq.dtype, n)
         S, H, d = q_seq.shape
         if out is None:
             out = torch.empty_like(q_seq)
-        _dev(out, "out")
+        _expect(out, q_seq.shape, q_seq.dtype, "out")
         if slots is None:
             slots = self.slot_workspaces(S, max(int(c) for c in chunk_sizes), d, q_seq.dtype)
+        if len(slots) != 4 or slots[0].dim() != 4:
+            raise ValueError("slots must be four [2][slot_heads][S][d] tensors")
         slot_heads = slots[0].shape[1]
         for t in slots:
-            _dev(t, "slot workspace")
-            if t.shape != (2, slot_heads, S, d) or t.dtype != q_seq.dtype:
-                raise ValueError("slot workspaces must be [2][slot_heads][S][d] of the input dtype")
+            _expect(t, (2, slot_heads, S, d), q_seq.dtype, "slot workspace")
+        _devs(((q_seq, "q_seq"), (k_seq, "k_seq"), (v_seq, "v_seq"), (out, "out"),
+               *((t, "slot workspace") for t in slots)))
         sizes, n = _ints(chunk_sizes)
         _check(load().hcms_forward_slots(
             self._h, q_seq.data_ptr(), k_seq.data_ptr(), v_seq.data_ptr(), out.data_ptr(),
@@ -519,8 +550,33 @@ class Context:
         (QKV projection with the rotation, :meth:`forward`, output projection).
         ``buffers`` (q_seq, k_seq, v_seq, o_seq, each [S][H][d]) are kept
         between calls with the same shape."""
-        _dev(x, "x")
+        if x.dim() != 2:
+            raise ValueError("x must be [S][D]")
         S, D = x.shape
+        _expect(x, (S, D), x.dtype, "x")
+        _expect(w_qkv, (3 * H * d, D), x.dtype, "w_qkv")
+        _expect(w_o, (D, H * d), x.dtype, "w_o")
+        if out is not None:
+            _expect(out, (S, D), x.dtype, "out")
+        if buffers is not None:
+            if len(buffers) != 4:
+                raise ValueError("buffers must be q_seq, k_seq, v_seq, o_seq")
+            for b, n in zip(buffers, ("q_seq", "k_seq", "v_seq", "o_seq")):
+                _expect(b, (S, H, d), x.dtype, n)
+        g = p = None
+        na = 0
+        tp = None
+        if table is not None:
+            _expect(table, (_table_rows(grid, axis_pairs), 2), torch.float32, "table")
+            _dev(table, "table")
+            g, na = _ints(grid)
+            p, _ = _ints(axis_pairs)
+            tp = table.data_ptr()
+        _devs(((x, "x"), (w_qkv, "w_qkv"), (w_o, "w_o")))
+        if out is not None:
+            _dev(out, "out")
+        for b in buffers or ():
+            _dev(b, "buffer")
         if out is None:
             out = torch.empty((S, D), dtype=x.dtype, device=x.device)
         if buffers is None:
@@ -531,13 +587,6 @@ class Context:
                 self._lbuf_key = key
             buffers = self._lbuf
         ws = self.workspaces(S, H, d, x.dtype)
-        g = p = None
-        na = 0
-        tp = None
-        if table is not None:
-            g, na = _ints(grid)
-            p, _ = _ints(axis_pairs)
-            tp = table.data_ptr()
         sizes, n = _ints(chunk_sizes)
         _check(load().hcms_layer_forward(
             self._h, x.data_ptr(), w_qkv.data_ptr(), w_o.data_ptr(), tp, g, p, na,

@@ -392,6 +392,67 @@ def test_binding_rejects_cpu_tensors(lib):
         hcms.attention(x.permute(1, 0, 2), x.permute(1, 0, 2), x.permute(1, 0, 2), 0.1)
 
 
+def test_binding_checks_sizes_before_any_launch(lib):
+    """The C ABI sees raw pointers, so the binding checks every tensor's
+    shape and dtype before its device: an undersized or mistyped output,
+    buffer or weight raises ValueError naming it, on the CPU, before the
+    library is called (the methods run on a stand-in context object that has
+    no library handle, so reaching the call would raise something else)."""
+    import torch
+    bf = torch.bfloat16
+    S, H, d, D, P = 24, 2, 64, 128, 2
+    grid, pairs = (2, 3, 4), (12, 10, 10)
+    n_table = hcms.load().hcms_rope_table_entries(_ints(grid), _ints(pairs), 3)
+    x = torch.zeros(S, D, dtype=bf)
+    w_qkv = torch.zeros(3 * H * d, D, dtype=bf)
+    w_o = torch.zeros(D, H * d, dtype=bf)
+    table = torch.zeros(n_table, 2)
+    seq = [torch.zeros(S, H, d, dtype=bf) for _ in range(4)]
+
+    def layer(**kw):
+        a = dict(x=x, w_qkv=w_qkv, w_o=w_o, P=P, H=H, d=d, scale=0.125, chunk_sizes=(1, 1),
+                 table=table, grid=grid, axis_pairs=pairs, out=torch.zeros(S, D, dtype=bf),
+                 buffers=seq)
+        a.update(kw)
+        return hcms.Context.layer_forward(object(), **a)
+
+    for kw, name in ((dict(w_qkv=w_qkv[:-1]), "w_qkv"), (dict(w_o=w_o[:, :-8]), "w_o"),
+                     (dict(w_o=w_o.float()), "w_o"), (dict(out=torch.zeros(S - 1, D, dtype=bf)), "out"),
+                     (dict(buffers=seq[:3] + [torch.zeros(S, H, d - 8, dtype=bf)]), "o_seq"),
+                     (dict(buffers=[seq[0].float()] + seq[1:]), "q_seq"),
+                     (dict(table=table[:-1]), "table"), (dict(table=table.double()), "table")):
+        with pytest.raises(ValueError, match=name):
+            layer(**kw)
+    with pytest.raises(ValueError, match="GPU tensor"):   # every size right: the device check
+        layer()
+
+    def qkv(**kw):
+        a = dict(x=x, w_qkv=w_qkv, H=H, d=d, table=table, grid=grid, axis_pairs=pairs,
+                 out=tuple(seq[:3]))
+        a.update(kw)
+        return hcms.qkv_projection(**a)
+
+    for kw, name in ((dict(w_qkv=torch.zeros(3 * H * d, D - 64, dtype=bf)), "w_qkv"),
+                     (dict(out=(seq[0], seq[1], seq[2][:-1])), "v_seq"),
+                     (dict(table=table[1:]), "table")):
+        with pytest.raises(ValueError, match=name):
+            qkv(**kw)
+
+    slots = [torch.zeros(2, 1, S, d, dtype=bf) for _ in range(4)]
+
+    def fslots(**kw):
+        a = dict(q_seq=seq[0], k_seq=seq[1], v_seq=seq[2], P=P, scale=0.125, chunk_sizes=(1, 1),
+                 out=seq[3], slots=slots)
+        a.update(kw)
+        return hcms.Context.forward_slots(object(), **a)
+
+    for kw, name in ((dict(out=torch.zeros(S, H, d - 8, dtype=bf)), "out"),
+                     (dict(out=seq[3].float()), "out"), (dict(v_seq=seq[2].float()), "v_seq"),
+                     (dict(slots=slots[:3] + [torch.zeros(2, 1, S - 2, d, dtype=bf)]), "slot")):
+        with pytest.raises(ValueError, match=name):
+            fslots(**kw)
+
+
 def test_training_forward_and_backward_validation(lib):
     sizes = (ctypes.c_int * 2)(2, 2)
     E, F, G_, H_ = 0x50000000, 0x60000000, 0x70000000, 0x80000000

@@ -206,14 +206,14 @@ def _delay(stream, cycles=40_000_000):
         torch.cuda._sleep(cycles)
 
 
-@pytest.mark.parametrize("mode", ["pipelined", "inline", "lanes"])
+@pytest.mark.parametrize("mode", ["pipelined", "inline", "lanes", "fused", "auto"])
 @pytest.mark.parametrize("late", ["copy", "compute", "main"])
 def test_backward_pipeline_respects_events_under_delay(hcms, late, mode):
     """Poison the backward workspaces and outputs, delay one stream with a
     bounded spin kernel, read the gradients on the main stream right after the
     call returns: a missing wait would expose poison or stale values."""
     w, qs, ks, vs, dos = _seq_case("small")
-    m = {"pipelined": hcms.MODE_PIPELINED, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES}[mode]
+    m = getattr(hcms, "MODE_" + mode.upper())
     sizes = (3, 3, 2)
     ctx = hcms.Context(max_chunks=8)
     ws = [torch.empty((w.H, w.S, w.d), dtype=qs.dtype, device="cuda") for _ in range(4)]

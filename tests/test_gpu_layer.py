@@ -143,8 +143,10 @@ def _oracle_layer(oracle_mod, w, x, w_qkv, w_o, rows):
                                 oracle_mod.attention_head, rows)
 
 
-@pytest.mark.parametrize("name", ["layer_small", "layer_ragged", "layer_fp32"])
+@pytest.mark.parametrize("name", ["layer_small", "layer_ragged", "layer_fp32", "layer_wan_p8"])
 def test_layer_forward_matches_oracle(hcms, oracle_mod, name):
+    """Whole layer against the oracle (every token of the small layers; 32
+    sampled tokens of the Wan2.2-shaped share, S = 56160, D = 5120)."""
     w = inputs.LAYERS[name]
     log(f"[layer] {name} S={w.S} H={w.H} d={w.d} D={w.D}")
     x, w_qkv, w_o = inputs.make_layer(w)

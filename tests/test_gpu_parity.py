@@ -231,8 +231,10 @@ def test_attention_bitwise_chunk_invariance(hcms, name):
         assert torch.equal(bits(out), bits(ref)), (name, sizes)
 
 
-@pytest.mark.parametrize("name", ["tiny", "small", "wan_p4", "wan_p8"])
-def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
+FORWARD_MODES = ("serial", "pipelined", "inline", "lanes", "slots", "fused", "auto")
+
+
+def _forward_modes_case(hcms, oracle_mod, name, rows_per_head):
     """hcms_forward (pack, attention, unpack on two streams) equals attention
     on the torch-transposed inputs, bitwise, for every chunking and mode, and
     matches the oracle on sampled rows of the [S][H][d] output."""
@@ -242,19 +244,39 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
     qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
     ref = hcms.attention(_cuda_hm(q), _cuda_hm(k), _cuda_hm(v), w.scale).permute(1, 0, 2).contiguous()
     ctx = hcms.Context(max_chunks=16)
+    out = torch.empty_like(qd)
     for sizes in _chunkings(w):
-        for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED, hcms.MODE_INLINE, hcms.MODE_LANES,
-                     hcms.MODE_FUSED, hcms.MODE_AUTO):
-            out = ctx.forward(qd, kd, vd, w.P, w.scale, sizes, mode=mode)
+        for mode in FORWARD_MODES:
+            log(f"    chunks={sizes} mode={mode}")
+            _fill_bits(out)
+            ctx.forward(qd, kd, vd, w.P, w.scale, sizes, mode=getattr(hcms, "MODE_" + mode.upper()),
+                        out=out)
             assert torch.equal(bits(out), bits(ref)), (name, sizes, mode)
+    del ref
     out = ctx.forward(qd, kd, vd, w.P, w.scale, w.chunkings[-1]).float().cpu()
-    rows = inputs.sample_rows(w, 64)
+    ctx.close()
+    del qd, kd, vd
+    rows = inputs.sample_rows(w, rows_per_head)
+    worst = (0.0, 0.0)
     for h in range(w.H):
         want = oracle_mod.attention_head(head_major_np(q, h), head_major_np(k, h),
                                          head_major_np(v, h), w.scale, rows[h])
         got = out[torch.from_numpy(rows[h]), h].double().numpy()
-        check_attention_rows(got, want, f"forward {name} head {h}")
-    ctx.close()
+        worst = max(worst, check_attention_rows(got, want, f"forward {name} head {h}"))
+    log(f"    oracle rows: max-abs {worst[0]:.3e}, normalised {worst[1]:.3e}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "wan_p4", "wan_p8"])
+def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
+    _forward_modes_case(hcms, oracle_mod, name, 64)
+
+
+def test_forward_stress_bitwise_across_modes_and_chunkings(hcms, oracle_mod):
+    """All 40 heads of S = 100000 on one GPU, chunkings {40}, {10 x 4} and
+    {14, 13, 13}: auto runs the fused plan on {14, 13, 13} (each launch
+    carrying copies of 13-14 heads over a 40-head strided layout) and lanes on
+    {10 x 4}.  Oracle on 32 sampled rows per head."""
+    _forward_modes_case(hcms, oracle_mod, "stress", 32)
 
 
 @pytest.mark.parametrize("S,H,P,sizes_list", [
@@ -262,7 +284,9 @@ def test_forward_bitwise_across_modes_and_chunkings(hcms, oracle_mod, name):
     (4096, 8, 8, [(1,) * 8, (7, 1)]),                 # 16 tiles per head: many idle CUs
     (56160, 5, 8, [(2, 2, 1), (1,) * 5, (4, 1)]),     # Wan-P8: 440 / 220 / 880 workgroups
     (64000, 2, 8, [(1, 1)]),                          # 250 workgroups: 6 idle CUs, too few to
-])                                                    # carry the copies; they run after it
+                                                      # carry the copies; they run after it
+    (100000, 40, 8, [(14, 13, 13), (10,) * 4]),       # Stress: copies of 13-14 of 40 heads
+])
 def test_fused_forward_bitwise_equals_serial(hcms, S, H, P, sizes_list):
     """The fused plan (the next chunk's pack and the previous chunk's unpack
     riding in each attention launch) gives the serial plan's bits, with the
