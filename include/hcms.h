@@ -172,6 +172,29 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
                                      void *dv, float *delta, int S, int H, int d, float scale,
                                      const int *chunk_sizes, int n_chunks, int dtype, void *stream);
 
+/*
+ * hcms_attention_backward without the delta workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * or training loops, harnesses that forbid hipMalloc).  D = <dO, O> per query
+ * goes to a scratch array inside the library instead: one per device,
+ * HCMS_NOALLOC_DELTA_MAX floats (16 MiB), allocated with the library's code
+ * object and held until the process ends.  The call itself allocates nothing
+ * (no hipMalloc, no hipFree); the caller passes every input and output.
+ * Arguments, results and errors are those of hcms_attention_backward (dq, dk,
+ * dv bit-identical to it), plus CAPACITY when S * H > HCMS_NOALLOC_DELTA_MAX.
+ * The first call on a device looks up that device's copy of the array.
+ * Calls on one device share its array: two calls whose launches can overlap
+ * on one GPU (different streams without an ordering between them) race and
+ * give undefined gradients.  Calls ordered on one stream are safe; every call
+ * writes D before it reads it, so nothing needs clearing between calls.
+ */
+#define HCMS_NOALLOC_DELTA_MAX (4 * 1024 * 1024)
+HCMS_API int hcms_attention_backward_noalloc(const void *q, const void *k, const void *v,
+                                             const void *out, const void *dout, const float *lse,
+                                             void *dq, void *dk, void *dv, int S, int H, int d,
+                                             float scale, const int *chunk_sizes, int n_chunks,
+                                             int dtype, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Scheduler                                                                 */
 /* ------------------------------------------------------------------------ */

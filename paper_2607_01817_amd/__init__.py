@@ -26,6 +26,7 @@ MODE_SERIAL, MODE_PIPELINED, MODE_INLINE, MODE_LANES, MODE_AUTO, MODE_SLOTS, MOD
     0, 1, 2, 3, 4, 5, 6)
 OP_RECORD, OP_WAIT, OP_PACK, OP_ATTENTION, OP_UNPACK = 0, 1, 2, 3, 4
 STREAM_MAIN, STREAM_COPY, STREAM_COMPUTE, STREAM_IN_ATTENTION = 0, 1, 2, 3
+NOALLOC_DELTA_MAX = 4 * 1024 * 1024   # S * H limit of attention_backward_noalloc
 
 _DTYPES = {torch.bfloat16: BF16, torch.float32: FP32}
 _lib = None
@@ -69,6 +70,8 @@ def load():
         "hcms_attention_lse": ([vp, vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
         "hcms_attention_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, f, ip, i, i,
                                      vp], i),
+        "hcms_attention_backward_noalloc": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, f, ip,
+                                             i, i, vp], i),
         "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
         "hcms_auto_mode": ([i, i, i, ip, i, i], i),
         "hcms_ctx_last_mode": ([vp], i),
@@ -323,6 +326,24 @@ def attention_backward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: t
         sizes, n, _dtype(q), _stream(stream)))
     return dq, dk, dv
 
+
+def attention_backward_noalloc(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                               out: torch.Tensor, dout: torch.Tensor, lse: torch.Tensor,
+                               scale: float, chunk_sizes, dq: torch.Tensor, dk: torch.Tensor,
+                               dv: torch.Tensor, stream=None):
+    """:func:`attention_backward` into caller-given ``dq``, ``dk``, ``dv``
+    with the library's own scratch array in place of the delta workspace:
+    the call allocates nothing (for code that must not allocate, such as a
+    captured graph).  S * H is limited to ``NOALLOC_DELTA_MAX``."""
+    _same_hm((k, v, out, dout, dq, dk, dv), ("k", "v", "out", "dout", "dq", "dk", "dv"), q)
+    H, S, d = q.shape
+    lse = _stats(lse, "lse", H, S, q.device)
+    sizes, n = _ints(chunk_sizes)
+    _check(load().hcms_attention_backward_noalloc(
+        q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), S, H, d, float(scale), sizes, n, _dtype(q),
+        _stream(stream)))
+    return dq, dk, dv
 
 def linear(x: torch.Tensor, w: torch.Tensor, out: torch.Tensor | None = None,
            stream=None) -> torch.Tensor:

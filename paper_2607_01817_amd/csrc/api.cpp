@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -794,6 +795,36 @@ int check_qkv(const void *x, const void *w, const float *table, const int *grid,
 
 }  // namespace
 
+// The scratch array of hcms_attention_backward_noalloc: D = <dO, O> of every
+// query of the call, HCMS_NOALLOC_DELTA_MAX floats (16 MiB) per device, held
+// until the process ends.  Host code never uses this name as an address: the
+// device address of each GPU's copy comes from hipGetSymbolAddress.
+static __device__ __align__(256) float scratch[HCMS_NOALLOC_DELTA_MAX];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device.
+int scratch_for_current_device(float **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(HCMS_ERR_ARG, "device %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(HCMS_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_ptr[dev] = static_cast<float *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return HCMS_OK;
+}
+}  // namespace
+
 extern "C" {
 
 int hcms_abi_version(void) { return HCMS_ABI_VERSION; }
@@ -885,10 +916,12 @@ int hcms_attention_lse(const void *q, const void *k, const void *v, void *out, f
                          static_cast<hipStream_t>(stream));
 }
 
-int hcms_attention_backward(const void *q, const void *k, const void *v, const void *out,
-                            const void *dout, const float *lse, void *dq, void *dk, void *dv,
-                            float *delta, int S, int H, int d, float scale,
-                            const int *chunk_sizes, int n_chunks, int dtype, void *stream) {
+// Validation shared by the two backward entry points; with_delta false: no
+// delta workspace (the library's own scratch array takes its place).
+static int check_backward_args(const void *q, const void *k, const void *v, const void *out,
+                               const void *dout, const float *lse, void *dq, void *dk, void *dv,
+                               bool with_delta, const float *delta, int S, int H, int d,
+                               float scale, const int *chunk_sizes, int n_chunks, int dtype) {
     int st = check_attention_args(q, k, v, out, S, H, d, scale, chunk_sizes, n_chunks, dtype);
     if (st != HCMS_OK) return st;
     if (S > 0 && (!dout || !dq || !dk || !dv)) return fail(HCMS_ERR_NULL, "a gradient tensor is NULL");
@@ -908,11 +941,20 @@ int hcms_attention_backward(const void *q, const void *k, const void *v, const v
                 return fail(HCMS_ERR_ALIAS, "gradients %d and %d overlap", i, j);
     }
     if ((st = check_stats(lse, "lse", S, H, dq, dk, dv, dout, d, dtype)) != HCMS_OK) return st;
-    if ((st = check_stats(delta, "delta", S, H, dq, dk, dv, dout, d, dtype)) != HCMS_OK) return st;
-    if ((st = check_stats(delta, "delta", S, H, q, k, v, out, d, dtype)) != HCMS_OK) return st;
-    if (S > 0 && overlaps(lse, int64_t{S} * H * 4, delta, int64_t{S} * H * 4))
-        return fail(HCMS_ERR_ALIAS, "lse and delta overlap");
-    if (S == 0) return ok();
+    if (with_delta) {
+        if ((st = check_stats(delta, "delta", S, H, dq, dk, dv, dout, d, dtype)) != HCMS_OK) return st;
+        if ((st = check_stats(delta, "delta", S, H, q, k, v, out, d, dtype)) != HCMS_OK) return st;
+        if (S > 0 && overlaps(lse, int64_t{S} * H * 4, delta, int64_t{S} * H * 4))
+            return fail(HCMS_ERR_ALIAS, "lse and delta overlap");
+    }
+    return HCMS_OK;
+}
+
+// The chunks' backward launches, in order on `stream`.
+static int run_backward(const void *q, const void *k, const void *v, const void *out,
+                        const void *dout, const float *lse, void *dq, void *dk, void *dv,
+                        float *delta, int S, int d, float scale, const int *chunk_sizes,
+                        int n_chunks, int dtype, hipStream_t stream) {
     const int64_t head = static_cast<int64_t>(S) * d * elem_bytes(dtype);
     int h0 = 0;
     for (int i = 0; i < n_chunks; ++i) {
@@ -922,11 +964,41 @@ int hcms_attention_backward(const void *q, const void *k, const void *v, const v
         auto atw = [off](void *p) { return static_cast<char *>(p) + off; };
         const hipError_t e = hcms::launch_attention_backward(
             at(q), at(k), at(v), at(out), at(dout), lse + soff, atw(dq), atw(dk), atw(dv),
-            delta + soff, S, chunk_sizes[i], d, scale, dtype, static_cast<hipStream_t>(stream));
+            delta + soff, S, chunk_sizes[i], d, scale, dtype, stream);
         if (e != hipSuccess) return hip_fail(e, "attention backward launch");
         h0 += chunk_sizes[i];
     }
     return ok();
+}
+
+int hcms_attention_backward(const void *q, const void *k, const void *v, const void *out,
+                            const void *dout, const float *lse, void *dq, void *dk, void *dv,
+                            float *delta, int S, int H, int d, float scale,
+                            const int *chunk_sizes, int n_chunks, int dtype, void *stream) {
+    const int st = check_backward_args(q, k, v, out, dout, lse, dq, dk, dv, true, delta, S, H, d,
+                                       scale, chunk_sizes, n_chunks, dtype);
+    if (st != HCMS_OK) return st;
+    if (S == 0) return ok();
+    return run_backward(q, k, v, out, dout, lse, dq, dk, dv, delta, S, d, scale, chunk_sizes,
+                        n_chunks, dtype, static_cast<hipStream_t>(stream));
+}
+
+int hcms_attention_backward_noalloc(const void *q, const void *k, const void *v, const void *out,
+                                    const void *dout, const float *lse, void *dq, void *dk,
+                                    void *dv, int S, int H, int d, float scale,
+                                    const int *chunk_sizes, int n_chunks, int dtype,
+                                    void *stream) {
+    int st = check_backward_args(q, k, v, out, dout, lse, dq, dk, dv, false, nullptr, S, H, d,
+                                 scale, chunk_sizes, n_chunks, dtype);
+    if (st != HCMS_OK) return st;
+    if (static_cast<int64_t>(S) * H > HCMS_NOALLOC_DELTA_MAX)
+        return fail(HCMS_ERR_CAPACITY, "S * H = %lld exceeds the scratch limit of %d queries",
+                    static_cast<long long>(S) * H, HCMS_NOALLOC_DELTA_MAX);
+    if (S == 0) return ok();
+    float *delta = nullptr;
+    if ((st = scratch_for_current_device(&delta)) != HCMS_OK) return st;
+    return run_backward(q, k, v, out, dout, lse, dq, dk, dv, delta, S, d, scale, chunk_sizes,
+                        n_chunks, dtype, static_cast<hipStream_t>(stream));
 }
 
 int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {

@@ -484,6 +484,35 @@ def test_training_forward_and_backward_validation(lib):
     assert bwd(S=0, dout=None, dq=None, dk=None, dv=None, lse=None, delta=None) == OK
 
 
+def test_noalloc_backward_validation(lib):
+    """The entry point without a delta workspace validates like
+    hcms_attention_backward and rejects S * H past its scratch array."""
+    sizes = (ctypes.c_int * 2)(2, 2)
+    E, F, G_, H_ = 0x50000000, 0x60000000, 0x70000000, 0x80000000
+    L = 0x90000000
+
+    def bwd(dout=E, dq=F, dk=G_, dv=H_, lse=L, S=512, H=4, d=64, sz=sizes, n=2):
+        return lib.hcms_attention_backward_noalloc(A, B, C_, D_, dout, lse, dq, dk, dv, S, H, d,
+                                                   0.125, sz, n, 1, None)
+
+    assert bwd(dout=None) == ENULL
+    assert bwd(lse=None) == ENULL
+    assert bwd(dk=G_ + 8) == EALIGN
+    assert bwd(dq=A) == EALIAS
+    assert bwd(lse=F + 16) == EALIAS
+    assert bwd(d=96) == ESHAPE
+    assert bwd(S=0, dout=None, dq=None, dk=None, dv=None, lse=None) == OK
+    # S * H one past the limit, on fake far-apart [H][S][64] bf16 tensors.
+    limit = hcms.NOALLOC_DELTA_MAX
+    S = limit // 2 + 8
+    span = 2 * S * 64 * 2
+    p = [(1 << 40) + i * span for i in range(9)]
+    one = (ctypes.c_int * 2)(1, 1)
+    st = lib.hcms_attention_backward_noalloc(*p, S, 2, 64, 0.125, one, 2, 0, None)
+    assert st == ECAP, hcms.load().hcms_last_error()
+    assert b"scratch" in lib.hcms_last_error()
+
+
 # ---------------------------------------------------------------------------
 # Layer neighbours: projection GEMM, rotation table, QKV projection, layer
 # ---------------------------------------------------------------------------
