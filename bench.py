@@ -148,15 +148,16 @@ def quartiles(xs):
     return {"median": round(float(q[1]), 4), "iqr": [round(float(q[0]), 4), round(float(q[2]), 4)]}
 
 
-def compare_modes(ctx, w, chunks, reps: int, dev):
-    """Serial, Alg. 1, inline, lanes, fused and two-slot schedules of one workload, interleaved
-    (order reversed every other rep to cancel clock drift), step time from
-    events on the main stream."""
+def compare_modes(ctx, w, chunks, reps: int, dev, modes=None):
+    """The schedules of one workload and chunking side by side: serial, Alg. 1,
+    inline, lanes, fused, the slots plan on two chunk slots and auto (the plan
+    MODE_AUTO picks), interleaved (order reversed every other rep to cancel
+    clock drift), step time from events on the main stream."""
     q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
     out = torch.empty_like(q)
     ws = ctx.workspaces(w.S, w.H, w.d, q.dtype)
     slots = ctx.slot_workspaces(w.S, max(chunks), w.d, q.dtype)
-    modes = ["serial", "pipelined", "inline", "lanes", "fused", "slots_two_slot"]
+    modes = modes or ["serial", "pipelined", "inline", "lanes", "fused", "slots_two_slot", "auto"]
 
     def run(m):
         if m == "slots_two_slot":   # the slots plan on two chunk slots
@@ -165,6 +166,8 @@ def compare_modes(ctx, w, chunks, reps: int, dev):
         return lambda: ctx.forward(q, k, v, w.P, w.scale, chunks, mode=MODES[m], out=out,
                                    workspaces=ws)
 
+    for m in modes:                 # one warm run of each
+        run(m)()
     times = {m: [] for m in modes}
     for r in range(reps + 1):
         for m in (modes if r % 2 == 0 else modes[::-1]):
@@ -180,6 +183,11 @@ def compare_modes(ctx, w, chunks, reps: int, dev):
         qm["gain_vs_serial_ms"] = round(ser["median"] - qm["median"], 4)
         qm["below_serial"] = bool(qm["iqr"][1] < ser["iqr"][0])
         res[m + "_ms"] = qm
+    if "auto" in modes:
+        # auto running the serial plan issues the serial plan's launches:
+        # equal by construction, whatever the noise between the two medians.
+        res["auto_not_above_serial"] = bool(res["auto_runs"] == "serial" or
+                                            res["auto_ms"]["median"] <= ser["median"])
     es = q.element_size()
     res["workspace_bytes"] = {"full": 4 * w.S * w.H * w.d * es,
                               "two_slot": 4 * 2 * max(chunks) * w.S * w.d * es}
@@ -189,8 +197,9 @@ def compare_modes(ctx, w, chunks, reps: int, dev):
 
 def time_model_sweep(ctx, w, reps: int, dev):
     """The paper's chunk-count study on one GPU: for C = 1..H (the default
-    partition), the serial, Alg. 1 and auto schedules interleaved, the layout
-    and attention kernel times of the serial run, and the time model
+    partition), the serial, Alg. 1 and auto schedules interleaved, and the
+    layout and attention kernel times of the serial plan (medians over `reps`
+    warmed runs with events around every kernel); the paper's
     T(C) = a + T_comm / C + beta C fitted to the scheduled times."""
     q, k, v = (x.to(dev) for x in inputs.make_qkv(w))
     out = torch.empty_like(q)
@@ -205,6 +214,8 @@ def time_model_sweep(ctx, w, reps: int, dev):
         def run(m):
             ctx.forward(q, k, v, w.P, w.scale, sizes, mode=MODES[m], out=out, workspaces=ws)
 
+        for m in modes:
+            run(m)
         times = {m: [] for m in modes}
         for r in range(reps + 1):
             for m in (modes if r % 2 == 0 else modes[::-1]):
@@ -213,18 +224,21 @@ def time_model_sweep(ctx, w, reps: int, dev):
                     times[m] += t
         for m in modes:
             med[m].append(float(np.median(times[m])))
-        ctx.set_timing(1)
-        run("serial")
+        ctx.set_timing(reps)
+        for _ in range(reps):
+            run("serial")
         torch.cuda.synchronize()
-        t_comm.append(sum(ctx.kernel_ms(hcms.OP_PACK)) + sum(ctx.kernel_ms(hcms.OP_UNPACK)))
-        t_attn.append(sum(ctx.kernel_ms(hcms.OP_ATTENTION)))
+        per_call = lambda kind: np.asarray(ctx.kernel_ms(kind)).reshape(reps, C).sum(axis=1)  # noqa: E731
+        t_comm.append(float(np.median(per_call(hcms.OP_PACK) + per_call(hcms.OP_UNPACK))))
+        t_attn.append(float(np.median(per_call(hcms.OP_ATTENTION))))
         ctx.set_timing(0)
-    res = {"workload": w.name, "chunk_counts": counts,
+    res = {"workload": w.name, "S": w.S, "H": w.H, "chunk_counts": counts,
            "serial_ms": [round(x, 4) for x in med["serial"]],
            "pipelined_ms": [round(x, 4) for x in med["pipelined"]],
            "auto_ms": [round(x, 4) for x in med["auto"]],
            "layout_kernels_ms": [round(x, 4) for x in t_comm],
-           "attention_kernels_ms": [round(x, 4) for x in t_attn]}
+           "attention_kernels_ms": [round(x, 4) for x in t_attn],
+           "note": "kernel columns: medians over the warmed serial runs, events around every kernel"}
     for m in ("pipelined", "auto"):
         a, tc, beta = hcms.model_fit(counts, med[m])
         pred = [a + tc / c + beta * c for c in counts]
@@ -238,6 +252,91 @@ def time_model_sweep(ctx, w, reps: int, dev):
             "best_c_measured": counts[int(np.argmin(med[m]))],
             "max_rel_error": round(err, 5)}
     del q, k, v, out
+    return res
+
+
+def adaptive_chunks(ctx, sweeps):
+    """Calibrate the one-GPU time model (hcms_model_plan_time) on the sweeps'
+    measurements and let hcms_choose_chunks pick the chunk count:
+      * t_round = kappa S (a full round of attention workgroups; its work per
+        workgroup is 4 Br S d) and g0 by least squares on the serial plans'
+        attention times, T_attn = kappa S (sum W / n) + kappa g0 S (R - sum W / n)
+        (R = sum ceil(W / n), the launches' round count), over every sweep;
+      * t_copy = the layout kernels at C = 1 over 4 H head-tensors;
+      * beta = (Alg. 1 - serial) at C = 1 over its 7 synchronisations.
+    Reports the model's prediction of the auto plan per C against the
+    measured auto time and whether the chosen C measures within 1 % of the
+    sweep's best."""
+    n = ctx.num_cu
+    rows, ys = [], []
+    for sw in sweeps:
+        tiles = -(-sw["S"] // 256)
+        for C, t in zip(sw["chunk_counts"], sw["attention_kernels_ms"]):
+            Ws = [tiles * h for h in hcms.default_chunks(sw["H"], C)]
+            R = sum(-(-x // n) for x in Ws)
+            rows.append([sw["S"] * sum(Ws) / n, sw["S"] * (R - sum(Ws) / n)])
+            ys.append(t)
+    (kappa, kg0), *_ = np.linalg.lstsq(np.asarray(rows), np.asarray(ys), rcond=None)
+    g0 = float(min(1.0, max(1e-3, kg0 / kappa))) if kappa > 0 else 1.0
+    out = {"kappa_ms_per_key": float(kappa), "g0": round(g0, 4), "configs": []}
+    for sw in sweeps:
+        S, H = sw["S"], sw["H"]
+        t_copy = sw["layout_kernels_ms"][0] / (4 * H)
+        beta = max(0.0, (sw["pipelined_ms"][0] - sw["serial_ms"][0]) / 7)
+        t_round = kappa * S
+        pred = [hcms.model_plan_time(S, 128, hcms.default_chunks(H, C), hcms.MODE_AUTO, n, t_round,
+                                     g0, t_copy, beta) for C in sw["chunk_counts"]]
+        sizes, plan, t_pred = hcms.choose_chunks(S, H, 128, n, t_round, g0, t_copy, beta)
+        meas = sw["auto_ms"]
+        best = min(meas)
+        chosen = meas[len(sizes) - 1]
+        out["configs"].append({
+            "workload": sw["workload"], "t_round_ms": round(t_round, 4),
+            "t_copy_ms": round(t_copy, 5), "beta_ms": round(beta, 5),
+            "predicted_auto_ms": [round(x, 4) for x in pred],
+            "measured_auto_ms": meas,
+            "prediction_error": [round((p_ - m_) / m_, 4) for p_, m_ in zip(pred, meas)],
+            "chosen_chunks": sizes, "chosen_plan": MODE_NAMES[plan],
+            "chosen_measured_ms": chosen, "best_measured_ms": best,
+            "best_measured_c": sw["chunk_counts"][int(np.argmin(meas))],
+            "chosen_within_1pct_of_best": bool(chosen <= 1.01 * best)})
+    return out
+
+
+def peak_memory(ctx, w, chunks, dev):
+    """The caching allocator's peak above the resident inputs for one forward
+    on full head-major workspaces and one on two chunk slots (workspaces and
+    output allocated inside the measured region).  The inputs are drawn on
+    the device (the byte counts do not depend on their values)."""
+    g = torch.Generator(device=dev).manual_seed(w.seed)
+    q, k, v = ((torch.randn((w.S, w.H, w.d), generator=g, device=dev) * w.sigma).to(torch.bfloat16)
+               for _ in range(3))
+    torch.cuda.synchronize()
+    res = {"workload": w.name, "chunks": list(chunks)}
+    for name in ("full_workspaces", "two_slots"):
+        torch.cuda.empty_cache()
+        base = torch.cuda.memory_allocated(dev)
+        torch.cuda.reset_peak_memory_stats(dev)
+        out = torch.empty_like(q)
+        if name == "full_workspaces":
+            ws = [torch.empty((w.H, w.S, w.d), dtype=q.dtype, device=dev) for _ in range(4)]
+            ctx.forward(q, k, v, w.P, w.scale, chunks, out=out, workspaces=ws)
+        else:
+            ws = [torch.empty((2, max(chunks), w.S, w.d), dtype=q.dtype, device=dev)
+                  for _ in range(4)]
+            ctx.forward_slots(q, k, v, w.P, w.scale, chunks, out=out, slots=ws)
+        torch.cuda.synchronize()
+        res[name + "_MB"] = round((torch.cuda.max_memory_allocated(dev) - base) / 1e6, 1)
+        del out, ws
+    inputs_mb = 3 * q.numel() * q.element_size() / 1e6
+    res["inputs_MB"] = round(inputs_mb, 1)
+    tot_f, tot_s = inputs_mb + res["full_workspaces_MB"], inputs_mb + res["two_slots_MB"]
+    res["peak_with_inputs_change"] = round(tot_s / tot_f - 1.0, 4)
+    res["note"] = ("peak = torch.cuda.max_memory_allocated above the resident Q, K, V; the paper "
+                   "reports -8.7 % peak memory for the whole model on 4 GPUs at 131K tokens "
+                   "(appendix memory table), context only")
+    del q, k, v
+    torch.cuda.empty_cache()
     return res
 
 
@@ -361,6 +460,73 @@ def layer_step(ctx, lw, chunks, reps: int, dev):
     return res
 
 
+def trace_summary(trace_csv: str, line_path: str) -> str:
+    """Markdown summary of a rocprofv3 kernel trace (``--kernel-trace
+    --output-format csv``) of one bench.py run, checked against the JSON line
+    that same run printed.  The attention dispatches are taken in issue order:
+    the first warmup * C are the warm-up steps, the next steps * C the timed
+    steps, the next steps * C the pass with events around every kernel (the
+    line's roofline), then the plain-launch pass under the fused plan."""
+    import csv
+    line = None
+    with open(line_path) as f:
+        for ln in f:
+            ln = ln.strip()
+            if ln.startswith("{") and '"metric"' in ln:
+                line = json.loads(ln)
+    if line is None:
+        raise SystemExit(f"no bench line in {line_path}")
+    cfg = line["config"]
+    chunks, S, d = cfg["chunks"], cfg["S"], cfg["d"]
+    C, W, K = len(chunks), line["warmup"], line["steps"]
+    rows = []
+    with open(trace_csv) as f:
+        for r in csv.DictReader(f):
+            if "attention_dma_kernel" in r["Kernel_Name"] or "attention_kernel" in r["Kernel_Name"]:
+                rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
+    rows.sort()
+    flops = [4.0 * S * S * chunks[i % C] * d for i in range(K * C)]
+
+    def pass_stats(first):
+        sel = rows[first:first + K * C]
+        if len(sel) < K * C:
+            return None
+        dur = [(e - b) * 1e-6 for b, e, _ in sel]          # ns -> ms
+        ach = sum(flops) / (sum(dur) * 1e-3) / 1e12
+        per_step = [sum(dur[i * C:(i + 1) * C]) for i in range(K)]
+        return {"avg_launch_ms": statistics.mean(dur), "kernel_ms_per_step": statistics.mean(per_step),
+                "achieved": ach, "frac": ach / MFMA_BF16_PEAK_TFLOPS, "names": {n for *_, n in sel}}
+
+    timed, events = pass_stats(W * C), pass_stats((W + K) * C)
+    rf = line["roofline"]
+    out = [f"Bench line: value {line['value']} TFLOP/s, ms_per_step {line['ms_per_step']}, "
+           f"roofline achieved {rf['achieved']} TFLOP/s, frac {rf['frac']} "
+           f"({cfg['workload']}; warmup {W}, steps {K}).", "",
+           f"Attention dispatches in the trace: {len(rows)}.", "",
+           "| Pass | Dispatches | Avg launch (ms) | Kernel time per step (ms) | TFLOP/s | frac |",
+           "|---|---|---|---|---|---|"]
+    for name, st, first in (("timed steps", timed, W * C), ("steps with events (the line's events_pass)",
+                                                            events, (W + K) * C)):
+        if st:
+            out.append(f"| {name} | {first}..{first + K * C - 1} | {st['avg_launch_ms']:.4f} | "
+                       f"{st['kernel_ms_per_step']:.4f} | {st['achieved']:.1f} | {st['frac']:.4f} |")
+    ev = rf.get("events_pass", {})
+    if timed:
+        out += ["",
+                f"- Attention kernel time per timed step {timed['kernel_ms_per_step']:.4f} ms <= "
+                f"the line's ms_per_step {line['ms_per_step']}: "
+                f"{timed['kernel_ms_per_step'] <= line['ms_per_step']}.",
+                f"- frac from the trace's timed steps {timed['frac']:.4f} against the line's "
+                f"{rf['frac']}: {abs(timed['frac'] / rf['frac'] - 1) * 100:.2f} % apart."]
+    if events and ev:
+        out.append(f"- frac from the trace's events pass {events['frac']:.4f} against the line's "
+                   f"events_pass {ev['frac']}: {abs(events['frac'] / ev['frac'] - 1) * 100:.2f} % "
+                   f"apart (the events add a few microseconds to each launch they bracket).")
+    if timed:
+        out.append(f"- Kernels: {', '.join(sorted(timed['names']))}.")
+    return "\n".join(out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -376,7 +542,15 @@ def main():
                     help="time the step only (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter passes)")
+    ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
+                    help="summarise a rocprofv3 kernel trace of a bench run (no GPU needed)")
+    ap.add_argument("--bench-line", metavar="FILE",
+                    help="with --trace-summary: the output of the traced run (its JSON line)")
     args = ap.parse_args()
+
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary, args.bench_line))
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the hot path "
@@ -452,7 +626,29 @@ def main():
     C = len(sizes)
     launch_flops = [4.0 * w.S * w.S * sizes[i % C] * w.d for i in range(len(attn_ms))]
     avg_attn_ms = statistics.mean(attn_ms)
-    achieved = sum(launch_flops) / (sum(attn_ms) * 1e-3) / 1e12
+    achieved_events = sum(launch_flops) / (sum(attn_ms) * 1e-3) / 1e12
+    # Copies that ran as kernels of their own (in the fused plan chunk 0's
+    # pack and the last unpack; the others rode in the attention launches).
+    own_pk = [i for i in range(len(pack_ms)) if plan != "fused" or i % C == 0]
+    own_up = [i for i in range(len(unpack_ms)) if plan != "fused" or i % C == C - 1]
+    if plan in ("fused", "serial"):
+        # One stream, kernels back to back: the timed steps' attention time
+        # is the step minus its own copy kernels (their durations from the
+        # events pass).  The events around every kernel in that pass
+        # lengthen each launch by a few microseconds, so this figure, from
+        # the timed region itself, is the roofline's.
+        copies_per_step = (sum(pack_ms[i] for i in own_pk) +
+                           sum(unpack_ms[i] for i in own_up)) / args.steps
+        attn_per_step = ms_per_step - copies_per_step
+        achieved = w.flops / (attn_per_step * 1e-3) / 1e12
+        how = (f"timed steps: {ms_per_step:.4f} ms per step minus its own copy kernels "
+               f"{copies_per_step:.4f} ms (pack of chunk 0 and unpack of the last chunk"
+               f"{'' if plan == 'fused' else ', and every other copy'}, from the events pass) = "
+               f"{attn_per_step:.4f} ms of attention launches per step, "
+               f"{attn_per_step / C:.4f} ms per launch on average")
+    else:
+        achieved = achieved_events
+        how = "the events pass (several streams: the step does not decompose)"
     result = {
         "metric": "attention TFLOP/s (4·S²·H·d) + pipelined vs serial chunk time, 1 MI355X",
         "value": round(tflops, 2),
@@ -484,10 +680,14 @@ def main():
                 "; in the fused plan each launch also carries the neighbouring chunks' copies "
                 "on the CUs its last round leaves idle (attention_dma_kernel<true>)"
                 if plan == "fused" else ""),
-            "per_launch": f"4*S^2*H_c*d FLOP per chunk launch; avg launch {avg_attn_ms:.4f} ms "
-                          f"over {len(attn_ms)} launches, events on the launching stream, in "
-                          f"a second pass of the {args.steps} steps "
-                          f"({ms_per_step_events:.4f} ms per step with the events)",
+            "per_launch": f"4*S^2*H_c*d FLOP per chunk launch; achieved from {how}",
+            "events_pass": {
+                "achieved": round(achieved_events, 2),
+                "frac": round(achieved_events / MFMA_BF16_PEAK_TFLOPS, 4),
+                "avg_launch_ms": round(avg_attn_ms, 4),
+                "note": f"events around every kernel on its stream, a second pass of the "
+                        f"{args.steps} steps ({ms_per_step_events:.4f} ms per step with the "
+                        f"events), {len(attn_ms)} launches"},
         },
     }
     if plain_ms:
@@ -507,9 +707,7 @@ def main():
         up_bytes = [2 * w.S * sizes[i % C] * w.d * es for i in range(len(unpack_ms))]
         # In the fused plan a copy that rides in an attention launch reports
         # that launch's time; the rates then cover the copies that ran alone
-        # (chunk 0's pack, the last chunk's unpack).
-        own_pk = [i for i in range(len(pack_ms)) if plan != "fused" or i % C == 0]
-        own_up = [i for i in range(len(unpack_ms)) if plan != "fused" or i % C == C - 1]
+        # (chunk 0's pack, the last chunk's unpack: own_pk, own_up above).
         pipe = {"pack_in_step_GBps": round(sum(pk_bytes[i] for i in own_pk) /
                                            (sum(pack_ms[i] for i in own_pk) * 1e-3) / 1e9, 1),
                 "unpack_in_step_GBps": round(sum(up_bytes[i] for i in own_up) /
@@ -556,11 +754,19 @@ def main():
         # ---- the schedules side by side: serial, Alg. 1, inline, lanes, fused ----
         torch.cuda.synchronize()
         reps = max(20, args.steps // 2)
-        cmp = [compare_modes(ctx, w, sizes, reps, dev), compare_modes(ctx, w, (w.H,), reps, dev)]
+        cmp = [compare_modes(ctx, w, sizes, reps, dev), compare_modes(ctx, w, (w.H,), reps, dev),
+               compare_modes(ctx, w, (1,) * w.H, reps, dev)]
         wp4 = inputs.WORKLOADS["wan_p4"]
-        for ch in ((5, 5), (10,)):
+        for ch in ((5, 5), (4, 3, 3), (10,)):
             cmp.append(compare_modes(ctx, wp4, ch, reps, dev))
+        small = inputs.WORKLOADS["small"]
+        for ch in ((3, 3, 2), (2, 2, 2, 2)):
+            cmp.append(compare_modes(ctx, small, ch, max(reps, 40), dev))
         result["schedules"] = cmp
+
+        # ---- allocator peak: full workspaces against two chunk slots ----
+        result["memory"] = [peak_memory(ctx, w, (1,) * w.H, dev),
+                            peak_memory(ctx, inputs.WORKLOADS["stress"], (10, 10, 10, 10), dev)]
 
         # ---- training: forward with the softmax statistic, then backward ----
         result["training"] = training_step(ctx, w, sizes, max(10, args.steps // 4), dev)
@@ -570,8 +776,9 @@ def main():
         result["layer"] = layer_step(ctx, lw, lw.chunkings[-1], max(10, args.steps // 2), dev)
 
         # ---- the time model over the chunk count (Wan-P8, Wan-P4) ----
-        result["time_model"] = [time_model_sweep(ctx, tw, reps, dev)
-                                for tw in dict.fromkeys((w, wp4))]
+        sweeps = [time_model_sweep(ctx, tw, reps, dev) for tw in dict.fromkeys((w, wp4))]
+        result["time_model"] = sweeps
+        result["adaptive_chunks"] = adaptive_chunks(ctx, sweeps)
 
     if not args.no_cpu:
         log("timing the oracle on the host ...")

@@ -293,10 +293,15 @@ HCMS_API int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap);
  * B the attention tiling for head dimension d: 256 queries and one workgroup
  * per CU for d = 128, 128 and two for d = 64).  One lane takes
  * sum_c ceil(W_c / (n_cu * B)) rounds of workgroups; two lanes pool them,
- * ceil(sum_c W_c / (n_cu * B)).  Returns HCMS_MODE_LANES when pooling saves a
- * round; otherwise HCMS_MODE_FUSED for d = 128 with bf16 storage (the launches
- * that can carry the neighbouring chunks' copies) and HCMS_MODE_INLINE for the
- * rest; HCMS_MODE_SERIAL for one chunk.  Errors: HCMS_ERR_SHAPE (S < 0, d),
+ * ceil(sum_c W_c / (n_cu * B)).  A launch's last round leaves
+ * n_cu * B * ceil(W_c / (n_cu * B)) - W_c slots idle.  Returns
+ * HCMS_MODE_SERIAL for one chunk; HCMS_MODE_LANES when pooling saves a round;
+ * otherwise, for d = 128 with bf16 storage, HCMS_MODE_FUSED when some launch
+ * leaves at least n_cu * B / 8 slots idle (where the neighbouring chunks'
+ * copies ride) and HCMS_MODE_SERIAL when none does (the fused plan would run
+ * the serial plan's launches); for the other kernels HCMS_MODE_INLINE when
+ * chunk 0's launch leaves that many slots idle (where packs 1..C-1 run) and
+ * HCMS_MODE_SERIAL otherwise.  Errors: HCMS_ERR_SHAPE (S < 0, d),
  * HCMS_ERR_DTYPE, HCMS_ERR_ARG (n_cu < 1), HCMS_ERR_NULL or HCMS_ERR_CHUNKS.
  * Host only.
  */
@@ -330,6 +335,50 @@ HCMS_API int hcms_model_optimal_chunks(double t_comm, double beta, int H, double
 HCMS_API int hcms_model_speedup(double rho, double beta_over_total, int n_chunks, double *s_out);
 HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n, double *a_out,
                             double *t_comm_out, double *beta_out);
+
+/*
+ * One-GPU extension of the time model (this library's, for the chunk-count
+ * study of Sec. 3.7 and the adaptive chunk count the paper leaves as future
+ * work, Sec. 6).  On one GPU the attention time depends on the chunking: a
+ * launch of W workgroups on n slots (n = n_cu for d = 128, 2 n_cu for
+ * d = 64) runs floor(W / n) full rounds and, when n does not divide W, a
+ * partial round keeping a fraction f = (W mod n) / n of the slots busy,
+ * which lasts t_round (g0 + (1 - g0) f) (the clock rises when part of the
+ * chip idles; g0 = 1: a partial round costs a full one).  Inputs measured on
+ * the device: t_round (one full round of attention workgroups), g0 in
+ * (0, 1], t_copy (the layout kernel for one head of one tensor) and beta (one
+ * event record or wait on the critical path).
+ *
+ * hcms_model_plan_time: model time of `mode` (a plan, or HCMS_MODE_AUTO for
+ *   the plan hcms_auto_mode picks) on chunk_sizes:
+ *     attention: the sum of the launches' rounds (HCMS_MODE_LANES: the
+ *       chunks' workgroups pooled into one launch's rounds), times t_round;
+ *     copies on the critical path, in head-tensors times t_copy (a pack moves
+ *       3 per head, an unpack 1): all 4 H in serial mode; otherwise chunk 0's
+ *       pack and the last chunk's unpack, plus in fused mode the copies a
+ *       launch with fewer than n / 8 idle slots cannot carry;
+ *     synchronisations times beta: 0 (serial, fused), 4 (inline, lanes),
+ *       2 C + 3 (pipelined, slots: the compute stream's wait and record per
+ *       chunk, the fork and the join).
+ *   With every launch filling whole rounds and equal chunks, the pipelined
+ *   plan's time is the paper's T_hcms(C) with T_comm = 4 H t_copy, per-chunk
+ *   overhead 2 beta and T_0 = 3 beta.
+ *   Errors: NULL, SHAPE (S < 0, d), DTYPE, CHUNKS, ARG (mode; a time negative
+ *   or not finite; n_cu < 1; g0 outside (0, 1]).
+ * hcms_choose_chunks: for C = 1 .. min(H, max_chunks), the chunk rule's sizes
+ *   (hcms_default_chunks) in the plan HCMS_MODE_AUTO would run; writes the
+ *   fastest under the model to sizes_out (room for min(H, max_chunks) ints),
+ *   its plan to *mode_out and its model time to *t_out (either may be NULL),
+ *   and returns its chunk count.  Ties go to fewer chunks.  Errors: as
+ *   hcms_model_plan_time, plus SHAPE (H < 1) and CHUNKS (max_chunks < 1).
+ * Host only.
+ */
+HCMS_API int hcms_model_plan_time(int S, int d, int dtype, const int *chunk_sizes, int n_chunks,
+                                  int mode, int n_cu, double t_round, double g0, double t_copy,
+                                  double beta, double *t_out);
+HCMS_API int hcms_choose_chunks(int S, int H, int d, int dtype, int n_cu, double t_round,
+                                double g0, double t_copy, double beta, int max_chunks,
+                                int *sizes_out, int *mode_out, double *t_out);
 
 typedef struct hcms_ctx hcms_ctx;
 

@@ -15,6 +15,19 @@ one function per equation of the paper, written from its definitions:
   measured points, by numpy's lstsq (the library routine is the step; the
   model is the paper's).
 
+The one-GPU extension (this build's reading; the paper holds the attention
+time fixed):
+
+* :func:`launch_rounds`  duration, in full rounds, of a launch of W
+  workgroups on n slots: floor(W / n) full rounds plus, when n does not
+  divide W, one partial round with a fraction f of the slots busy lasting
+  g0 + (1 - g0) f of a full one;
+* :func:`plan_time`      that attention time summed over the launches (the
+  lanes plan pools the chunks' workgroups), plus the copies a plan leaves on
+  the critical path times t_copy, plus its synchronisations times beta;
+* :func:`choose_chunks`  the chunk count of the chunk rule whose plan the
+  model predicts fastest, by evaluating every C.
+
 Pins in ``tests/test_time_model.py``: C* zeroes dT/dC and every integer
 neighbour is no better; S(C) = T_base / T(C) with rho = T_comm / T_base;
 S -> 1 / (1 - rho) as beta -> 0 and C grows (the paper's upper bound); S(1) =
@@ -53,3 +66,64 @@ def fit(chunk_counts, times) -> tuple[float, float, float]:
     A = np.stack([np.ones_like(c), 1.0 / c, c], axis=1)
     x, *_ = np.linalg.lstsq(A, np.asarray(times, dtype=np.float64), rcond=None)
     return float(x[0]), float(x[1]), float(x[2])
+
+
+# ---------------------------------------------------------------------------
+# One GPU: the attention time depends on the chunking through its rounds
+# ---------------------------------------------------------------------------
+SERIAL, PIPELINED, INLINE, LANES, AUTO, SLOTS, FUSED = 0, 1, 2, 3, 4, 5, 6
+
+
+def launch_rounds(W: int, n: int, g0: float) -> float:
+    """Full rounds of a launch of W workgroups on n slots, the last one
+    counted as g0 + (1 - g0) f of a round when only a fraction f of the slots
+    has work."""
+    full, rem = divmod(W, n)
+    if rem == 0:
+        return float(full)
+    f = rem / n
+    return full + g0 + (1.0 - g0) * f
+
+
+def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_round: float,
+              g0: float, t_copy: float, beta: float) -> float:
+    """Model time of one plan of the chunk sizes ``sizes`` on one GPU with
+    ``n_slots`` attention workgroups per round of ``queries_per_wg`` queries."""
+    sizes = list(sizes)
+    C, H = len(sizes), sum(sizes)
+    tiles = -(-S // queries_per_wg)
+    W = [tiles * h for h in sizes]
+    if C == 1:
+        mode = SERIAL
+    if mode == LANES:
+        attn = launch_rounds(sum(W), n_slots, g0)
+    else:
+        attn = sum(launch_rounds(w, n_slots, g0) for w in W)
+    if mode == SERIAL:
+        copies = 4 * H                    # 3 tensors packed, 1 unpacked, per head
+    else:
+        copies = 3 * sizes[0] + sizes[-1]
+        if mode == FUSED:
+            for c, w in enumerate(W):
+                idle = (n_slots - w % n_slots) % n_slots
+                if idle >= max(1, n_slots // 8):
+                    continue              # this launch carries its neighbours' copies
+                if c + 1 < C:
+                    copies += 3 * sizes[c + 1]
+                if c >= 1:
+                    copies += sizes[c - 1]
+    syncs = {SERIAL: 0, FUSED: 0, INLINE: 4, LANES: 4, PIPELINED: 2 * C + 3, SLOTS: 2 * C + 3}[mode]
+    return attn * t_round + copies * t_copy + syncs * beta
+
+
+def choose_chunks(S: int, H: int, plan_of, n_slots: int, queries_per_wg: int, t_round: float,
+                  g0: float, t_copy: float, beta: float, max_chunks: int | None = None):
+    """(sizes, model time) of the fastest chunk count of the chunk rule, each
+    C in the plan ``plan_of(sizes)`` picks; ties go to fewer chunks."""
+    best = None
+    for C in range(1, min(H, max_chunks or H) + 1):
+        sizes = [H // C + (1 if c < H % C else 0) for c in range(C)]   # Sec. 3.3 chunk rule
+        t = plan_time(S, sizes, plan_of(sizes), n_slots, queries_per_wg, t_round, g0, t_copy, beta)
+        if best is None or t < best[1]:
+            best = (sizes, t)
+    return best

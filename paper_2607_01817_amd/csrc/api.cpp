@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdint>
@@ -331,19 +332,40 @@ int plan_size(int C, int mode) {
 // When pooling saves no round, the launches that can carry the neighbouring
 // chunks' copies (d = 128, bf16 storage) run the fused plan, the others the
 // inline one.
-int auto_mode(int S, int d, int dtype, const int *sizes, int C, int n_cu) {
+}  // namespace
+
+// The plan HCMS_MODE_AUTO runs (hcms_auto_mode without validation).
+int hcms::auto_plan(int S, int d, int dtype, const int *sizes, int C, int n_cu) {
     if (C == 1) return HCMS_MODE_SERIAL;
     const int64_t br = hcms::attention_queries_per_block(d);
     const int64_t slots = static_cast<int64_t>(n_cu) * hcms::attention_blocks_per_cu(d);
     const int64_t tiles = (S + br - 1) / br;
     int64_t rounds = 0, total = 0;
+    bool some_idle = false;       // a launch whose last round leaves enough slots idle
+    bool first_idle = false;      // ... for chunk 0's launch in particular
     for (int c = 0; c < C; ++c) {
         const int64_t wc = tiles * sizes[c];
         rounds += (wc + slots - 1) / slots;
         total += wc;
+        const int64_t idle = (slots - wc % slots) % slots;
+        const bool enough = idle >= std::max<int64_t>(1, slots / 8);
+        some_idle = some_idle || enough;
+        if (c == 0) first_idle = enough;
     }
+    // Two lanes pool the chunks' partial rounds: a whole round saved.
     if (rounds > (total + slots - 1) / slots) return HCMS_MODE_LANES;
-    return d == 128 && dtype == HCMS_BF16 ? HCMS_MODE_FUSED : HCMS_MODE_INLINE;
+    // The fused plan moves copies only on CUs a launch's last round leaves
+    // idle; with none anywhere it would run the serial plan's launches.
+    if (d == 128 && dtype == HCMS_BF16) return some_idle ? HCMS_MODE_FUSED : HCMS_MODE_SERIAL;
+    // The inline plan pays four synchronisations to run packs 1..C-1 beside
+    // attention 0's last round: only worth it when that round has idle CUs.
+    return first_idle ? HCMS_MODE_INLINE : HCMS_MODE_SERIAL;
+}
+
+namespace {
+
+int auto_mode(int S, int d, int dtype, const int *sizes, int C, int n_cu) {
+    return hcms::auto_plan(S, d, dtype, sizes, C, n_cu);
 }
 
 // Saves the current device, switches to `dev`, restores on scope exit.

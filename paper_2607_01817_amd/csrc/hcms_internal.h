@@ -41,6 +41,10 @@ inline constexpr unsigned kCopyBesideAttentionLds = 40 * 1024;
 // Tiling of the attention launch: queries per workgroup, and workgroups one
 // CU holds at once, for head dimension d (64 or 128).
 int attention_queries_per_block(int d);
+
+// The plan HCMS_MODE_AUTO runs for these chunks (hcms_auto_mode's rule; the
+// arguments are not validated).
+int auto_plan(int S, int d, int dtype, const int *sizes, int C, int n_cu);
 int attention_blocks_per_cu(int d);
 
 // lse, if not NULL, receives [n_heads][S] fp32 log2 softmax denominators:

@@ -232,31 +232,35 @@ def test_one_gpu_plans_with_one_chunk_are_serial(lib):
 
 # Rounds of attention workgroups, worked by hand for 256 CUs.  d = 128: 256
 # queries per workgroup, one per CU; d = 64: 128 queries, two per CU.
-# Where pooling saves no round, d = 128 bf16 runs the fused plan, the rest
-# the inline one.
+# Where pooling saves no round, d = 128 bf16 runs the fused plan if some
+# launch's last round leaves at least 1/8 of the slots idle, the serial one
+# if none does; the other kernels run the inline plan if chunk 0's launch
+# leaves that many idle, the serial one otherwise.  (want bf16, want fp32)
 @pytest.mark.parametrize("S,d,sizes,want", [
-    (56160, 128, (2, 2, 1), "fused"),         # 220 tiles: 2+2+1 rounds = ceil(1100/256) = 5
-    (56160, 128, (1, 1, 1, 1, 1), "fused"),   # 5 x 1 = ceil(1100/256) = 5
-    (32760, 128, (5, 5), "lanes"),            # 128 tiles: 3+3 = 6 > ceil(1280/256) = 5
-    (32760, 128, (4, 3, 3), "lanes"),         # 2+2+2 = 6 > 5
-    (100000, 128, (10, 10, 10, 10), "lanes"),  # 391 tiles: 4 x 16 = 64 > ceil(15640/256) = 62
-    (100000, 128, (14, 13, 13), "fused"),     # 22+20+20 = 62 = ceil(15640/256)
-    (65536, 128, (2, 2), "fused"),            # 256 tiles: 2+2 = 4 = ceil(1024/256)
-    (4096, 128, (3, 3, 2), "lanes"),          # 16 tiles: 1+1+1 = 3 > ceil(128/256) = 1
-    (4096, 64, (3, 3, 2), "lanes"),           # 32 tiles, 512 slots: 3 > 1
-    (32768, 64, (4, 4), "inline"),            # 256 tiles, 512 slots: 2+2 = 4 = ceil(2048/512)
-    (32768, 64, (3, 5), "lanes"),             # 2+3 = 5 > ceil(2048/512) = 4
-    (56160, 128, (5,), "serial"),             # one chunk
-    (0, 128, (2, 2), "fused"),                # nothing to launch: 0 rounds either way
+    (56160, 128, (2, 2, 1), ("fused", "inline")),   # 220 tiles: 2+2+1 = ceil(1100/256); idle 72, 72, 36
+    (56160, 128, (1, 1, 1, 1, 1), ("fused", "inline")),  # 5 x 1 = 5; idle 36 each
+    (32760, 128, (5, 5), ("lanes",) * 2),           # 128 tiles: 3+3 = 6 > ceil(1280/256) = 5
+    (32760, 128, (4, 3, 3), ("lanes",) * 2),        # 2+2+2 = 6 > 5
+    (32760, 128, (2,) * 5, ("serial",) * 2),        # 256 workgroups each: no idle CU anywhere
+    (100000, 128, (10, 10, 10, 10), ("lanes",) * 2),  # 391 tiles: 4 x 16 = 64 > ceil(15640/256) = 62
+    (100000, 128, (14, 13, 13), ("fused", "inline")),  # 22+20+20 = 62; chunk 0 idles 158
+    (65536, 128, (2, 2), ("serial",) * 2),          # 256 tiles: 512 workgroups, no idle CU
+    (4096, 128, (3, 3, 2), ("lanes",) * 2),         # 16 tiles: 1+1+1 = 3 > ceil(128/256) = 1
+    (4096, 64, (3, 3, 2), ("lanes",) * 2),          # 32 tiles, 512 slots: 3 > 1
+    (32768, 64, (4, 4), ("serial",) * 2),           # 256 tiles, 512 slots: 2+2 = 4, no idle slot
+    (32768, 64, (3, 5), ("lanes",) * 2),            # 2+3 = 5 > ceil(2048/512) = 4
+    (8192, 64, (9, 16), ("inline",) * 2),           # 64 tiles: 576 + 1024 = 2+2 = ceil(1600/512); chunk 0 idles 448
+    (8192, 64, (16, 9), ("serial",) * 2),           # chunk 0 fills two rounds exactly
+    (56160, 128, (5,), ("serial",) * 2),            # one chunk
+    (0, 128, (2, 2), ("serial",) * 2),              # nothing to launch
 ])
 def test_auto_mode_by_rounds(lib, S, d, sizes, want):
     modes = {"serial": hcms.MODE_SERIAL, "inline": hcms.MODE_INLINE, "lanes": hcms.MODE_LANES,
              "fused": hcms.MODE_FUSED}
-    assert hcms.auto_mode(S, d, sizes, 256) == modes[want]
+    assert hcms.auto_mode(S, d, sizes, 256) == modes[want[0]]
     # fp32 storage takes the register-staged kernel, whose launches carry no
-    # copies: inline where bf16 would be fused.
-    fp32 = hcms.auto_mode(S, d, sizes, 256, dtype=hcms.FP32)
-    assert fp32 == (hcms.MODE_INLINE if want == "fused" else modes[want])
+    # copies: the inline plan in their place.
+    assert hcms.auto_mode(S, d, sizes, 256, dtype=hcms.FP32) == modes[want[1]]
 
 
 def test_auto_mode_validation(lib):

@@ -25,6 +25,14 @@ MUTANTS = {
     "integer optimum ignores the overhead": ("(t_comm / c + c * beta, c)", "(t_comm / c, c)"),
     "fit basis C instead of 1 / C": ("A = np.stack([np.ones_like(c), 1.0 / c, c], axis=1)",
                                      "A = np.stack([np.ones_like(c), c, c * c], axis=1)"),
+    "partial round costs a full one": ("return full + g0 + (1.0 - g0) * f", "return full + 1.0"),
+    "partial round costs only its busy share": ("return full + g0 + (1.0 - g0) * f",
+                                                "return full + f"),
+    "lanes do not pool the rounds": ("attn = launch_rounds(sum(W), n_slots, g0)",
+                                     "attn = sum(launch_rounds(w, n_slots, g0) for w in W)"),
+    "serial plan moves only the unpacks": ("copies = 4 * H ", "copies = H "),
+    "one synchronisation per chunk": ("PIPELINED: 2 * C + 3", "PIPELINED: C + 3"),
+    "fused launches always carry": ("if idle >= max(1, n_slots // 8):", "if True:"),
 }
 
 PINS = [
@@ -35,6 +43,10 @@ PINS = [
     pins.test_speedup_is_baseline_over_hcms_time,
     pins.test_one_chunk_pays_only_its_overhead,
     pins.test_fit_recovers_planted_parameters,
+    pins.test_theory_validation_row_predicts_five_chunks,
+    pins.test_round_identity,
+    pins.test_one_gpu_model_reduces_to_the_paper_model,
+    pins.test_worked_rounds_of_the_wan_p4_share,
 ]
 
 
