@@ -460,6 +460,45 @@ def layer_step(ctx, lw, chunks, reps: int, dev):
     return res
 
 
+def one_chunk_roofline(ctx, w, qd, kd, vd, out, ws, steps: int, warmup: int):
+    """The attention roofline of the workload in one chunk of all heads (the
+    serial plan: pack, one attention launch, unpack): the timed steps' step
+    time minus the step's copy kernels (timed in a second pass with events
+    around every kernel), over the launch's FLOPs."""
+    sizes = (w.H,)
+
+    def step():
+        ctx.forward(qd, kd, vd, w.P, w.scale, sizes, mode=hcms.MODE_SERIAL, out=out, workspaces=ws)
+
+    for _ in range(warmup):
+        step()
+    main_stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(main_stream)
+    for _ in range(steps):
+        step()
+    t1.record(main_stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    ctx.set_timing(steps)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    attn = ctx.kernel_ms(hcms.OP_ATTENTION)
+    copies = (sum(ctx.kernel_ms(hcms.OP_PACK)) + sum(ctx.kernel_ms(hcms.OP_UNPACK))) / steps
+    ctx.set_timing(0)
+    achieved = w.flops / ((ms - copies) * 1e-3) / 1e12
+    ev = w.flops / (statistics.mean(attn) * 1e-3) / 1e12
+    return {"chunks": list(sizes), "plan": "serial", "ms_per_step": round(ms, 4),
+            "achieved": round(achieved, 2), "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "events_pass_frac": round(ev / MFMA_BF16_PEAK_TFLOPS, 4),
+            "avg_launch_ms_events": round(statistics.mean(attn), 4),
+            "note": f"{steps} timed steps after {warmup} warm-up steps; achieved = 4 S^2 H d over "
+                    f"the step minus its pack and unpack kernels ({copies:.4f} ms)"}
+
+
 def trace_summary(trace_csv: str, line_path: str) -> str:
     """Markdown summary of a rocprofv3 kernel trace (``--kernel-trace
     --output-format csv``) of one bench.py run, checked against the JSON line
@@ -690,6 +729,9 @@ def main():
                         f"events), {len(attn_ms)} launches"},
         },
     }
+    if tuple(sizes) != (w.H,):
+        result["roofline"]["one_chunk"] = one_chunk_roofline(ctx, w, qd, kd, vd, out, ws,
+                                                             args.steps, max(args.warmup, 20))
     if plain_ms:
         plain = sum(launch_flops) / (sum(plain_ms) * 1e-3) / 1e12
         result["roofline"]["plain_launch"] = {

@@ -22,6 +22,8 @@ time fixed):
   workgroups on n slots: floor(W / n) full rounds plus, when n does not
   divide W, one partial round with a fraction f of the slots busy lasting
   g0 + (1 - g0) f of a full one;
+* :func:`tail_ways`      how many workgroups share each tile of a launch's
+  last round when the kernel splits it by key segments;
 * :func:`plan_time`      that attention time summed over the launches (the
   lanes plan pools the chunks' workgroups), plus the copies a plan leaves on
   the critical path times t_copy, plus its synchronisations times beta;
@@ -74,21 +76,38 @@ def fit(chunk_counts, times) -> tuple[float, float, float]:
 SERIAL, PIPELINED, INLINE, LANES, AUTO, SLOTS, FUSED = 0, 1, 2, 3, 4, 5, 6
 
 
-def launch_rounds(W: int, n: int, g0: float) -> float:
+def launch_rounds(W: int, n: int, g0: float, ways: int = 1) -> float:
     """Full rounds of a launch of W workgroups on n slots, the last one
     counted as g0 + (1 - g0) f of a round when only a fraction f of the slots
-    has work."""
+    has work.  With its last round's tiles split ``ways`` = 2 or 3 ways by key
+    segments, that round holds ways times as many workgroups, each doing a
+    share of the work: it lasts 2/3 (two ways: segments 0-1 and 2) or 1/3
+    (three ways) as long."""
     full, rem = divmod(W, n)
     if rem == 0:
         return float(full)
-    f = rem / n
-    return full + g0 + (1.0 - g0) * f
+    f = rem * ways / n
+    length = {1: 1.0, 2: 2.0 / 3.0, 3: 1.0 / 3.0}[ways]
+    return full + length * (g0 + (1.0 - g0) * f)
+
+
+def tail_ways(W: int, n: int, S: int, split: bool) -> int:
+    """How many workgroups share each tile of a launch's last round: 3 when
+    three times its rem = W mod n tiles fit in one round, else 2 when twice
+    do, else 1; only when ``split`` (a kernel that splits) and the keys span
+    at least 12 blocks of 64 (three segments)."""
+    rem = W % n
+    if not split or rem == 0 or -(-S // 64) < 12:
+        return 1
+    return 3 if 3 * rem <= n else 2 if 2 * rem <= n else 1
 
 
 def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_round: float,
-              g0: float, t_copy: float, beta: float) -> float:
+              g0: float, t_copy: float, beta: float, split: bool = False) -> float:
     """Model time of one plan of the chunk sizes ``sizes`` on one GPU with
-    ``n_slots`` attention workgroups per round of ``queries_per_wg`` queries."""
+    ``n_slots`` attention workgroups per round of ``queries_per_wg`` queries;
+    ``split``: the attention kernel splits its launches' last rounds (the
+    lanes plan keeps every tile whole)."""
     sizes = list(sizes)
     C, H = len(sizes), sum(sizes)
     tiles = -(-S // queries_per_wg)
@@ -98,14 +117,15 @@ def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_rou
     if mode == LANES:
         attn = launch_rounds(sum(W), n_slots, g0)
     else:
-        attn = sum(launch_rounds(w, n_slots, g0) for w in W)
+        attn = sum(launch_rounds(w, n_slots, g0, tail_ways(w, n_slots, S, split)) for w in W)
     if mode == SERIAL:
         copies = 4 * H                    # 3 tensors packed, 1 unpacked, per head
     else:
         copies = 3 * sizes[0] + sizes[-1]
         if mode == FUSED:
             for c, w in enumerate(W):
-                idle = (n_slots - w % n_slots) % n_slots
+                w_run = (w - w % n_slots) + (w % n_slots) * tail_ways(w, n_slots, S, split)
+                idle = (n_slots - w_run % n_slots) % n_slots
                 if idle >= max(1, n_slots // 8):
                     continue              # this launch carries its neighbours' copies
                 if c + 1 < C:
@@ -117,13 +137,15 @@ def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_rou
 
 
 def choose_chunks(S: int, H: int, plan_of, n_slots: int, queries_per_wg: int, t_round: float,
-                  g0: float, t_copy: float, beta: float, max_chunks: int | None = None):
+                  g0: float, t_copy: float, beta: float, max_chunks: int | None = None,
+                  split: bool = False):
     """(sizes, model time) of the fastest chunk count of the chunk rule, each
     C in the plan ``plan_of(sizes)`` picks; ties go to fewer chunks."""
     best = None
     for C in range(1, min(H, max_chunks or H) + 1):
         sizes = [H // C + (1 if c < H % C else 0) for c in range(C)]   # Sec. 3.3 chunk rule
-        t = plan_time(S, sizes, plan_of(sizes), n_slots, queries_per_wg, t_round, g0, t_copy, beta)
+        t = plan_time(S, sizes, plan_of(sizes), n_slots, queries_per_wg, t_round, g0, t_copy, beta,
+                      split)
         if best is None or t < best[1]:
             best = (sizes, t)
     return best

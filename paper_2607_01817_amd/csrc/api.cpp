@@ -347,7 +347,10 @@ int hcms::auto_plan(int S, int d, int dtype, const int *sizes, int C, int n_cu) 
         const int64_t wc = tiles * sizes[c];
         rounds += (wc + slots - 1) / slots;
         total += wc;
-        const int64_t idle = (slots - wc % slots) % slots;
+        // The workgroups the launch runs: its last round's tiles may be split.
+        const int64_t rem = wc % slots;
+        const int64_t run = wc - rem + rem * hcms::attention_split_ways(wc, S, d, dtype, n_cu);
+        const int64_t idle = (slots - run % slots) % slots;
         const bool enough = idle >= std::max<int64_t>(1, slots / 8);
         some_idle = some_idle || enough;
         if (c == 0) first_idle = enough;
@@ -402,7 +405,8 @@ int run_attention(const void *q, const void *k, const void *v, void *out, float 
         const hipError_t e = hcms::launch_attention(
             static_cast<const char *>(q) + off, static_cast<const char *>(k) + off,
             static_cast<const char *>(v) + off, static_cast<char *>(out) + off,
-            lse ? lse + static_cast<int64_t>(h0) * S : nullptr, S, chunk_sizes[i], d, c, dtype, stream);
+            lse ? lse + static_cast<int64_t>(h0) * S : nullptr, S, chunk_sizes[i], d, c, dtype,
+            nullptr, stream);
         if (e != hipSuccess) return hip_fail(e, "attention launch");
         h0 += chunk_sizes[i];
     }
@@ -437,6 +441,12 @@ struct hcms_ctx {
     std::vector<hipEvent_t> t_begin;     // [call][kind][chunk] timing events
     std::vector<hipEvent_t> t_end;
     std::vector<int> timed_chunks;       // chunk count of each timed call
+    // Scratch that lets an attention launch split its last round of tiles:
+    // one region for launches on the main stream, one for the compute stream
+    // (launches on one stream are ordered, so each region serves one launch
+    // at a time).  No region: every tile whole, with the same results.
+    void *split_mem = nullptr;
+    hcms::SplitScratch split[2] = {};
 };
 
 namespace {
@@ -663,6 +673,14 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
         return static_cast<char *>(p) + head_bytes * first;
     };
     const auto beside = copy_lds_reserve(mode, f.n_chunks);
+    // The split scratch of the stream an attention launch runs on.  Lanes
+    // keep every tile whole: their two launches already share the rounds.
+    auto split_for = [&](hipStream_t s) -> const hcms::SplitScratch * {
+        if (mode == HCMS_MODE_LANES) return nullptr;
+        const int r = s == static_cast<hipStream_t>(f.main_stream) ? 0
+                      : s == static_cast<hipStream_t>(f.compute_stream) ? 1 : -1;
+        return r >= 0 && f.ctx->split[r].part ? &f.ctx->split[r] : nullptr;
+    };
     auto launch = [&](int kind, int c, int h0, int hc, hipStream_t s) -> hipError_t {
         if (kind == HCMS_OP_PACK) {
             const void *src[3] = {f.q_seq, f.k_seq, f.v_seq};
@@ -673,7 +691,7 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
             return hcms::launch_attention(at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0),
                                           at(f.o_hm, c, h0),
                                           f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr,
-                                          f.S, hc, f.d, c_log2e, f.dtype, s);
+                                          f.S, hc, f.d, c_log2e, f.dtype, split_for(s), s);
         const void *src[1] = {at(f.o_hm, c, h0)};
         void *dst[1] = {f.o_seq};
         return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, beside(kind, c), s);
@@ -706,7 +724,7 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
         return hcms::launch_attention_riding(
             at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0), at(f.o_hm, c, h0),
             f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr, f.S, hc, f.d, c_log2e,
-            f.dtype, cp, n, f.H, f.ctx->n_cu, riding, s);
+            f.dtype, cp, n, f.H, f.ctx->n_cu, split_for(s), riding, s);
     };
     return execute_plan(f.ctx, mode, f.chunk_sizes, f.n_chunks, f.main_stream, f.copy_stream,
                         f.compute_stream, launch, ride);
@@ -1102,6 +1120,32 @@ int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out) {
         }
         ctx->events.push_back(ev);
     }
+    // Split scratch, two regions of n_cu slots and n_cu counters each.  If it
+    // cannot be had, launches keep every tile whole (same results).
+    {
+        const int64_t slot = hcms::attention_split_slot_bytes();
+        const int64_t n = ctx->n_cu;
+        const int64_t region = n * slot + n * 4;
+        void *mem = nullptr;
+        if (hipMalloc(&mem, 2 * region) == hipSuccess && mem) {
+            if (hipMemset(mem, 0, 2 * region) == hipSuccess) {
+                ctx->split_mem = mem;
+                for (int r = 0; r < 2; ++r) {
+                    char *base = static_cast<char *>(mem) + r * region;
+                    hcms::SplitScratch &sp = ctx->split[r];
+                    sp.part = base;
+                    sp.ml = base + n * (slot - 256 * 16);
+                    sp.count = reinterpret_cast<int *>(base + n * slot);
+                    sp.slots = static_cast<int>(n);
+                    sp.counters = static_cast<int>(n);
+                    sp.n_cu = ctx->n_cu;
+                }
+            } else {
+                (void)hipFree(mem);
+            }
+        }
+        (void)hipGetLastError();
+    }
     *out = ctx;
     return ok();
 }
@@ -1112,6 +1156,7 @@ int hcms_ctx_destroy(hcms_ctx *ctx) {
     for (hipEvent_t ev : ctx->events) (void)hipEventDestroy(ev);
     for (hipEvent_t ev : ctx->t_begin) (void)hipEventDestroy(ev);
     for (hipEvent_t ev : ctx->t_end) (void)hipEventDestroy(ev);
+    if (ctx->split_mem) (void)hipFree(ctx->split_mem);
     delete ctx;
     return ok();
 }

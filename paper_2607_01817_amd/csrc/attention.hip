@@ -203,14 +203,17 @@ __device__ inline float halves_max(float x) {
 // sum over the 64 keys exceeds this bound.
 constexpr float kRaiseBound = 256.0f;
 
-// Keys at or past `kvalid` inside the block get the score -inf.
+// Keys at or past `kvalid` inside the block get the score -inf.  Key
+// mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3) is compared as its constant part
+// against kvalid - 4 g, so no per-lane key indices need registers.
 __device__ inline void mask_block(f32x16 (&s)[2], int g, int kvalid) {
+    const int kv = kvalid - g * 4;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int key = mt * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-            if (key >= kvalid) s[mt][r] = -INFINITY;
+            const int key = mt * 32 + (r >> 2) * 8 + (r & 3);
+            if (key >= kv) s[mt][r] = -INFINITY;
         }
 }
 
@@ -536,15 +539,35 @@ constexpr int kD = 128;
 constexpr int kWaves = 8;
 constexpr int kRowB = kD * 2;                          // bytes per key row
 constexpr int kTileB = kBC * kRowB;                    // one 64-key block: 16 KiB
-constexpr int kNB = 4;                                 // LDS buffers per tensor
+constexpr int kNB = 3;                                 // LDS buffers per tensor
 constexpr int kPerWave = kTileB / (64 * 16) / kWaves;  // DMA instructions per wave and block
-#ifndef HCMS_ATTN_DIST
-#define HCMS_ATTN_DIST 3
-#endif
 // Steps between a block's load and the step that reads it.
-constexpr int kDist = HCMS_ATTN_DIST;
+constexpr int kDist = 2;
 static_assert(kDist >= 1 && kDist + 1 <= kNB, "more blocks in flight than LDS buffers");
 static_assert(kPerWave == 2, "the wait counts below assume two DMA instructions per block");
+
+// Key segments.  Every query visits its keys as kSeg fixed segments of whole
+// blocks (one segment when the sequence has fewer than kSegMinBlocks blocks),
+// each an online softmax of its own, and the segments' states are merged in a
+// fixed order (merge_states).  The boundaries depend only on S, so the
+// arithmetic of a query never depends on which workgroups computed which
+// segments: a tile may be computed whole by one workgroup or split over
+// several, with bit-identical results.
+constexpr int kSeg = 3;
+constexpr int kSegMinBlocks = 12;
+__host__ __device__ inline int n_segments(int nkb) { return nkb >= kSegMinBlocks ? kSeg : 1; }
+// First block of segment g (g = n_segments: one past the last block).
+__host__ __device__ inline int seg_begin(int nkb, int g) {
+    const int n = n_segments(nkb);
+    return g <= 0 ? 0 : g >= n ? nkb : (g * nkb + n / 2) / n;
+}
+// A segment's unnormalised output, rounded to bf16, kept in LDS between
+// segments: 64 values per lane, chunk k (values 8k .. 8k + 7) of lane l of
+// wave w at byte w * 8 KiB + k * 1 KiB + 16 l.  Partial states of split tiles
+// use the same layout in global memory.
+constexpr int kStashWaveB = 64 * 64 * 2;
+constexpr int kStashB = kWaves * kStashWaveB;           // 64 KiB
+constexpr int kLdsB = 2 * kNB * kTileB + kStashB;       // 160 KiB, all of a CU's LDS
 
 // Score operands: S^T[i & 1] += K rows 32 (i & 1) + li, chunk 2 (i >> 1) + g,
 // times Q^T; `k_rd[i >> 1]` is the lane's byte offset of its row and chunk.
@@ -673,7 +696,6 @@ struct Riders {
     RiderJob job[2];
     int64_t S, H;
     unsigned n_jobs, bx;  // bx = copy::blocks_x(S, 4)
-    unsigned n_attn;      // attention workgroups in front of the riders
 };
 
 // Rows of d = 128 bf16 elements: 256 bytes = 16 units of 16 bytes.
@@ -696,29 +718,151 @@ __device__ inline void run_riders(const Riders &r, unsigned rider, unsigned n_ri
     }
 }
 
+// Tiles split over several workgroups (the launch's last, partial round of
+// tiles; see plan_split).  Workgroup n_whole + u computes segments of tile
+// n_whole + u % n_split: with 3 ways segment u / n_split, with 2 ways
+// segments 0-1 (u < n_split) or 2.  Each writes its partial state to slot
+// u (the normalised output in the stash layout, and (m, l, E) per query)
+// and counts itself in on its tile's counter; the last to arrive merges the
+// tile's partial states in segment order, writes the output and sets the
+// counter back to zero.
+struct TailSplit {
+    char *part;      // n_split * ways slots of kStashB bytes
+    float4 *ml;      // n_split * ways slots of 256 (m, l, E, 0) per query
+    int *count;      // n_split counters, zero between launches
+    int n_whole;     // tiles computed whole by one workgroup: the first n_whole
+    int n_split;     // tiles split: the last n_split
+    int ways;        // 2 or 3
+};
+
+// The state of a query after some of its key segments: the maximum m of its
+// raw scores, the row sum l of exp2(c (s - m)), and the normalised output N
+// (this lane's 64 values of it).  Between segments a state is kept in 16 bits
+// per value: N scaled by 2^-E, E the binary exponent of the query's largest
+// |N| (over both halves of the wave), rounded to fp16 (nearest-even), so a
+// stored value keeps 11 significant bits relative to the query's largest.
+// quantise applies exactly that rounding in registers; store_state and
+// load_state move the rounded values through LDS or global memory unchanged.
+__device__ inline int state_exponent(const f32x16 (&n)[4]) {
+    float a = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) a = fmaxf(a, fabsf(n[dt][r]));
+    return __builtin_amdgcn_frexp_expf(halves_max(a));   // max = f 2^E, f in [0.5, 1)
+}
+__device__ inline void quantise(f32x16 (&n)[4], int E) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            n[dt][r] = __builtin_ldexpf(static_cast<float>(static_cast<_Float16>(__builtin_ldexpf(n[dt][r], -E))), E);
+}
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+// Chunk k (values 8k .. 8k + 7) of lane l at base + k * 1 KiB + 16 l.  The
+// pointers come from the stash or the split scratch; the compiler infers LDS
+// or global after inlining.
+__device__ inline void store_state(char *base, const f32x16 (&n)[4], int E, int lane) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        f16x8 h;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            h[i] = static_cast<_Float16>(__builtin_ldexpf(n[k >> 1][(k & 1) * 8 + i], -E));
+        *reinterpret_cast<f16x8 *>(base + k * 1024 + 16 * lane) = h;
+    }
+}
+__device__ inline void load_state(f32x16 (&n)[4], const char *base, int E, int lane) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const f16x8 h = *reinterpret_cast<const f16x8 *>(base + k * 1024 + 16 * lane);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) n[k >> 1][(k & 1) * 8 + i] = __builtin_ldexpf(static_cast<float>(h[i]), E);
+    }
+}
+
+// The state of one segment from its online softmax: N = O / l, in place.
+__device__ inline void segment_state(f32x16 (&o)[4], float l) {
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[dt][r] *= inv;
+}
+
+// Canonical merge of two states of one query (A of the earlier segments, B
+// of the later): the merged maximum and row sum, and the weights of A's and
+// B's normalised outputs, N = fma(N_A, wa, N_B * wb) element by element.
+__device__ inline void merge_weights(float mA, float lA, float mB, float lB, float c, float &m,
+                                     float &l, float &wa, float &wb) {
+    m = fmaxf(mA, mB);
+    const float a = __builtin_amdgcn_exp2f((mA - m) * c) * lA;
+    const float b = __builtin_amdgcn_exp2f((mB - m) * c) * lB;
+    l = a + b;
+    const float inv = 1.0f / l;
+    wa = a * inv;
+    wb = b * inv;
+}
+// Merges a stored state (chunk k of lane l at base + k * 1 KiB + 16 l, scale
+// 2^E) into this lane's 64 values n, chunk by chunk: stored_is_a says whether
+// the stored state is A (the earlier segments) or B.
+__device__ inline void merge_stored(f32x16 (&n)[4], const char *base, int E, int lane, float wa,
+                                    float wb, bool stored_is_a) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const f16x8 h = *reinterpret_cast<const f16x8 *>(base + k * 1024 + 16 * lane);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float x = __builtin_ldexpf(static_cast<float>(h[i]), E);
+            const float y = n[k >> 1][(k & 1) * 8 + i];
+            n[k >> 1][(k & 1) * 8 + i] = stored_is_a ? __builtin_fmaf(x, wa, y * wb) : __builtin_fmaf(y, wa, x * wb);
+        }
+    }
+}
+
 template <bool kRiders>
 __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_dma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
-    __bf16 *__restrict__ o, float *__restrict__ lse, int S, int n_qtiles, float c, Riders riders) {
+    __bf16 *__restrict__ o, float *__restrict__ lse, int S, int n_qtiles, float c, TailSplit tail,
+    Riders riders) {
     using namespace dma;
+    const int n_attn = tail.n_whole + tail.n_split * tail.ways;
     if constexpr (kRiders) {
-        if (blockIdx.x >= riders.n_attn) {
-            run_riders(riders, blockIdx.x - riders.n_attn, gridDim.x - riders.n_attn);
+        if (blockIdx.x >= static_cast<unsigned>(n_attn)) {
+            run_riders(riders, blockIdx.x - n_attn, gridDim.x - n_attn);
             return;
         }
     }
     constexpr int D = kD, KK = D / 16, DT = D / 32;
-    __shared__ __attribute__((aligned(1024))) char lds[2 * kNB * kTileB];
+    __shared__ __attribute__((aligned(1024))) char lds[kLdsB];
     const char *const kbase = lds;                  // K buffer b at kbase + b * kTileB
     const char *const vbase = lds + kNB * kTileB;   // V buffer b at vbase + b * kTileB
+    char *const stash = lds + 2 * kNB * kTileB;
 
-    // XCD-aware tile order, as in attention_kernel.
-    const int nb = kRiders ? static_cast<int>(riders.n_attn) : static_cast<int>(gridDim.x);
+    // Which tile, and which of its segments.  Whole tiles: XCD-aware order,
+    // workgroup b runs on XCD b % 8 and each XCD takes a contiguous range of
+    // (head, query tile) pairs, so concurrent workgroups of an XCD stream the
+    // same K/V blocks through its L2.
     const int b = blockIdx.x;
-    const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
-    const int logical = xcd * per + min(xcd, rem) + (b >> 3);
+    int logical, split_u = -1;
+    if (b < tail.n_whole) {
+        const int nb = tail.n_whole;
+        const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
+        logical = xcd * per + min(xcd, rem) + (b >> 3);
+    } else {
+        split_u = b - tail.n_whole;
+        logical = tail.n_whole + split_u % tail.n_split;
+    }
     const int head = logical / n_qtiles;
     const int qtile = logical - head * n_qtiles;
+    const int nkb = (S + kBC - 1) / kBC;
+    const int nseg = n_segments(nkb);
+    int g_first = 0, g_last = nseg;
+    if (split_u >= 0) {
+        const int p = split_u / tail.n_split;
+        g_first = tail.ways == 3 ? p : 2 * p;
+        g_last = tail.ways == 3 ? p + 1 : (p == 0 ? 2 : 3);
+    }
 
     const int64_t hoff = static_cast<int64_t>(head) * S * D;
     const int64_t hbytes = static_cast<int64_t>(S) * D * 2;
@@ -768,163 +912,254 @@ __global__ __launch_bounds__(64 * dma::kWaves, dma::kWaves / 4) void attention_d
     for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(v_rd[dt]));
     const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<uintptr_t>(lds));
     const unsigned wave_dst = lds0 + kPerWave * wave * 1024;
-    auto issue_k = [&](int blk) {
-        const unsigned dst = wave_dst + (blk & (kNB - 1)) * kTileB;
-#pragma unroll
-        for (int i = 0; i < kPerWave; ++i) load_lds(dst + i * 1024, kr, k_src[i], blk * kTileB);
-    };
-    auto issue_v = [&](int blk) {
-        const unsigned dst = wave_dst + (kNB + (blk & (kNB - 1))) * kTileB;
-#pragma unroll
-        for (int i = 0; i < kPerWave; ++i) load_lds(dst + i * 1024, vr, v_src[i], blk * kTileB);
-    };
 
     f32x16 oacc[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
-    const int nkb = (S + kBC - 1) / kBC;
+    float m = 0.f, mc = 0.f, lsum = 0.f;
 
-    // Prologue: K_0, V_0, ..., K_{kDist-1}, V_{kDist-1}, K_kDist in flight;
-    // step j then issues K_{j+1+kDist} and V_{j+kDist} (blocks past the end
-    // read as zeros and are never used).
+    // One segment: blocks blk0 .. blk0 + nb - 1 of the keys, an online softmax
+    // starting afresh (its first block sets the running maximum).  Leaves the
+    // segment's unnormalised output in oacc, its maximum in m and this lane's
+    // share of its row sum in lsum.  Block j of the segment (relative index)
+    // sits in LDS buffer j % kNB.
+    auto segment = [&](const int blk0, const int nb) {
+        auto issue_k = [&](int j) {
+            const unsigned dst = wave_dst + (j % kNB) * kTileB;
 #pragma unroll
-    for (int blk = 0; blk <= kDist; ++blk) {
-        issue_k(blk);
-        if (blk < kDist) issue_v(blk);
-    }
-    wait_vm<4 * kDist>();  // K_0 landed
-    __syncthreads();
-    f32x16 sa[2], sb[2];
-    qk(sa, kbase, k_rd, qreg);
-    wait_vm<4 * kDist - 4>();  // V_0 and K_1 landed
-    __syncthreads();           // and every wave is done with K_0's buffer
-
-    // Block 0 sets the running maximum; the lazy rescaling is that of
-    // attention_kernel.  The exponentials of block j are split over two
-    // steps: keys 0-31 (tile 0) during the PV of block j - 1, keys 32-63
-    // (tile 1) during the scores of block j + 1, followed by the overflow test
-    // of block j.  So both phases of a step carry half of the VALU work next to
-    // their 16 MFMAs.  lo[j & 1] holds tile 0 of block j's P, hi tile 1; s0 the
-    // row sum over tile 0 (continued by tile 1 in exp_block's order).
-    float m, mc, lsum, s0 = 0.f;
-    bf16x8 lo[2][2], hi[2];
-    if (nkb == 1) mask_block(sa, g, S);
-    m = block_max(sa);
-    mc = m * c;
-    lsum = exp_half(sa[1], c, mc, hi[0], hi[1], exp_half(sa[0], c, mc, lo[0][0], lo[0][1], 0.f));
-
-    bf16x8 vpre[kVAhead];
-    // Tile 1 of block j (scores s, tile 0 already in lo_j with sum s0), the
-    // overflow test and, when some query needs it, the recompute branch.
-    auto finish = [&](const f32x16(&s)[2], bf16x8(&lo_j)[2], const char *vb) {
-        float bsum = exp_half(s[1], c, mc, hi[0], hi[1], s0);
-        pv_prefetch(vpre, vb, v_rd);
-        interleave_qk();
-        const bool up = halves_sum(bsum) > kRaiseBound;
-        if (__any(up)) {
-            const float mx = block_max(s);
-            const float m_new = up ? mx : m;
-            const float alpha = up ? __builtin_amdgcn_exp2f((m - mx) * c) : 1.0f;
-            m = m_new;
-            mc = m_new * c;
-            bsum = exp_half(s[1], c, mc, hi[0], hi[1], exp_half(s[0], c, mc, lo_j[0], lo_j[1], 0.f));
-            lsum *= alpha;
+            for (int i = 0; i < kPerWave; ++i) load_lds(dst + i * 1024, kr, k_src[i], (blk0 + j) * kTileB);
+        };
+        auto issue_v = [&](int j) {
+            const unsigned dst = wave_dst + (kNB + j % kNB) * kTileB;
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
+            for (int i = 0; i < kPerWave; ++i) load_lds(dst + i * 1024, vr, v_src[i], (blk0 + j) * kTileB);
+        };
 #pragma unroll
-                for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+        // Prologue: K_0, V_0, ..., K_{kDist-1}, V_{kDist-1}, K_kDist in
+        // flight; step j then issues K_{j+1+kDist} and V_{j+kDist} (blocks
+        // past the segment are loaded but never used; past S they read as
+        // zeros).
+#pragma unroll
+        for (int j = 0; j <= kDist; ++j) {
+            issue_k(j);
+            if (j < kDist) issue_v(j);
         }
-        lsum += bsum;
-    };
-    // PV of block j beside tile 0 of block j + 1 (scores sn, already masked
-    // when block j + 1 is the last one).
-    auto pv_next = [&](const bf16x8(&lo_j)[2], const char *vb, f32x16(&sn)[2], bf16x8(&lo_n)[2]) {
-        pv(oacc, lo_j, hi, vb, v_rd, vpre);
-        s0 = exp_half(sn[0], c, mc, lo_n[0], lo_n[1], 0.f);
-        interleave_pv();
-    };
-
-    // Step j: K_{j+1} is in buffer (j + 1) % kNB, V_j in buffer j % kNB.
-    // Block j + 1 is masked when it is the last one; the steady-state steps
-    // (all but the last) never are, so they carry no masking code.
-    auto step = [&](int j, auto ph, auto first, auto last, f32x16(&scur)[2], f32x16(&snext)[2],
-                    bf16x8(&lo_j)[2], bf16x8(&lo_n)[2]) {
-        // P: j % kNB, or -1 when only known at run time (one step per workgroup);
-        // step 0 has no exponentials left to finish (block 0 took them all).
-        constexpr int P = decltype(ph)::value;
-        const int kb = P >= 0 ? (P + 1) % kNB : (j + 1) % kNB;
-        const int vb = P >= 0 ? P : j % kNB;
-        issue_k(j + 1 + kDist);
-        issue_v(j + kDist);
-        qk(snext, kbase + kb * kTileB, k_rd, qreg);
-        if constexpr (decltype(first)::value) pv_prefetch(vpre, vbase, v_rd);
-        else finish(scur, lo_j, vbase + vb * kTileB);
-        if constexpr (decltype(last)::value) mask_block(snext, g, S - (j + 1) * kBC);
-        pv_next(lo_j, vbase + vb * kTileB, snext, lo_n);
-        wait_vm<4 * (kDist - 1)>();  // K_{j+2} and V_{j+1} landed
+        wait_vm<4 * kDist>();  // K_0 landed
         __syncthreads();
-    };
-    using Last = std::true_type;
-    using NotLast = std::false_type;
-    using First = std::true_type;
-    using Next = std::false_type;
-    if (nkb > 1) {
-        // Step 0: block 0's PV and block 1's scores.
-        if (nkb == 2) step(0, Phase<0>{}, First{}, Last{}, sa, sb, lo[0], lo[1]);
-        else step(0, Phase<0>{}, First{}, NotLast{}, sa, sb, lo[0], lo[1]);
-        int j = 1;
-        for (; j + 5 < nkb; j += 4) {
-            step(j, Phase<1>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
-            step(j + 1, Phase<2>{}, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
-            step(j + 2, Phase<3>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
-            step(j + 3, Phase<0>{}, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
-        }
-        if (j + 2 < nkb) {
-            step(j, Phase<1>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
-            ++j;
-            if (j + 2 < nkb) {
-                step(j, Phase<2>{}, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
+        f32x16 sa[2], sb[2];
+        qk(sa, kbase, k_rd, qreg);
+        wait_vm<4 * kDist - 4>();  // V_0 and K_1 landed
+        __syncthreads();           // and every wave is done with K_0's buffer
+
+        // The first block sets the running maximum; the lazy rescaling is that
+        // of attention_kernel.  The exponentials of block j are split over two
+        // steps: keys 0-31 (tile 0) during the PV of block j - 1, keys 32-63
+        // (tile 1) during the scores of block j + 1, followed by the overflow
+        // test of block j.  So both phases of a step carry half of the VALU
+        // work next to their 16 MFMAs.  lo[j & 1] holds tile 0 of block j's P,
+        // hi tile 1; s0 the row sum over tile 0 (continued by tile 1 in
+        // exp_block's order).
+        float s0 = 0.f;
+        bf16x8 lo[2][2], hi[2];
+        if (nb == 1) mask_block(sa, g, S - blk0 * kBC);
+        m = block_max(sa);
+        mc = m * c;
+        lsum = exp_half(sa[1], c, mc, hi[0], hi[1], exp_half(sa[0], c, mc, lo[0][0], lo[0][1], 0.f));
+
+        bf16x8 vpre[kVAhead];
+        // Tile 1 of block j (scores s, tile 0 already in lo_j with sum s0),
+        // the overflow test and, when some query needs it, the recompute
+        // branch.
+        auto finish = [&](const f32x16(&s)[2], bf16x8(&lo_j)[2], const char *vb) {
+            float bsum = exp_half(s[1], c, mc, hi[0], hi[1], s0);
+            pv_prefetch(vpre, vb, v_rd);
+            interleave_qk();
+            const bool up = halves_sum(bsum) > kRaiseBound;
+            if (__any(up)) {
+                const float mx = block_max(s);
+                const float m_new = up ? mx : m;
+                const float alpha = up ? __builtin_amdgcn_exp2f((m - mx) * c) : 1.0f;
+                m = m_new;
+                mc = m_new * c;
+                bsum = exp_half(s[1], c, mc, hi[0], hi[1], exp_half(s[0], c, mc, lo_j[0], lo_j[1], 0.f));
+                lsum *= alpha;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+            }
+            lsum += bsum;
+        };
+        // PV of block j beside tile 0 of block j + 1 (scores sn, already
+        // masked when block j + 1 is the last one of the keys).
+        auto pv_next = [&](const bf16x8(&lo_j)[2], const char *vb, f32x16(&sn)[2], bf16x8(&lo_n)[2]) {
+            pv(oacc, lo_j, hi, vb, v_rd, vpre);
+            s0 = exp_half(sn[0], c, mc, lo_n[0], lo_n[1], 0.f);
+            interleave_pv();
+        };
+
+        // Step j: K_{j+1} is in buffer (j + 1) % kNB, V_j in buffer j % kNB.
+        // The step of the segment's last scores masks them (a no-op unless
+        // that block is the last of the keys); the other steps carry no
+        // masking code.
+        auto step = [&](int j, auto ph, auto first, auto last, f32x16(&scur)[2], f32x16(&snext)[2],
+                        bf16x8(&lo_j)[2], bf16x8(&lo_n)[2]) {
+            // P: j % 6 (buffers j % kNB and the score registers' alternation
+            // j % 2), or -1 when only known at run time.
+            constexpr int P = decltype(ph)::value;
+            const int kb = P >= 0 ? (P + 1) % kNB : (j + 1) % kNB;
+            const int vb = P >= 0 ? P % kNB : j % kNB;
+            issue_k(j + 1 + kDist);
+            issue_v(j + kDist);
+            qk(snext, kbase + kb * kTileB, k_rd, qreg);
+            if constexpr (decltype(first)::value) pv_prefetch(vpre, vbase, v_rd);
+            else finish(scur, lo_j, vbase + vb * kTileB);
+            if constexpr (decltype(last)::value) mask_block(snext, g, S - (blk0 + j + 1) * kBC);
+            pv_next(lo_j, vbase + vb * kTileB, snext, lo_n);
+            wait_vm<4 * (kDist - 1)>();  // K_{j+2} and V_{j+1} landed
+            __syncthreads();
+        };
+        using Last = std::true_type;
+        using NotLast = std::false_type;
+        using First = std::true_type;
+        using Next = std::false_type;
+        if (nb > 1) {
+            // Step 0: block 0's PV and block 1's scores.
+            if (nb == 2) step(0, Phase<0>{}, First{}, Last{}, sa, sb, lo[0], lo[1]);
+            else step(0, Phase<0>{}, First{}, NotLast{}, sa, sb, lo[0], lo[1]);
+            int j = 1;
+            // Odd steps hold the current block's scores in sb, even ones in sa.
+            auto steady = [&](auto ph) {
+                if constexpr (decltype(ph)::value % 2 == 1)
+                    step(j, ph, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
+                else
+                    step(j, ph, Next{}, NotLast{}, sa, sb, lo[0], lo[1]);
                 ++j;
-                if (j + 2 < nkb) {
-                    step(j, Phase<3>{}, Next{}, NotLast{}, sb, sa, lo[1], lo[0]);
-                    ++j;
+            };
+            while (j + 7 < nb) {
+                steady(Phase<1>{});
+                steady(Phase<2>{});
+                steady(Phase<3>{});
+                steady(Phase<4>{});
+                steady(Phase<5>{});
+                steady(Phase<0>{});
+            }
+            if (j + 2 < nb) {
+                steady(Phase<1>{});
+                if (j + 2 < nb) {
+                    steady(Phase<2>{});
+                    if (j + 2 < nb) {
+                        steady(Phase<3>{});
+                        if (j + 2 < nb) {
+                            steady(Phase<4>{});
+                            if (j + 2 < nb) steady(Phase<5>{});
+                        }
+                    }
                 }
             }
-        }
-        // Block j's scores and tile 0 are in sa and lo[0] when j is even.
-        auto to_odd = [&]() {
-            if ((j & 1) == 0) {
+            // Block j's scores and tile 0 are in sa and lo[0] when j is even.
+            if (j + 1 < nb) {
+                // The step of the last scores (j = nb - 2); it leaves the last
+                // block's scores and tile 0 in sa and lo[0].
+                if ((j & 1) == 0) {
+                    sb[0] = sa[0];
+                    sb[1] = sa[1];
+                    lo[1][0] = lo[0][0];
+                    lo[1][1] = lo[0][1];
+                }
+                step(j, Phase<-1>{}, Next{}, Last{}, sb, sa, lo[1], lo[0]);
+                ++j;
                 sb[0] = sa[0];
                 sb[1] = sa[1];
                 lo[1][0] = lo[0][0];
                 lo[1][1] = lo[0][1];
             }
-        };
-        if (j + 1 < nkb) {
-            // The step of the last scores (j = nkb - 2); it leaves the last
-            // block's scores and tile 0 in sa and lo[0].
-            to_odd();
-            step(j, Phase<-1>{}, Next{}, Last{}, sb, sa, lo[1], lo[0]);
-            ++j;
-            sb[0] = sa[0];
-            sb[1] = sa[1];
-            lo[1][0] = lo[0][0];
-            lo[1][1] = lo[0][1];
+            // Last block of the segment (j = nb - 1) in sb and lo[1].
+            finish(sb, lo[1], vbase + (j % kNB) * kTileB);
+            pv(oacc, lo[1], hi, vbase + (j % kNB) * kTileB, v_rd, vpre);
+        } else {
+            pv_prefetch(vpre, vbase, v_rd);
+            pv(oacc, lo[0], hi, vbase, v_rd, vpre);
         }
-        // Last block (j = nkb - 1, masked) in sb and lo[1].
-        finish(sb, lo[1], vbase + (j % kNB) * kTileB);
-        pv(oacc, lo[1], hi, vbase + (j % kNB) * kTileB, v_rd, vpre);
-    } else {
-        pv_prefetch(vpre, vbase, v_rd);
-        pv(oacc, lo[0], hi, vbase, v_rd, vpre);
-    }
-    wait_vm<0>();  // no load into LDS is pending when the workgroup ends
+        wait_vm<0>();   // no load into LDS is pending
+        __syncthreads();  // every wave is done with the buffers the next segment loads into
+    };
 
     const int qi = q0 + li;
-    const float l = halves_sum(lsum);
-    const float inv = 1.0f / l;
+    char *const my_stash = stash + wave * kStashWaveB;
+    float m_s = 0.f, l_s = 0.f;       // merged state of the segments so far
+    int e_s = 0;
+    bool normalised = false;          // oacc holds N (several segments) or O (one)
+    for (int gs = g_first; gs < g_last; ++gs) {
+        const int b0 = seg_begin(nkb, gs);
+        segment(b0, seg_begin(nkb, gs + 1) - b0);
+        const float l_g = halves_sum(lsum);
+        if (nseg == 1) {  // one segment: its state is the result
+            m_s = m;
+            l_s = l_g;
+            break;
+        }
+        normalised = true;
+        // This segment's state, quantised like every segment state ...
+        segment_state(oacc, l_g);
+        const int e_g = state_exponent(oacc);
+        quantise(oacc, e_g);
+        if (gs == g_first) {
+            m_s = m;
+            l_s = l_g;
+            e_s = e_g;
+        } else {
+            // ... merged into the stored state of the earlier segments.
+            float wa, wb;
+            merge_weights(m_s, l_s, m, l_g, c, m_s, l_s, wa, wb);
+            merge_stored(oacc, my_stash, e_s, lane, wa, wb, true);
+            if (gs + 1 < nseg) {   // segments 0-1 merged: quantised as a stored state
+                e_s = state_exponent(oacc);
+                quantise(oacc, e_s);
+            }
+        }
+        if (gs + 1 < g_last) store_state(my_stash, oacc, e_s, lane);  // read back by this lane only
+    }
+
+    if (split_u >= 0) {
+        // A share of a split tile: publish this workgroup's partial state, and
+        // the last of the tile's workgroups to arrive merges them all.
+        const int slot = split_u;
+        store_state(tail.part + static_cast<int64_t>(slot) * kStashB + wave * kStashWaveB, oacc, e_s, lane);
+        if (g == 0)
+            tail.ml[slot * 256 + wave * kQW + li] = make_float4(m_s, l_s, __builtin_bit_cast(float, e_s), 0.f);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        // The stash is free now: its first word carries thread 0's arrival
+        // count to the other waves.
+        volatile int *arrived = reinterpret_cast<volatile int *>(stash);
+        __syncthreads();
+        const int tt = split_u % tail.n_split;
+        if (tid == 0) *arrived = atomicAdd(&tail.count[tt], 1);
+        __syncthreads();
+        if (*arrived != tail.ways - 1) return;
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        // The tile's partial states in segment order (slots tt + p n_split),
+        // this workgroup's own read back like the others.
+        auto slot_of = [&](int p) { return tt + p * tail.n_split; };
+        auto part_of = [&](int p) {
+            return tail.part + static_cast<int64_t>(slot_of(p)) * kStashB + wave * kStashWaveB;
+        };
+        float4 st = tail.ml[slot_of(0) * 256 + wave * kQW + li];
+        m_s = st.x;
+        l_s = st.y;
+        load_state(oacc, part_of(0), __builtin_bit_cast(int, st.z), lane);
+        for (int p = 1; p < tail.ways; ++p) {
+            st = tail.ml[slot_of(p) * 256 + wave * kQW + li];
+            float wa, wb;
+            merge_weights(m_s, l_s, st.x, st.y, c, m_s, l_s, wa, wb);
+            merge_stored(oacc, part_of(p), __builtin_bit_cast(int, st.z), lane, wa, wb, false);
+            if (p + 1 < tail.ways) quantise(oacc, state_exponent(oacc));   // segments 0-1 merged
+        }
+        if (tid == 0) atomicExch(&tail.count[tt], 0);   // ready for the next launch on this scratch
+    }
+
+    const float inv = normalised ? 1.0f : 1.0f / l_s;
     if (lse != nullptr && g == 0 && qi < S)
-        lse[static_cast<int64_t>(head) * S + qi] = mc + __builtin_amdgcn_logf(l);
+        lse[static_cast<int64_t>(head) * S + qi] = m_s * c + __builtin_amdgcn_logf(l_s);
     if (qi < S) {
         __bf16 *orow = oh + static_cast<int64_t>(qi) * D;
 #pragma unroll
@@ -956,18 +1191,43 @@ struct Shape {
     static constexpr int PER_CU = D == 128 ? 1 : 2;   // workgroups one CU holds
 };
 
+// The split of a d = 128 bf16 launch of W tiles on n_cu CUs (one workgroup
+// per CU): when its last round holds rem = W mod n_cu tiles and 3 rem (or
+// 2 rem) workgroups fit in one round, those tiles are split three (or two)
+// ways by key segments, so the last round lasts a third (two thirds) as
+// long.  Needs scratch (none: every tile whole, the same results).
+TailSplit plan_split(int64_t W, int S, const SplitScratch *sp) {
+    TailSplit t{nullptr, nullptr, nullptr, static_cast<int>(W), 0, 1};
+    const int nkb = (S + kBC - 1) / kBC;
+    if (!sp || !sp->part || sp->n_cu < 2 || dma::n_segments(nkb) != dma::kSeg) return t;
+    const int64_t n = sp->n_cu, rem = W % n;
+    if (rem == 0) return t;
+    const int ways = 3 * rem <= n ? 3 : 2 * rem <= n ? 2 : 0;
+    if (ways == 0 || rem * ways > sp->slots || rem > sp->counters) return t;
+    t.part = static_cast<char *>(sp->part);
+    t.ml = static_cast<float4 *>(sp->ml);
+    t.count = sp->count;
+    t.n_whole = static_cast<int>(W - rem);
+    t.n_split = static_cast<int>(rem);
+    t.ways = ways;
+    return t;
+}
+
 template <int D, typename T>
 hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, float *lse, int S,
-                        int n_heads, float c, hipStream_t stream) {
+                        int n_heads, float c, const SplitScratch *split, hipStream_t stream) {
     using Sh = Shape<D>;
     const int n_qtiles = (S + Sh::BR - 1) / Sh::BR;
     const int64_t blocks = static_cast<int64_t>(n_qtiles) * n_heads;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     if constexpr (D == dma::kD && sizeof(T) == 2 && kLdsDma) {
         static_assert(Sh::NT == 1 && Sh::WAVES == dma::kWaves, "the DMA kernel covers 256 queries in 8 waves");
-        attention_dma_kernel<false><<<static_cast<unsigned>(blocks), 64 * dma::kWaves, 0, stream>>>(
+        const TailSplit t = plan_split(blocks, S, split);
+        const int64_t grid = t.n_whole + static_cast<int64_t>(t.n_split) * t.ways;
+        if (grid > 0x7fffffff) return hipErrorInvalidValue;
+        attention_dma_kernel<false><<<static_cast<unsigned>(grid), 64 * dma::kWaves, 0, stream>>>(
             static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
-            static_cast<__bf16 *>(o), lse, S, n_qtiles, c, Riders{});
+            static_cast<__bf16 *>(o), lse, S, n_qtiles, c, t, Riders{});
     } else {
         attention_kernel<D, T, Sh::WAVES, Sh::NT, Sh::PER_CU><<<static_cast<unsigned>(blocks), 64 * Sh::WAVES, 0, stream>>>(
             static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
@@ -981,31 +1241,46 @@ hipError_t launch_typed(const void *q, const void *k, const void *v, void *o, fl
 int attention_queries_per_block(int d) { return d == 128 ? Shape<128>::BR : Shape<64>::BR; }
 int attention_blocks_per_cu(int d) { return d == 128 ? Shape<128>::PER_CU : Shape<64>::PER_CU; }
 
+int64_t attention_split_slot_bytes() { return dma::kStashB + 256 * int64_t{sizeof(float4)}; }
+
+int attention_split_ways(int64_t W, int S, int d, int dtype, int n_cu) {
+    if (!(kLdsDma && d == dma::kD && dtype == 0)) return 1;
+    SplitScratch sp{};
+    sp.part = sp.ml = reinterpret_cast<void *>(uintptr_t{256});   // placeholders: never dereferenced
+    sp.n_cu = n_cu;
+    sp.slots = sp.counters = n_cu;
+    const TailSplit t = plan_split(W, S, &sp);
+    return t.n_split > 0 ? t.ways : 1;
+}
+
 hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, float *lse, int S,
-                            int n_heads, int d, float scale_log2e, int dtype, hipStream_t stream) {
+                            int n_heads, int d, float scale_log2e, int dtype,
+                            const SplitScratch *split, hipStream_t stream) {
     if (S == 0 || n_heads == 0) return hipSuccess;
     if (d == 128 && dtype == 0)
-        return launch_typed<128, __bf16>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
+        return launch_typed<128, __bf16>(q, k, v, o, lse, S, n_heads, scale_log2e, split, stream);
     if (d == 64 && dtype == 0)
-        return launch_typed<64, __bf16>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
+        return launch_typed<64, __bf16>(q, k, v, o, lse, S, n_heads, scale_log2e, split, stream);
     if (d == 128 && dtype == 1)
-        return launch_typed<128, float>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
+        return launch_typed<128, float>(q, k, v, o, lse, S, n_heads, scale_log2e, split, stream);
     if (d == 64 && dtype == 1)
-        return launch_typed<64, float>(q, k, v, o, lse, S, n_heads, scale_log2e, stream);
+        return launch_typed<64, float>(q, k, v, o, lse, S, n_heads, scale_log2e, split, stream);
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention_riding(const void *q, const void *k, const void *v, void *o, float *lse,
                                    int S, int n_heads, int d, float scale_log2e, int dtype,
                                    const RidingCopy *copies, int n_copies, int64_t H, int n_cu,
-                                   bool *riding, hipStream_t stream) {
+                                   const SplitScratch *split, bool *riding, hipStream_t stream) {
     *riding = false;
     const bool can = kLdsDma && d == dma::kD && dtype == 0 && S > 0 && n_heads > 0 && copies &&
                      n_copies >= 1 && n_copies <= 2 && n_cu > 0 && copy::strided_span_fits(H);
-    if (!can) return launch_attention(q, k, v, o, lse, S, n_heads, d, scale_log2e, dtype, stream);
+    if (!can)
+        return launch_attention(q, k, v, o, lse, S, n_heads, d, scale_log2e, dtype, split, stream);
     using Sh = Shape<dma::kD>;
     const int64_t n_qtiles = (S + Sh::BR - 1) / Sh::BR;
-    const int64_t n_attn = n_qtiles * n_heads;
+    const TailSplit t = plan_split(n_qtiles * n_heads, S, split);
+    const int64_t n_attn = t.n_whole + static_cast<int64_t>(t.n_split) * t.ways;
     const int64_t idle = (n_cu - n_attn % n_cu) % n_cu;
     Riders r{};
     r.S = S;
@@ -1035,11 +1310,10 @@ hipError_t launch_attention_riding(const void *q, const void *k, const void *v, 
     // counts: the caller launches the copies itself.
     if (idle < std::max(1, n_cu / 8) || total >= (int64_t{1} << 31) ||
         n_attn + idle > 0x7fffffff)
-        return launch_attention(q, k, v, o, lse, S, n_heads, d, scale_log2e, dtype, stream);
-    r.n_attn = static_cast<unsigned>(n_attn);
+        return launch_attention(q, k, v, o, lse, S, n_heads, d, scale_log2e, dtype, split, stream);
     attention_dma_kernel<true><<<static_cast<unsigned>(n_attn + idle), 64 * dma::kWaves, 0, stream>>>(
         static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
-        static_cast<__bf16 *>(o), lse, S, static_cast<int>(n_qtiles), scale_log2e, r);
+        static_cast<__bf16 *>(o), lse, S, static_cast<int>(n_qtiles), scale_log2e, t, r);
     const hipError_t e = hipGetLastError();
     if (e == hipSuccess) *riding = true;
     return e;

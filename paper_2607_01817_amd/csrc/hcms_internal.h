@@ -47,11 +47,29 @@ int attention_queries_per_block(int d);
 int auto_plan(int S, int d, int dtype, const int *sizes, int C, int n_cu);
 int attention_blocks_per_cu(int d);
 
+// Scratch for splitting a launch's last round of tiles over several
+// workgroups (d = 128 bf16): `slots` partial states of
+// attention_split_slot_bytes() bytes each (part: slots x 64 KiB, ml: slots x
+// 4 KiB, 16-byte aligned) and `counters` ints that are zero between launches.  At most one
+// launch may use one scratch at a time (launches on one stream are ordered).
+struct SplitScratch {
+    void *part;
+    void *ml;
+    int *count;
+    int slots, counters;
+    int n_cu;
+};
+int64_t attention_split_slot_bytes();
+// Workgroups per split tile (2 or 3) a d = 128 bf16 launch of W tiles splits
+// its last round's tiles into on n_cu CUs, or 1 when it splits none.
+int attention_split_ways(int64_t W, int S, int d, int dtype, int n_cu);
+
 // lse, if not NULL, receives [n_heads][S] fp32 log2 softmax denominators:
-// P_ij = exp2(scale_log2e * <q_i, k_j> - lse_i).
+// P_ij = exp2(scale_log2e * <q_i, k_j> - lse_i).  split: NULL, or scratch
+// that lets the launch split its last round (same results either way).
 hipError_t launch_attention(const void *q, const void *k, const void *v, void *o, float *lse,
                             int S, int n_heads, int d, float scale_log2e, int dtype,
-                            hipStream_t stream);
+                            const SplitScratch *split, hipStream_t stream);
 
 // A head-chunk copy that can ride in an attention launch: the arguments of
 // launch_pack (unpack = false) or launch_unpack (unpack = true) for rows of
@@ -73,7 +91,7 @@ struct RidingCopy {
 hipError_t launch_attention_riding(const void *q, const void *k, const void *v, void *o, float *lse,
                                    int S, int n_heads, int d, float scale_log2e, int dtype,
                                    const RidingCopy *copies, int n_copies, int64_t H, int n_cu,
-                                   bool *riding, hipStream_t stream);
+                                   const SplitScratch *split, bool *riding, hipStream_t stream);
 // Backward of attention for `n_heads` consecutive heads (head-major buffers
 // starting at the chunk's first head; lse and delta [n_heads][S] fp32): one
 // query-parallel launch writing delta = <dO, O> and dq, then one key-parallel

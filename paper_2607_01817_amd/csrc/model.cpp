@@ -18,7 +18,9 @@
 // t_round (g0 + (1 - g0) f) rather than a whole t_round.  Summed over the
 // launches, T_attn = t_round (sum W / n) + t_round g0 (R - sum W / n) with
 // R = sum ceil(W / n) the round count: only the idle share of the partial
-// rounds depends on C.  hcms_model_plan_time adds the copies each plan
+// rounds depends on C.  A launch that splits its last round's tiles by key
+// segments (attention_split_ways) shortens that round to a third or two
+// thirds.  hcms_model_plan_time adds the copies each plan
 // leaves on the critical path and its synchronisations; hcms_choose_chunks
 // picks the chunk count whose plan (the one HCMS_MODE_AUTO runs) the model
 // predicts fastest.
@@ -64,12 +66,17 @@ bool solve3(double m[3][3], double r[3], double x[3]) {
     return std::isfinite(x[0]) && std::isfinite(x[1]) && std::isfinite(x[2]);
 }
 
-// Duration of one launch of W workgroups on n slots, in units of a full round.
-double launch_rounds(int64_t W, int64_t n, double g0) {
+// Duration of one launch of W workgroups on n slots, in units of a full round,
+// when its last round's tiles are split `ways` ways by key segments (1: not
+// split; 2: the round lasts two thirds as long with 2 rem workgroups busy;
+// 3: a third as long with 3 rem busy).
+double launch_rounds(int64_t W, int64_t n, double g0, int ways) {
     if (W <= 0) return 0.0;
     const int64_t full = W / n, rem = W % n;
-    const double f = static_cast<double>(rem) / static_cast<double>(n);
-    return static_cast<double>(full) + (rem > 0 ? g0 + (1.0 - g0) * f : 0.0);
+    if (rem == 0) return static_cast<double>(full);
+    const double f = static_cast<double>(rem * ways) / static_cast<double>(n);
+    const double len = ways == 3 ? 1.0 / 3.0 : ways == 2 ? 2.0 / 3.0 : 1.0;
+    return static_cast<double>(full) + len * (g0 + (1.0 - g0) * f);
 }
 
 bool plan_mode(int m) {
@@ -78,8 +85,8 @@ bool plan_mode(int m) {
 }
 
 // Model time of one plan; arguments already validated.
-double plan_time(int S, int d, const int *sizes, int C, int mode, int n_cu, double t_round,
-                 double g0, double t_copy, double beta) {
+double plan_time(int S, int d, int dtype, const int *sizes, int C, int mode, int n_cu,
+                 double t_round, double g0, double t_copy, double beta) {
     const int64_t br = hcms::attention_queries_per_block(d);
     const int64_t n = static_cast<int64_t>(n_cu) * hcms::attention_blocks_per_cu(d);
     const int64_t tiles = (static_cast<int64_t>(S) + br - 1) / br;
@@ -90,10 +97,13 @@ double plan_time(int S, int d, const int *sizes, int C, int mode, int n_cu, doub
     }
     if (C == 1) mode = HCMS_MODE_SERIAL;
     double attn = 0.0;
-    if (mode == HCMS_MODE_LANES) {
-        attn = launch_rounds(total, n, g0);
+    if (mode == HCMS_MODE_LANES) {   // the two lanes' launches keep their tiles whole
+        attn = launch_rounds(total, n, g0, 1);
     } else {
-        for (int c = 0; c < C; ++c) attn += launch_rounds(tiles * sizes[c], n, g0);
+        for (int c = 0; c < C; ++c) {
+            const int64_t W = tiles * sizes[c];
+            attn += launch_rounds(W, n, g0, hcms::attention_split_ways(W, S, d, dtype, n_cu));
+        }
     }
     attn *= t_round;
     // Copies on the critical path, in head-tensors (a pack moves 3 per head,
@@ -108,7 +118,9 @@ double plan_time(int S, int d, const int *sizes, int C, int mode, int n_cu, doub
         if (mode == HCMS_MODE_FUSED)
             for (int c = 0; c < C; ++c) {
                 const int64_t W = tiles * sizes[c];
-                const int64_t idle = (n - W % n) % n;
+                const int64_t rem = W % n;
+                const int64_t W_run = W - rem + rem * hcms::attention_split_ways(W, S, d, dtype, n_cu);
+                const int64_t idle = (n - W_run % n) % n;
                 if (idle >= std::max<int64_t>(1, n / 8)) continue;
                 if (c + 1 < C) copies += 3.0 * sizes[c + 1];
                 if (c >= 1) copies += sizes[c - 1];
@@ -152,7 +164,7 @@ int hcms_model_plan_time(int S, int d, int dtype, const int *chunk_sizes, int n_
         mode = hcms::auto_plan(S, d, dtype, chunk_sizes, n_chunks, n_cu);
     }
     if (!plan_mode(mode)) return hcms::fail(HCMS_ERR_ARG, "mode %d is not a plan", mode);
-    *t_out = plan_time(S, d, chunk_sizes, n_chunks, mode, n_cu, t_round, g0, t_copy, beta);
+    *t_out = plan_time(S, d, dtype, chunk_sizes, n_chunks, mode, n_cu, t_round, g0, t_copy, beta);
     return hcms::ok();
 }
 
@@ -171,7 +183,7 @@ int hcms_choose_chunks(int S, int H, int d, int dtype, int n_cu, double t_round,
     for (int C = 1; C <= top; ++C) {
         for (int c = 0; c < C; ++c) sizes[c] = H / C + (c < H % C ? 1 : 0);
         const int mode = hcms::auto_plan(S, d, dtype, sizes.data(), C, n_cu);
-        const double t = plan_time(S, d, sizes.data(), C, mode, n_cu, t_round, g0, t_copy, beta);
+        const double t = plan_time(S, d, dtype, sizes.data(), C, mode, n_cu, t_round, g0, t_copy, beta);
         if (t < best_t) {   // ties keep the smaller chunk count
             best_t = t;
             best_mode = mode;

@@ -328,13 +328,20 @@ def test_auto_mode_runs_the_predicted_plan(hcms, name, sizes):
     ctx.close()
 
 
-def test_forward_is_deterministic(hcms):
-    w = inputs.WORKLOADS["wan_p8"]
-    q, k, v = (x.cuda() for x in workload_inputs("wan_p8"))
+@pytest.mark.parametrize("name,sizes", [("wan_p8", (2, 2, 1)), ("wan_p8", (5,)), ("small", (8,)),
+                                        ("small", (3, 3, 2))])
+def test_forward_is_deterministic(hcms, name, sizes):
+    """Repeated forwards give the same bits.  Wan-P8 {5} splits its last round
+    of 76 tiles three ways and Small {8} its 128 tiles two ways, so each call
+    also checks that the split tiles' arrival counters are back at zero."""
+    w = inputs.WORKLOADS[name]
+    q, k, v = (x.cuda() for x in workload_inputs(name))
+    ref = hcms.attention(_cuda_hm(q), _cuda_hm(k), _cuda_hm(v), w.scale).permute(1, 0, 2)
     ctx = hcms.Context()
-    first = bits(ctx.forward(q, k, v, w.P, w.scale, (2, 2, 1)).clone())
-    for _ in range(2):
-        assert torch.equal(bits(ctx.forward(q, k, v, w.P, w.scale, (2, 2, 1))), first)
+    for mode in (hcms.MODE_SERIAL, hcms.MODE_FUSED):
+        for _ in range(3):
+            got = ctx.forward(q, k, v, w.P, w.scale, sizes, mode=mode)
+            assert torch.equal(bits(got), bits(ref)), (name, sizes, mode)
     ctx.close()
 
 

@@ -206,6 +206,27 @@ def test_worked_rounds_of_the_wan_p4_share():
     assert fused == pytest.approx(tm.plan_time(S, (2,) * 5, tm.SERIAL, 256, 256, tr, g0, tc, b))
 
 
+def test_worked_split_tails():
+    """The kernel splits a launch's last round by key segments.  Wan-P8 in
+    one chunk (S = 56160: 220 tiles per head, 878 key blocks): 1100
+    workgroups = 4 full rounds and 76 tiles; 3 x 76 = 228 <= 256, so three
+    ways, a round a third as long with 228 of 256 slots busy.  Wan-P4 in
+    5 + 5 (S = 32760): 640 = 2 rounds and 128 tiles, 2 x 128 = 256: two ways,
+    two thirds of a full round.  Wan-P8 in 2 + 2 + 1: 440 = 256 + 184 and
+    220, no split fits.  Keys of fewer than 12 blocks are never split."""
+    g0 = 0.4
+    assert tm.tail_ways(1100, 256, 56160, True) == 3
+    assert tm.launch_rounds(1100, 256, g0, 3) == pytest.approx(4 + (g0 + (1 - g0) * 228 / 256) / 3)
+    assert tm.plan_time(56160, (5,), tm.SERIAL, 256, 256, 1.0, g0, 0.0, 0.0, True) == \
+        pytest.approx(4 + (g0 + (1 - g0) * 228 / 256) / 3)
+    assert tm.tail_ways(640, 256, 32760, True) == 2
+    assert tm.plan_time(32760, (5, 5), tm.SERIAL, 256, 256, 1.0, g0, 0.0, 0.0, True) == \
+        pytest.approx(2 * (2 + 2 / 3))
+    assert tm.tail_ways(440, 256, 56160, True) == 1 and tm.tail_ways(220, 256, 56160, True) == 1
+    assert tm.tail_ways(1100, 256, 56160, False) == 1
+    assert tm.tail_ways(1100, 256, 64 * 11, True) == 1
+
+
 def _plan_of(S, d, dtype=0, n_cu=256):
     return lambda sizes: hcms.auto_mode(S, d, sizes, n_cu, dtype=dtype)
 
@@ -224,13 +245,15 @@ def test_plan_time_and_choice_match_oracle(S, H, d):
             for mode in (hcms.MODE_SERIAL, hcms.MODE_PIPELINED, hcms.MODE_INLINE, hcms.MODE_LANES,
                          hcms.MODE_SLOTS, hcms.MODE_FUSED):
                 got = hcms.model_plan_time(S, d, sizes, mode, 256, t_round, g0, t_copy, beta)
-                want = tm.plan_time(S, sizes, mode, n, br, t_round, g0, t_copy, beta)
+                want = tm.plan_time(S, sizes, mode, n, br, t_round, g0, t_copy, beta, d == 128)
                 assert got == pytest.approx(want, rel=1e-12)
             auto = hcms.model_plan_time(S, d, sizes, hcms.MODE_AUTO, 256, t_round, g0, t_copy, beta)
             assert auto == pytest.approx(tm.plan_time(S, sizes, _plan_of(S, d)(sizes), n, br,
-                                                      t_round, g0, t_copy, beta), rel=1e-12)
+                                                      t_round, g0, t_copy, beta, d == 128),
+                                         rel=1e-12)
         sizes, mode, t = hcms.choose_chunks(S, H, d, 256, t_round, g0, t_copy, beta)
-        o_sizes, o_t = tm.choose_chunks(S, H, _plan_of(S, d), n, br, t_round, g0, t_copy, beta)
+        o_sizes, o_t = tm.choose_chunks(S, H, _plan_of(S, d), n, br, t_round, g0, t_copy, beta,
+                                        split=d == 128)
         assert sizes == o_sizes and t == pytest.approx(o_t, rel=1e-12)
         assert mode == _plan_of(S, d)(sizes)
         # brute force over every C: nothing is faster than the choice

@@ -25,14 +25,18 @@ MUTANTS = {
     "integer optimum ignores the overhead": ("(t_comm / c + c * beta, c)", "(t_comm / c, c)"),
     "fit basis C instead of 1 / C": ("A = np.stack([np.ones_like(c), 1.0 / c, c], axis=1)",
                                      "A = np.stack([np.ones_like(c), c, c * c], axis=1)"),
-    "partial round costs a full one": ("return full + g0 + (1.0 - g0) * f", "return full + 1.0"),
-    "partial round costs only its busy share": ("return full + g0 + (1.0 - g0) * f",
-                                                "return full + f"),
+    "partial round costs a full one": ("return full + length * (g0 + (1.0 - g0) * f)",
+                                       "return full + length"),
+    "partial round costs only its busy share": ("return full + length * (g0 + (1.0 - g0) * f)",
+                                                "return full + length * f"),
     "lanes do not pool the rounds": ("attn = launch_rounds(sum(W), n_slots, g0)",
                                      "attn = sum(launch_rounds(w, n_slots, g0) for w in W)"),
     "serial plan moves only the unpacks": ("copies = 4 * H ", "copies = H "),
     "one synchronisation per chunk": ("PIPELINED: 2 * C + 3", "PIPELINED: C + 3"),
     "fused launches always carry": ("if idle >= max(1, n_slots // 8):", "if True:"),
+    "split tail keeps its full length": ("length = {1: 1.0, 2: 2.0 / 3.0, 3: 1.0 / 3.0}[ways]",
+                                         "length = 1.0"),
+    "split three ways where two fit": ("return 3 if 3 * rem <= n else", "return 3 if 2 * rem <= n else"),
 }
 
 PINS = [
@@ -47,6 +51,7 @@ PINS = [
     pins.test_round_identity,
     pins.test_one_gpu_model_reduces_to_the_paper_model,
     pins.test_worked_rounds_of_the_wan_p4_share,
+    pins.test_worked_split_tails,
 ]
 
 
