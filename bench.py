@@ -258,41 +258,73 @@ def time_model_sweep(ctx, w, reps: int, dev):
 def adaptive_chunks(ctx, sweeps):
     """Calibrate the one-GPU time model (hcms_model_plan_time) on the sweeps'
     measurements and let hcms_choose_chunks pick the chunk count:
-      * t_round = kappa S (a full round of attention workgroups; its work per
-        workgroup is 4 Br S d) and g0 by least squares on the serial plans'
-        attention times, T_attn = kappa S (sum W / n) + kappa g0 S (R - sum W / n)
-        (R = sum ceil(W / n), the launches' round count), over every sweep;
+      * t_round = kappa S (a full round of attention workgroups; a
+        workgroup's work is 4 Br S d) and g0 by least squares on the serial
+        plans' attention kernel times over every sweep:
+        T_attn = kappa S X1 + kappa g0 S X2, where X1 + g0 X2 is the
+        launches' round count with partial (and split) rounds costing
+        g0 + (1 - g0) f of theirs (X1, X2 read off the library's model at
+        g0 = 1 and g0 -> 0);
       * t_copy = the layout kernels at C = 1 over 4 H head-tensors;
-      * beta = (Alg. 1 - serial) at C = 1 over its 7 synchronisations.
+      * beta = (Alg. 1 - serial) at C = 1 over its 7 synchronisations;
+      * drain (rounds per attention launch on the critical path) and a
+        constant T_0 per workload by least squares on the auto plans' step
+        times' residuals.
     Reports the model's prediction of the auto plan per C against the
     measured auto time and whether the chosen C measures within 1 % of the
     sweep's best."""
     n = ctx.num_cu
+    tiny = 1e-9
     rows, ys = [], []
     for sw in sweeps:
-        tiles = -(-sw["S"] // 256)
         for C, t in zip(sw["chunk_counts"], sw["attention_kernels_ms"]):
-            Ws = [tiles * h for h in hcms.default_chunks(sw["H"], C)]
-            R = sum(-(-x // n) for x in Ws)
-            rows.append([sw["S"] * sum(Ws) / n, sw["S"] * (R - sum(Ws) / n)])
+            sz = hcms.default_chunks(sw["H"], C)
+            x_lo = hcms.model_plan_time(sw["S"], 128, sz, hcms.MODE_SERIAL, n, 1.0, tiny, 0.0, 0.0)
+            x_hi = hcms.model_plan_time(sw["S"], 128, sz, hcms.MODE_SERIAL, n, 1.0, 1.0, 0.0, 0.0)
+            x2 = (x_hi - x_lo) / (1.0 - tiny)
+            rows.append([sw["S"] * (x_lo - tiny * x2), sw["S"] * x2])
             ys.append(t)
     (kappa, kg0), *_ = np.linalg.lstsq(np.asarray(rows), np.asarray(ys), rcond=None)
     g0 = float(min(1.0, max(1e-3, kg0 / kappa))) if kappa > 0 else 1.0
-    out = {"kappa_ms_per_key": float(kappa), "g0": round(g0, 4), "configs": []}
+    par = {}
     for sw in sweeps:
         S, H = sw["S"], sw["H"]
-        t_copy = sw["layout_kernels_ms"][0] / (4 * H)
-        beta = max(0.0, (sw["pipelined_ms"][0] - sw["serial_ms"][0]) / 7)
-        t_round = kappa * S
-        pred = [hcms.model_plan_time(S, 128, hcms.default_chunks(H, C), hcms.MODE_AUTO, n, t_round,
-                                     g0, t_copy, beta) for C in sw["chunk_counts"]]
-        sizes, plan, t_pred = hcms.choose_chunks(S, H, 128, n, t_round, g0, t_copy, beta)
+        par[sw["workload"]] = (kappa * S, sw["layout_kernels_ms"][0] / (4 * H),
+                               max(0.0, (sw["pipelined_ms"][0] - sw["serial_ms"][0]) / 7))
+    # Drain and T_0 from the step times: residual = T_0(workload) + drain x
+    # (the plan's launches on the critical path x t_round).
+    rows, ys = [], []
+    names = [sw["workload"] for sw in sweeps]
+    for sw in sweeps:
+        t_round, t_copy, beta = par[sw["workload"]]
+        for C in sw["chunk_counts"]:
+            sz = hcms.default_chunks(sw["H"], C)
+            for mode, meas in ((hcms.MODE_AUTO, sw["auto_ms"][C - 1]),):
+                p0 = hcms.model_plan_time(sw["S"], 128, sz, mode, n, t_round, g0, t_copy, beta)
+                p1 = hcms.model_plan_time(sw["S"], 128, sz, mode, n, t_round, g0, t_copy, beta,
+                                          drain=1.0)
+                rows.append([1.0 if nm == sw["workload"] else 0.0 for nm in names] + [p1 - p0])
+                ys.append(meas - p0)
+    sol, *_ = np.linalg.lstsq(np.asarray(rows), np.asarray(ys), rcond=None)
+    t0 = dict(zip(names, (float(x) for x in sol[:-1])))
+    drain = float(max(0.0, sol[-1]))
+    out = {"kappa_ms_per_key": float(kappa), "g0": round(g0, 4), "drain_rounds": round(drain, 4),
+           "configs": []}
+    for sw in sweeps:
+        S, H = sw["S"], sw["H"]
+        t_round, t_copy, beta = par[sw["workload"]]
+        pred = [t0[sw["workload"]] +
+                hcms.model_plan_time(S, 128, hcms.default_chunks(H, C), hcms.MODE_AUTO, n, t_round,
+                                     g0, t_copy, beta, drain=drain) for C in sw["chunk_counts"]]
+        sizes, plan, t_pred = hcms.choose_chunks(S, H, 128, n, t_round, g0, t_copy, beta,
+                                                 drain=drain)
         meas = sw["auto_ms"]
         best = min(meas)
         chosen = meas[len(sizes) - 1]
         out["configs"].append({
             "workload": sw["workload"], "t_round_ms": round(t_round, 4),
             "t_copy_ms": round(t_copy, 5), "beta_ms": round(beta, 5),
+            "t0_ms": round(t0[sw["workload"]], 4),
             "predicted_auto_ms": [round(x, 4) for x in pred],
             "measured_auto_ms": meas,
             "prediction_error": [round((p_ - m_) / m_, 4) for p_, m_ in zip(pred, meas)],
@@ -579,6 +611,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--no-extras", action="store_true",
                     help="time the step only (for profiler runs)")
+    ap.add_argument("--only", choices=("training", "layer"),
+                    help="run only that section on the workload and chunks (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy first (for counter passes)")
     ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
@@ -608,6 +642,16 @@ def main():
     dev = torch.device("cuda:0")
     if args.copy_calibration:
         copy_calibration(dev)
+    if args.only:
+        ctx = hcms.Context(max_chunks=max(16, len(sizes)))
+        if args.only == "training":
+            res = training_step(ctx, w, sizes, max(10, args.steps // 4), dev)
+        else:
+            lw = inputs.LAYERS["layer_wan_p8"]
+            res = layer_step(ctx, lw, lw.chunkings[-1], max(10, args.steps // 2), dev)
+        ctx.close()
+        print(json.dumps({"only": args.only, args.only: res}), flush=True)
+        return
     log(f"workload {w.name}: S={w.S} H={w.H} d={w.d} {w.dtype} P={w.P} chunks={sizes} "
         f"mode={args.mode}")
     q, k, v = inputs.make_qkv(w)

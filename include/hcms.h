@@ -344,15 +344,22 @@ HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n,
  * d = 64) runs floor(W / n) full rounds and, when n does not divide W, a
  * partial round keeping a fraction f = (W mod n) / n of the slots busy,
  * which lasts t_round (g0 + (1 - g0) f) (the clock rises when part of the
- * chip idles; g0 = 1: a partial round costs a full one).  Inputs measured on
- * the device: t_round (one full round of attention workgroups), g0 in
- * (0, 1], t_copy (the layout kernel for one head of one tensor) and beta (one
- * event record or wait on the critical path).
+ * chip idles; g0 = 1: a partial round costs a full one).  When the attention
+ * kernel splits that round's tiles by key segments (hcms_forward's d = 128
+ * bf16 launches outside the lanes plan: 3 rem <= n three ways, else
+ * 2 rem <= n two ways, with S of 12 key blocks or more) the round holds
+ * ways rem workgroups and lasts a third (three ways) or two thirds (two ways)
+ * as long.  Every launch on the critical path adds `drain` rounds (its last
+ * workgroups finish at different times).  Inputs measured on the device:
+ * t_round (one full round of attention workgroups), g0 in (0, 1], drain >= 0,
+ * t_copy (the layout kernel for one head of one tensor) and beta (one event
+ * record or wait on the critical path).
  *
  * hcms_model_plan_time: model time of `mode` (a plan, or HCMS_MODE_AUTO for
  *   the plan hcms_auto_mode picks) on chunk_sizes:
- *     attention: the sum of the launches' rounds (HCMS_MODE_LANES: the
- *       chunks' workgroups pooled into one launch's rounds), times t_round;
+ *     attention: the sum of the launches' rounds plus C drains
+ *       (HCMS_MODE_LANES: the chunks' workgroups pooled into one launch's
+ *       rounds, unsplit, plus ceil(C / 2) drains), times t_round;
  *     copies on the critical path, in head-tensors times t_copy (a pack moves
  *       3 per head, an unpack 1): all 4 H in serial mode; otherwise chunk 0's
  *       pack and the last chunk's unpack, plus in fused mode the copies a
@@ -362,9 +369,9 @@ HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n,
  *       chunk, the fork and the join).
  *   With every launch filling whole rounds and equal chunks, the pipelined
  *   plan's time is the paper's T_hcms(C) with T_comm = 4 H t_copy, per-chunk
- *   overhead 2 beta and T_0 = 3 beta.
- *   Errors: NULL, SHAPE (S < 0, d), DTYPE, CHUNKS, ARG (mode; a time negative
- *   or not finite; n_cu < 1; g0 outside (0, 1]).
+ *   overhead 2 beta + drain t_round and T_0 = 3 beta.
+ *   Errors: NULL, SHAPE (S < 0, d), DTYPE, CHUNKS, ARG (mode; a time or drain
+ *   negative or not finite; n_cu < 1; g0 outside (0, 1]).
  * hcms_choose_chunks: for C = 1 .. min(H, max_chunks), the chunk rule's sizes
  *   (hcms_default_chunks) in the plan HCMS_MODE_AUTO would run; writes the
  *   fastest under the model to sizes_out (room for min(H, max_chunks) ints),
@@ -374,11 +381,11 @@ HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n,
  * Host only.
  */
 HCMS_API int hcms_model_plan_time(int S, int d, int dtype, const int *chunk_sizes, int n_chunks,
-                                  int mode, int n_cu, double t_round, double g0, double t_copy,
-                                  double beta, double *t_out);
+                                  int mode, int n_cu, double t_round, double g0, double drain,
+                                  double t_copy, double beta, double *t_out);
 HCMS_API int hcms_choose_chunks(int S, int H, int d, int dtype, int n_cu, double t_round,
-                                double g0, double t_copy, double beta, int max_chunks,
-                                int *sizes_out, int *mode_out, double *t_out);
+                                double g0, double drain, double t_copy, double beta,
+                                int max_chunks, int *sizes_out, int *mode_out, double *t_out);
 
 typedef struct hcms_ctx hcms_ctx;
 

@@ -103,11 +103,14 @@ def tail_ways(W: int, n: int, S: int, split: bool) -> int:
 
 
 def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_round: float,
-              g0: float, t_copy: float, beta: float, split: bool = False) -> float:
+              g0: float, t_copy: float, beta: float, split: bool = False,
+              drain: float = 0.0) -> float:
     """Model time of one plan of the chunk sizes ``sizes`` on one GPU with
     ``n_slots`` attention workgroups per round of ``queries_per_wg`` queries;
     ``split``: the attention kernel splits its launches' last rounds (the
-    lanes plan keeps every tile whole)."""
+    lanes plan keeps every tile whole); ``drain``: rounds each attention
+    launch on the critical path adds while its last workgroups finish (C of
+    them in one lane, ceil(C / 2) when two lanes alternate)."""
     sizes = list(sizes)
     C, H = len(sizes), sum(sizes)
     tiles = -(-S // queries_per_wg)
@@ -115,9 +118,10 @@ def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_rou
     if C == 1:
         mode = SERIAL
     if mode == LANES:
-        attn = launch_rounds(sum(W), n_slots, g0)
+        attn = launch_rounds(sum(W), n_slots, g0) + drain * math.ceil(C / 2)
     else:
         attn = sum(launch_rounds(w, n_slots, g0, tail_ways(w, n_slots, S, split)) for w in W)
+        attn += drain * C
     if mode == SERIAL:
         copies = 4 * H                    # 3 tensors packed, 1 unpacked, per head
     else:
@@ -138,14 +142,14 @@ def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_rou
 
 def choose_chunks(S: int, H: int, plan_of, n_slots: int, queries_per_wg: int, t_round: float,
                   g0: float, t_copy: float, beta: float, max_chunks: int | None = None,
-                  split: bool = False):
+                  split: bool = False, drain: float = 0.0):
     """(sizes, model time) of the fastest chunk count of the chunk rule, each
     C in the plan ``plan_of(sizes)`` picks; ties go to fewer chunks."""
     best = None
     for C in range(1, min(H, max_chunks or H) + 1):
         sizes = [H // C + (1 if c < H % C else 0) for c in range(C)]   # Sec. 3.3 chunk rule
         t = plan_time(S, sizes, plan_of(sizes), n_slots, queries_per_wg, t_round, g0, t_copy, beta,
-                      split)
+                      split, drain)
         if best is None or t < best[1]:
             best = (sizes, t)
     return best

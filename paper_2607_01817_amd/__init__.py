@@ -79,8 +79,8 @@ def load():
         "hcms_model_optimal_chunks": ([d, d, i, dp], i),
         "hcms_model_speedup": ([d, d, i, dp], i),
         "hcms_model_fit": ([ip, dp, i, dp, dp, dp], i),
-        "hcms_model_plan_time": ([i, i, i, ip, i, i, i, d, d, d, d, dp], i),
-        "hcms_choose_chunks": ([i, i, i, i, i, d, d, d, d, i, ip, ip, dp], i),
+        "hcms_model_plan_time": ([i, i, i, ip, i, i, i, d, d, d, d, d, dp], i),
+        "hcms_choose_chunks": ([i, i, i, i, i, d, d, d, d, d, i, ip, ip, dp], i),
         "hcms_ctx_num_cu": ([vp], i),
         "hcms_ctx_create": ([i, i, ctypes.POINTER(vp)], i),
         "hcms_ctx_destroy": ([vp], i),
@@ -219,25 +219,27 @@ def model_fit(chunk_counts, times) -> tuple[float, float, float]:
 
 
 def model_plan_time(S: int, d: int, chunk_sizes, mode: int, n_cu: int, t_round: float,
-                    g0: float, t_copy: float, beta: float, dtype: int = BF16) -> float:
+                    g0: float, t_copy: float, beta: float, dtype: int = BF16,
+                    drain: float = 0.0) -> float:
     """One-GPU model time of a plan (see hcms.h, hcms_model_plan_time)."""
     sizes, n = _ints(chunk_sizes)
     out = ctypes.c_double()
-    _check(load().hcms_model_plan_time(S, d, dtype, sizes, n, mode, n_cu, t_round, g0, t_copy,
-                                       beta, ctypes.byref(out)))
+    _check(load().hcms_model_plan_time(S, d, dtype, sizes, n, mode, n_cu, t_round, g0, drain,
+                                       t_copy, beta, ctypes.byref(out)))
     return out.value
 
 
 def choose_chunks(S: int, H: int, d: int, n_cu: int, t_round: float, g0: float, t_copy: float,
-                  beta: float, max_chunks: int | None = None, dtype: int = BF16):
+                  beta: float, max_chunks: int | None = None, dtype: int = BF16,
+                  drain: float = 0.0):
     """(sizes, plan, model time) of the chunk count the one-GPU model predicts
     fastest under the plan MODE_AUTO runs (hcms_choose_chunks)."""
     top = H if max_chunks is None else max_chunks
     buf = (ctypes.c_int * max(1, min(H, top)))()
     mode = ctypes.c_int()
     t = ctypes.c_double()
-    n = _check(load().hcms_choose_chunks(S, H, d, dtype, n_cu, t_round, g0, t_copy, beta, top,
-                                         buf, ctypes.byref(mode), ctypes.byref(t)))
+    n = _check(load().hcms_choose_chunks(S, H, d, dtype, n_cu, t_round, g0, drain, t_copy, beta,
+                                         top, buf, ctypes.byref(mode), ctypes.byref(t)))
     return list(buf[:n]), mode.value, t.value
 
 

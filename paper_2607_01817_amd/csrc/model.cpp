@@ -20,7 +20,9 @@
 // R = sum ceil(W / n) the round count: only the idle share of the partial
 // rounds depends on C.  A launch that splits its last round's tiles by key
 // segments (attention_split_ways) shortens that round to a third or two
-// thirds.  hcms_model_plan_time adds the copies each plan
+// thirds.  Each launch also drains: its last workgroups finish at different
+// times (the XCDs run at different clocks), a cost of `drain` rounds per
+// launch on the critical path.  hcms_model_plan_time adds the copies each plan
 // leaves on the critical path and its synchronisations; hcms_choose_chunks
 // picks the chunk count whose plan (the one HCMS_MODE_AUTO runs) the model
 // predicts fastest.
@@ -86,7 +88,7 @@ bool plan_mode(int m) {
 
 // Model time of one plan; arguments already validated.
 double plan_time(int S, int d, int dtype, const int *sizes, int C, int mode, int n_cu,
-                 double t_round, double g0, double t_copy, double beta) {
+                 double t_round, double g0, double drain, double t_copy, double beta) {
     const int64_t br = hcms::attention_queries_per_block(d);
     const int64_t n = static_cast<int64_t>(n_cu) * hcms::attention_blocks_per_cu(d);
     const int64_t tiles = (static_cast<int64_t>(S) + br - 1) / br;
@@ -98,8 +100,9 @@ double plan_time(int S, int d, int dtype, const int *sizes, int C, int mode, int
     if (C == 1) mode = HCMS_MODE_SERIAL;
     double attn = 0.0;
     if (mode == HCMS_MODE_LANES) {   // the two lanes' launches keep their tiles whole
-        attn = launch_rounds(total, n, g0, 1);
+        attn = launch_rounds(total, n, g0, 1) + drain * ((C + 1) / 2);
     } else {
+        attn = drain * C;
         for (int c = 0; c < C; ++c) {
             const int64_t W = tiles * sizes[c];
             attn += launch_rounds(W, n, g0, hcms::attention_split_ways(W, S, d, dtype, n_cu));
@@ -132,13 +135,14 @@ double plan_time(int S, int d, int dtype, const int *sizes, int C, int mode, int
     return attn + copies * t_copy + syncs * beta;
 }
 
-int check_one_gpu(int S, int d, int dtype, int n_cu, double t_round, double g0, double t_copy,
-                  double beta) {
+int check_one_gpu(int S, int d, int dtype, int n_cu, double t_round, double g0, double drain,
+                  double t_copy, double beta) {
     if (S < 0) return hcms::fail(HCMS_ERR_SHAPE, "S=%d must be >= 0", S);
     if (d != 64 && d != 128) return hcms::fail(HCMS_ERR_SHAPE, "d=%d must be 64 or 128", d);
     if (dtype != HCMS_BF16 && dtype != HCMS_FP32) return hcms::fail(HCMS_ERR_DTYPE, "dtype %d", dtype);
     if (n_cu < 1) return hcms::fail(HCMS_ERR_ARG, "n_cu=%d must be >= 1", n_cu);
-    if (!finite_nonneg(t_round) || !finite_nonneg(t_copy) || !finite_nonneg(beta))
+    if (!finite_nonneg(t_round) || !finite_nonneg(t_copy) || !finite_nonneg(beta) ||
+        !finite_nonneg(drain))
         return hcms::fail(HCMS_ERR_ARG, "times must be finite and >= 0");
     if (!(g0 > 0.0 && g0 <= 1.0)) return hcms::fail(HCMS_ERR_ARG, "g0=%g must be in (0, 1]", g0);
     return HCMS_OK;
@@ -149,11 +153,12 @@ int check_one_gpu(int S, int d, int dtype, int n_cu, double t_round, double g0, 
 extern "C" {
 
 int hcms_model_plan_time(int S, int d, int dtype, const int *chunk_sizes, int n_chunks, int mode,
-                         int n_cu, double t_round, double g0, double t_copy, double beta,
-                         double *t_out) {
+                         int n_cu, double t_round, double g0, double drain, double t_copy,
+                         double beta, double *t_out) {
     int st;
     if (!t_out || !chunk_sizes) return hcms::fail(HCMS_ERR_NULL, "an argument is NULL");
-    if ((st = check_one_gpu(S, d, dtype, n_cu, t_round, g0, t_copy, beta)) != HCMS_OK) return st;
+    if ((st = check_one_gpu(S, d, dtype, n_cu, t_round, g0, drain, t_copy, beta)) != HCMS_OK)
+        return st;
     if (n_chunks < 1) return hcms::fail(HCMS_ERR_CHUNKS, "n_chunks=%d must be >= 1", n_chunks);
     for (int c = 0; c < n_chunks; ++c)
         if (chunk_sizes[c] < 1) return hcms::fail(HCMS_ERR_CHUNKS, "chunk %d has %d heads", c, chunk_sizes[c]);
@@ -164,16 +169,18 @@ int hcms_model_plan_time(int S, int d, int dtype, const int *chunk_sizes, int n_
         mode = hcms::auto_plan(S, d, dtype, chunk_sizes, n_chunks, n_cu);
     }
     if (!plan_mode(mode)) return hcms::fail(HCMS_ERR_ARG, "mode %d is not a plan", mode);
-    *t_out = plan_time(S, d, dtype, chunk_sizes, n_chunks, mode, n_cu, t_round, g0, t_copy, beta);
+    *t_out = plan_time(S, d, dtype, chunk_sizes, n_chunks, mode, n_cu, t_round, g0, drain, t_copy,
+                       beta);
     return hcms::ok();
 }
 
 int hcms_choose_chunks(int S, int H, int d, int dtype, int n_cu, double t_round, double g0,
-                       double t_copy, double beta, int max_chunks, int *sizes_out, int *mode_out,
-                       double *t_out) {
+                       double drain, double t_copy, double beta, int max_chunks, int *sizes_out,
+                       int *mode_out, double *t_out) {
     int st;
     if (!sizes_out) return hcms::fail(HCMS_ERR_NULL, "sizes_out is NULL");
-    if ((st = check_one_gpu(S, d, dtype, n_cu, t_round, g0, t_copy, beta)) != HCMS_OK) return st;
+    if ((st = check_one_gpu(S, d, dtype, n_cu, t_round, g0, drain, t_copy, beta)) != HCMS_OK)
+        return st;
     if (H < 1) return hcms::fail(HCMS_ERR_SHAPE, "H=%d must be >= 1", H);
     if (max_chunks < 1) return hcms::fail(HCMS_ERR_CHUNKS, "max_chunks=%d must be >= 1", max_chunks);
     const int top = std::min(H, max_chunks);
@@ -183,7 +190,8 @@ int hcms_choose_chunks(int S, int H, int d, int dtype, int n_cu, double t_round,
     for (int C = 1; C <= top; ++C) {
         for (int c = 0; c < C; ++c) sizes[c] = H / C + (c < H % C ? 1 : 0);
         const int mode = hcms::auto_plan(S, d, dtype, sizes.data(), C, n_cu);
-        const double t = plan_time(S, d, dtype, sizes.data(), C, mode, n_cu, t_round, g0, t_copy, beta);
+        const double t = plan_time(S, d, dtype, sizes.data(), C, mode, n_cu, t_round, g0, drain,
+                                   t_copy, beta);
         if (t < best_t) {   // ties keep the smaller chunk count
             best_t = t;
             best_mode = mode;

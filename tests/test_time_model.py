@@ -164,22 +164,23 @@ def test_round_identity():
 def test_one_gpu_model_reduces_to_the_paper_model():
     """Launches that fill whole rounds keep the attention time fixed; the
     pipelined plan of C equal chunks is then the appendix's T_hcms(C) with
-    T_comm = 4 H t_copy (pack 3 tensors, unpack 1), beta' = 2 beta per chunk
-    and T_0 = 3 beta."""
+    T_comm = 4 H t_copy (pack 3 tensors, unpack 1), per-chunk overhead
+    beta' = 2 beta + drain t_round and T_0 = 3 beta."""
     n, br = 256, 256
     for H, S in ((8, 256 * 64), (12, 256 * 128)):
         tiles = S // br
         for C in (c for c in range(1, H + 1) if H % c == 0 and (tiles * (H // c)) % n == 0):
             sizes = [H // C] * C
             t_round, t_copy, beta = 0.9, 0.004, 0.006
+            drain = 0.02
             got = tm.plan_time(S, sizes, tm.PIPELINED if C > 1 else tm.SERIAL, n, br, t_round,
-                               0.5, t_copy, beta)
+                               0.5, t_copy, beta, True, drain)
             t_attn = t_round * tiles * H / n
             if C == 1:
-                assert got == pytest.approx(t_attn + 4 * H * t_copy)
+                assert got == pytest.approx(t_attn + 4 * H * t_copy + drain * t_round)
             else:
                 assert got == pytest.approx(tm.hcms_time(3 * beta, 4 * H * t_copy, t_attn,
-                                                         2 * beta, C))
+                                                         2 * beta + drain * t_round, C))
 
 
 def test_worked_rounds_of_the_wan_p4_share():
@@ -275,20 +276,49 @@ def test_one_gpu_model_validation():
     out = ctypes.c_double()
     sz = (ctypes.c_int * 2)(2, 3)
     f = lib.hcms_model_plan_time
-    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, None) == ENULL
-    assert f(100, 96, 0, sz, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == ESHAPE
-    assert f(100, 128, 3, sz, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == EDTYPE
-    assert f(100, 128, 0, sz, 2, 9, 256, 1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == EARG
-    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 0.0, 0.0, 0.0, ctypes.byref(out)) == EARG
-    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 1.5, 0.0, 0.0, ctypes.byref(out)) == EARG
-    assert f(100, 128, 0, sz, 2, 0, 0, 1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == EARG
-    assert f(100, 128, 0, sz, 2, 0, 256, -1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == EARG
-    assert f(100, 128, 0, sz, 0, 0, 256, 1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == ECHUNKS
+    o = ctypes.byref(out)
+    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, None) == ENULL
+    assert f(100, 96, 0, sz, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, o) == ESHAPE
+    assert f(100, 128, 3, sz, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, o) == EDTYPE
+    assert f(100, 128, 0, sz, 2, 9, 256, 1.0, 0.5, 0.0, 0.0, 0.0, o) == EARG
+    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 0.0, 0.0, 0.0, 0.0, o) == EARG
+    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 1.5, 0.0, 0.0, 0.0, o) == EARG
+    assert f(100, 128, 0, sz, 2, 0, 256, 1.0, 0.5, -0.1, 0.0, 0.0, o) == EARG
+    assert f(100, 128, 0, sz, 2, 0, 0, 1.0, 0.5, 0.0, 0.0, 0.0, o) == EARG
+    assert f(100, 128, 0, sz, 2, 0, 256, -1.0, 0.5, 0.0, 0.0, 0.0, o) == EARG
+    assert f(100, 128, 0, sz, 0, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, o) == ECHUNKS
     bad = (ctypes.c_int * 2)(2, 0)
-    assert f(100, 128, 0, bad, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, ctypes.byref(out)) == ECHUNKS
+    assert f(100, 128, 0, bad, 2, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, o) == ECHUNKS
     buf = (ctypes.c_int * 4)()
     c = lib.hcms_choose_chunks
-    assert c(100, 0, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 4, buf, None, None) == ESHAPE
-    assert c(100, 4, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 0, buf, None, None) == ECHUNKS
-    assert c(100, 4, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 4, None, None, None) == ENULL
-    assert c(100, 4, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 2, buf, None, None) in (1, 2)
+    assert c(100, 0, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, 4, buf, None, None) == ESHAPE
+    assert c(100, 4, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, 0, buf, None, None) == ECHUNKS
+    assert c(100, 4, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, 4, None, None, None) == ENULL
+    assert c(100, 4, 128, 0, 256, 1.0, 0.5, 0.0, 0.0, 0.0, 2, buf, None, None) in (1, 2)
+
+
+def test_drain_adds_per_launch():
+    """Each attention launch on the critical path adds `drain` rounds: C of
+    them in one lane, ceil(C / 2) in two alternating lanes."""
+    S, sizes = 32760, (2,) * 5        # five launches of one whole round each
+    for mode, launches in ((tm.SERIAL, 5), (tm.FUSED, 5), (tm.PIPELINED, 5), (tm.LANES, 3)):
+        a = tm.plan_time(S, sizes, mode, 256, 256, 1.0, 0.5, 0.01, 0.002, True, 0.0)
+        b = tm.plan_time(S, sizes, mode, 256, 256, 1.0, 0.5, 0.01, 0.002, True, 0.03)
+        assert b - a == pytest.approx(0.03 * launches)
+
+
+def test_drain_library_matches_oracle():
+    S = 32760
+    rng = random.Random(9)
+    for _ in range(50):
+        dr = rng.uniform(0, 0.05)
+        for C in range(1, 11):
+            sz = hcms.default_chunks(10, C)
+            for mode in (hcms.MODE_SERIAL, hcms.MODE_LANES, hcms.MODE_FUSED, hcms.MODE_PIPELINED):
+                got = hcms.model_plan_time(S, 128, sz, mode, 256, 0.8, 0.4, 0.003, 0.006, drain=dr)
+                want = tm.plan_time(S, sz, mode, 256, 256, 0.8, 0.4, 0.003, 0.006, True, dr)
+                assert got == pytest.approx(want, rel=1e-12)
+        sizes2, _, t = hcms.choose_chunks(S, 10, 128, 256, 0.8, 0.4, 0.003, 0.006, drain=dr)
+        o = tm.choose_chunks(S, 10, _plan_of(S, 128), 256, 256, 0.8, 0.4, 0.003, 0.006,
+                             split=True, drain=dr)
+        assert sizes2 == o[0] and t == pytest.approx(o[1], rel=1e-12)

@@ -37,6 +37,7 @@ MUTANTS = {
     "split tail keeps its full length": ("length = {1: 1.0, 2: 2.0 / 3.0, 3: 1.0 / 3.0}[ways]",
                                          "length = 1.0"),
     "split three ways where two fit": ("return 3 if 3 * rem <= n else", "return 3 if 2 * rem <= n else"),
+    "drain once per plan": ("        attn += drain * C", "        attn += drain"),
 }
 
 PINS = [
@@ -52,6 +53,7 @@ PINS = [
     pins.test_one_gpu_model_reduces_to_the_paper_model,
     pins.test_worked_rounds_of_the_wan_p4_share,
     pins.test_worked_split_tails,
+    pins.test_drain_adds_per_launch,
 ]
 
 
