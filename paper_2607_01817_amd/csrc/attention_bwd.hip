@@ -41,8 +41,12 @@
 // transposed operands come from the row-major tiles by ds_read_b64_tr_b16.
 // A 16-byte chunk c of tile row r sits at chunk position c ^ f(r), with
 // f(r) = 4 (r mod 4) + (r / 4 mod 4), which keeps both the 16-byte row reads
-// and the transposing reads free of bank conflicts.  They use the same
-// operand values and MFMA order, so they give the same bits.
+// and the transposing reads free of bank conflicts.  The dQ form uses the
+// operand values and MFMA order of attention_dq_kernel, so the two give the
+// same bits; the dK/dV form adds the per-query statistics through one more
+// MFMA each (see there), so its rounding differs from attention_dkdv_kernel's
+// in the last bits.  Either way every query's and key's arithmetic depends on
+// S, d and the data only, never on the chunking.
 //
 // Tails: loads go through buffer resources bounded by the head's tensor (rows
 // >= S read as zeros); keys or queries past S get P = 0 and are not stored.
@@ -251,6 +255,19 @@ template <int P>
 struct Phase {
     static constexpr int value = P;
 };
+template <bool B>
+struct Flag {
+    static constexpr bool value = B;
+};
+
+// x = hi + mid + lo exactly, each a bf16 (a float's 24-bit significand in
+// three 8-bit pieces, each piece's rounding error carried into the next).
+__device__ inline void split3(float x, __bf16 &hi, __bf16 &mid, __bf16 &lo) {
+    hi = static_cast<__bf16>(x);
+    const float r = x - static_cast<float>(hi);
+    mid = static_cast<__bf16>(r);
+    lo = static_cast<__bf16>(r - static_cast<float>(mid));
+}
 
 }  // namespace bdma
 
@@ -298,6 +315,7 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
     const float Di = swap_halves_sum(dpart);
     const float Li = qi < S ? lse[static_cast<int64_t>(head) * S + qi] : 0.f;
     if (g == 0 && qi < S) delta[static_cast<int64_t>(head) * S + qi] = Di;
+    drain_vm_loads();
 
     // Lane offsets: DMA sources (row r = 4 (2 wave + i) + lane / 16, chunk at
     // position lane % 16), 16-byte row reads (row li of a 32-key half, chunk
@@ -350,9 +368,11 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
     __syncthreads();
 
     typedef __attribute__((address_space(3))) bf16x4 LdsV4;
-    // Block j in buffer P (P = j % kNB, or -1 when known only at run time).
-    auto step = [&](int j, auto ph) {
+    // Block j in buffer P (P = j % kNB, or -1 when known only at run time);
+    // only the last block (M) can hold keys past S.
+    auto step = [&](int j, auto ph, auto masked) {
         constexpr int P = decltype(ph)::value;
+        constexpr bool M = decltype(masked)::value;
         const int bi = P >= 0 ? P : j % kNB;
         const char *kb = kbase + bi * kTileB;
         const char *vb = vbase + bi * kTileB;
@@ -376,7 +396,7 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
                 for (int r = 0; r < 8; ++r) {
                     const int rr = h * 8 + r;
                     const int key = mt * 32 + (rr >> 2) * 8 + g * 4 + (rr & 3);
-                    const float p = key < kvalid
+                    const float p = !M || key < kvalid
                         ? __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rr], c, -Li)) : 0.f;
                     x[r] = p * (dpacc[rr] - Di);
                 }
@@ -397,14 +417,16 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
         wait_vm<4 * (kDist - 1)>();  // block j + 1 landed
         __syncthreads();
     };
+    const int nwhole = nkb - 1;  // every block but the last holds 64 keys below S
     int j = 0;
-    for (; j + 4 <= nkb; j += 4) {
-        step(j, Phase<0>{});
-        step(j + 1, Phase<1>{});
-        step(j + 2, Phase<2>{});
-        step(j + 3, Phase<3>{});
+    for (; j + 4 <= nwhole; j += 4) {
+        step(j, Phase<0>{}, Flag<false>{});
+        step(j + 1, Phase<1>{}, Flag<false>{});
+        step(j + 2, Phase<2>{}, Flag<false>{});
+        step(j + 3, Phase<3>{}, Flag<false>{});
     }
-    for (; j < nkb; ++j) step(j, Phase<-1>{});
+    for (; j < nwhole; ++j) step(j, Phase<-1>{}, Flag<false>{});
+    step(nwhole, Phase<-1>{}, Flag<true>{});
     wait_vm<0>();  // no load into LDS is pending when the workgroup ends
 
     if (qi < S) {
@@ -490,8 +512,8 @@ struct QStage {
 // attention_dq_dma_kernel, read as 16-byte rows (S = Q K^T, dP = dO V^T) and
 // transposed by ds_read_b64_tr_b16 (dV^T += dO^T P, dK^T += Q^T dS).  Waves
 // 0 and 1 also load L and D (4 bytes per lane), so they count one more load
-// per block.  The operand values and the MFMA order are those of
-// attention_dkdv_kernel.
+// per block.  L and D enter the scores through one more MFMA each, and the two
+// waves of each SIMD take a step's work in different orders (both below).
 __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention_dkdv_dma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
     const __bf16 *__restrict__ dout, const float *__restrict__ lse, const float *__restrict__ delta,
@@ -538,6 +560,7 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
         *reinterpret_cast<u32x4 *>(vrows + row * QLds<D>::RS + ch * 8) =
             load8<__bf16>(vr, static_cast<unsigned>((key0 + row) * D + ch * 8) * 2);
     }
+    drain_vm_loads();
     f32x16 dkacc[DT], dvacc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -582,27 +605,40 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
         if (wave == 0) load_lds_b32(lds0 + 2 * kNB * QTB + b * STB, lr, lane * 4, blk * kQB * 4);
         if (wave == 1) load_lds_b32(lds0 + 2 * kNB * QTB + kNB * STB + b * STB, er, lane * 4, blk * kQB * 4);
     };
-    // All but the latest (kDist - 1) blocks' loads of this wave landed.
-    auto wait_blocks = [&]() {
-        if (wave < 2) wait_vm<3 * (kDist - 1)>();
-        else wait_vm<2 * (kDist - 1)>();
+    // All but the latest block's loads of this wave landed.
+    auto wait_one_block = [&]() {
+        if (wave < 2) wait_vm<3>();
+        else wait_vm<2>();
     };
 
 #pragma unroll
     for (int blk = 0; blk < kDist; ++blk) issue(blk);
-    wait_blocks();  // block 0 landed (and the V rows were stored)
+    wait_one_block();  // blocks 0 and 1 landed (and the V rows were stored)
     __syncthreads();
 
-    typedef __attribute__((address_space(3))) bf16x4 LdsV4;
-    auto step = [&](int i, auto ph) {
-        constexpr int P = decltype(ph)::value;
-        const int bi = P >= 0 ? P : i % kNB;
+    // The statistics of a block's queries enter S and dP through one more
+    // MFMA each: A holds -L_i / c (or -D_i) of query i = li in three bf16
+    // pieces at k = 0..2, B holds ones there and zeros elsewhere, so the
+    // product adds the exact fp32 value to all 32 keys' entries of that query
+    // (its accumulator row), with no broadcast of per-row values.
+    const bf16x8 ones = g == 0 ? bf16x8{1, 1, 1, 0, 0, 0, 0, 0} : bf16x8{};
+    const float inv_c = 1.0f / c;
+    auto pieces = [](float x) {
+        __bf16 h, m, l;
+        split3(x, h, m, l);
+        return bf16x8{h, m, l, 0, 0, 0, 0, 0};
+    };
+
+    // s = Q K^T - L / c and dp = dO V^T - D of the block in buffer bi, rows =
+    // queries; the statistic is added last, so dp - D rounds once, as a
+    // subtraction would (a query whose dP equals D gets dS = 0 exactly).
+    auto scores = [&](int bi, f32x16 &s, f32x16 &dp) {
         const char *qb = qbase + bi * QTB;
         const char *db = dbase + bi * QTB;
         const float *lb = reinterpret_cast<const float *>(lbase + bi * STB);
         const float *eb = reinterpret_cast<const float *>(ebase + bi * STB);
-        issue(i + kDist);
-        f32x16 s = {}, dp = {};
+        s = f32x16{};
+        dp = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8 qa = *reinterpret_cast<const bf16x8 *>(qb + row_rd[kk]);
@@ -611,23 +647,27 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
             s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], s, 0, 0, 0);
             dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
         }
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pieces(-lb[li] * inv_c), ones, s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pieces(-eb[li]), ones, dp, 0, 0, 0);
+    };
+    typedef __attribute__((address_space(3))) bf16x4 LdsV4;
+    // P and dS of block i from its scores (queries past S get P = 0 when M),
+    // then dV^T += dO^T P and dK^T += Q^T dS from buffer bi.
+    auto products = [&](int i, int bi, const f32x16 &s, const f32x16 &dp, auto masked) {
+        constexpr bool M = decltype(masked)::value;
+        const char *qb = qbase + bi * QTB;
+        const char *db = dbase + bi * QTB;
         const int qvalid = S - i * kQB;
         bf16x8 pb[2], dsb[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            const f32x4 l0 = *reinterpret_cast<const f32x4 *>(lb + h * 16 + g * 4);
-            const f32x4 l1 = *reinterpret_cast<const f32x4 *>(lb + h * 16 + 8 + g * 4);
-            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(eb + h * 16 + g * 4);
-            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(eb + h * 16 + 8 + g * 4);
             f32x8 p, ds;
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
                 const int rr = h * 8 + r;
                 const int qrow = (rr >> 2) * 8 + g * 4 + (rr & 3);
-                const float Lr = (r < 4) ? l0[r & 3] : l1[r & 3];
-                const float Dr = (r < 4) ? e0[r & 3] : e1[r & 3];
-                p[r] = qrow < qvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[rr], c, -Lr)) : 0.f;
-                ds[r] = p[r] * (dp[rr] - Dr);
+                p[r] = !M || qrow < qvalid ? __builtin_amdgcn_exp2f(s[rr] * c) : 0.f;
+                ds[r] = p[r] * dp[rr];
             }
             pb[h] = __builtin_convertvector(p, bf16x8);
             dsb[h] = __builtin_convertvector(ds, bf16x8);
@@ -646,17 +686,47 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
                 dvacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, pb[qs], dvacc[dt], 0, 0, 0);
                 dkacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, dsb[qs], dkacc[dt], 0, 0, 0);
             }
-        wait_blocks();  // block i + 1 landed
-        __syncthreads();
     };
-    int i = 0;
-    for (; i + 4 <= nqb; i += 4) {
-        step(i, Phase<0>{});
-        step(i + 1, Phase<1>{});
-        step(i + 2, Phase<2>{});
-        step(i + 3, Phase<3>{});
-    }
-    for (; i < nqb; ++i) step(i, Phase<-1>{});
+    // The two waves of a SIMD (w and w + 4) take a step's work in different
+    // orders, so that one's MFMAs run while the other computes exponentials:
+    // waves 0-3 compute block i's scores, then its softmax and products;
+    // waves 4-7 start a step with the softmax and products of block i (scores
+    // from the step before) and end it with the scores of block i + 1.  Step
+    // i loads block i + 3 into the buffer block i - 1 left and ends when
+    // block i + 2 has landed, which the late scores of waves 4-7 need.
+    // Each group runs its own loop (the same number of barriers).
+    const int nwhole = nqb - 1;  // every block but the last holds 32 queries below S
+    auto run = [&](auto late_flag) {
+        constexpr bool kLate = decltype(late_flag)::value;
+        f32x16 sc, dpc;
+        if (kLate) scores(0, sc, dpc);
+        auto step = [&](int i, auto ph, auto masked) {
+            constexpr int P = decltype(ph)::value;
+            constexpr bool M = decltype(masked)::value;
+            const int bi = P >= 0 ? P : i % kNB;
+            issue(i + kDist);
+            if constexpr (!kLate) {
+                scores(bi, sc, dpc);
+                products(i, bi, sc, dpc, masked);
+            } else {
+                products(i, bi, sc, dpc, masked);
+                if constexpr (!M) scores((bi + 1) & (kNB - 1), sc, dpc);
+            }
+            wait_one_block();
+            __syncthreads();
+        };
+        int i = 0;
+        for (; i + 4 <= nwhole; i += 4) {
+            step(i, Phase<0>{}, Flag<false>{});
+            step(i + 1, Phase<1>{}, Flag<false>{});
+            step(i + 2, Phase<2>{}, Flag<false>{});
+            step(i + 3, Phase<3>{}, Flag<false>{});
+        }
+        for (; i < nwhole; ++i) step(i, Phase<-1>{}, Flag<false>{});
+        step(nwhole, Phase<-1>{}, Flag<true>{});
+    };
+    if (wave < 4) run(Flag<false>{});
+    else run(Flag<true>{});
     wait_vm<0>();
 
     if (kj < S) {

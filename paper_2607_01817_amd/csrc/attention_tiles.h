@@ -79,6 +79,16 @@ __device__ inline void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
+// Wait for every vector memory load of this wave (s_waitcnt vmcnt(0),
+// expcnt and lgkmcnt left open: simm16 0x0F70), issued as the compiler's own
+// instruction.  The compiler places waits for register loads by counting the
+// loads it can see; it does not see the loads into LDS above.  After a
+// prologue that fills registers by plain loads, its first use of those
+// registers inside a key loop would otherwise get a vmcnt wait on every
+// iteration, which in hardware also waits for the LDS loads in flight.  This
+// wait, which the compiler does see, ends those loads before the loop.
+__device__ inline void drain_vm_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Position of key `k` (0..63) inside a transposed V row: bits 2 and 3 swapped.
 __device__ inline int vt_pos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
 
