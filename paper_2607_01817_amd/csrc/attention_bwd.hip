@@ -388,6 +388,19 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
                 sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
                 dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
             }
+            // The K^T operands of this half's dQ products, read before the
+            // softmax so that its arithmetic covers their latency.
+            bf16x8 kt[DT][2];
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const char *p0 = kb + (mt * 2 + h) * 16 * kRowB;
+                    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p0 + tr_rd[0][dt]));
+                    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p0 + tr_rd[1][dt]));
+                    kt[dt][h] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                }
+            __builtin_amdgcn_sched_barrier(0);
             bf16x8 dsb[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
@@ -405,14 +418,8 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int ks = mt * 2 + h;
-                    const char *p0 = kb + ks * 16 * kRowB;
-                    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p0 + tr_rd[0][dt]));
-                    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(p0 + tr_rd[1][dt]));
-                    const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                    dqacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[h], dqacc[dt], 0, 0, 0);
-                }
+                for (int h = 0; h < 2; ++h)
+                    dqacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dt][h], dsb[h], dqacc[dt], 0, 0, 0);
         }
         wait_vm<4 * (kDist - 1)>();  // block j + 1 landed
         __syncthreads();
