@@ -734,8 +734,11 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
 // Layer neighbours: projections and rotary position embedding
 // ---------------------------------------------------------------------------
 
-// Y[M][N] = X[M][K] W[N][K]^T: shapes, pointers, alignment, aliasing.
-int check_linear(const void *x, const void *w, const void *y, int M, int N, int K, int dtype) {
+// Y[M][N] = X[M][K] W[N][K]^T: shapes, pointers, alignment and, when
+// y_is_matrix, that the [M][N] output overlaps neither input (the QKV
+// projection writes three [M][N/3] tensors instead and checks them itself).
+int check_linear(const void *x, const void *w, const void *y, int M, int N, int K, int dtype,
+                 bool y_is_matrix = true) {
     int st;
     if ((st = check_dtype(dtype)) != HCMS_OK) return st;
     if (M < 0 || N < 0) return fail(HCMS_ERR_SHAPE, "need M >= 0 and N >= 0 (M=%d N=%d)", M, N);
@@ -751,7 +754,7 @@ int check_linear(const void *x, const void *w, const void *y, int M, int N, int 
     const int64_t es = elem_bytes(dtype);
     const int64_t xb = static_cast<int64_t>(M) * K * es, wb = static_cast<int64_t>(N) * K * es;
     const int64_t yb = static_cast<int64_t>(M) * N * es;
-    if (overlaps(y, yb, x, xb) || overlaps(y, yb, w, wb))
+    if (y_is_matrix && (overlaps(y, yb, x, xb) || overlaps(y, yb, w, wb)))
         return fail(HCMS_ERR_ALIAS, "the output overlaps an input");
     return HCMS_OK;
 }
@@ -799,7 +802,7 @@ int check_qkv(const void *x, const void *w, const float *table, const int *grid,
                     S, H, d);
     if (static_cast<int64_t>(3) * H * d > (1 << 20))
         return fail(HCMS_ERR_SHAPE, "3 H d = %lld exceeds 2^20", 3LL * H * d);
-    if ((st = check_linear(x, w, q, S, 3 * H * d, D, dtype)) != HCMS_OK) return st;
+    if ((st = check_linear(x, w, q, S, 3 * H * d, D, dtype, false)) != HCMS_OK) return st;
     *ax = hcms::RopeAxes{};
     if (S == 0) return HCMS_OK;
     if (!k || !v) return fail(HCMS_ERR_NULL, "k or v is NULL");

@@ -582,6 +582,9 @@ def test_qkv_projection_validation(lib):
     assert call(k=D_ + 1024) == EALIAS          # outputs overlap
     assert call(q=A) == EALIAS                  # output overlaps x
     assert call(table=D_ + 4096) == EALIAS      # table overlaps q
+    # x right after q's [S][H][d] bytes overlaps nothing: the check goes on to
+    # the table's alignment (q is not a [S][3 H d] matrix).
+    assert call(x=D_ + 240 * 4 * 64 * 2, table=C_ + 8) == EALIGN
     assert call(S=0, x=None, q=None, k=None, v=None) == OK
     # Without a table, grid and pairs are not looked at.
     assert f(A, B, None, None, None, 0, D_, D_ + big, D_ + 2 * big, 0, 256, 4, 64, 0, None) == OK
