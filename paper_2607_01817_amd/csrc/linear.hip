@@ -29,9 +29,12 @@
 //     issued two k-blocks before its MFMAs; every operand read from LDS feeds
 //     2 (W) or 4 (X) MFMAs;
 //   * tiles are ordered in groups of 8 row tiles (all column tiles of a group
-//     before the next group), and the 8 XCDs each take a contiguous range of
-//     that order, so the 32 workgroups resident on an XCD share 8 X panels and
-//     4 W panels through its L2.
+//     before the next group); the grid holds one persistent workgroup per CU,
+//     each round of the grid takes the next G tiles of that order, and the 8
+//     XCDs each take a contiguous range of a round, so the 32 workgroups
+//     resident on an XCD share 8 X panels and 4 W panels through its L2;
+//   * a workgroup's tiles form one stream of k-blocks, so the next tile's
+//     first blocks load during the current tile's last ones and its epilogue.
 //
 // Tails: rows past M or N are read through buffer resources bounded by the
 // last row, so they read as zeros; rows past M and columns past N are not
@@ -59,6 +62,7 @@ constexpr int kNT = kBN / kWavesN / 32;      // 32-column tiles per wave
 constexpr int kRow = kBK + 8;            // LDS row stride, elements (144 bytes)
 constexpr int kTile = 256 * kRow;        // one staged 256 x 64 block, elements
 constexpr int kGroupM = 8;               // row tiles per group of the tile order
+constexpr int kPersistK = 1024;          // longest K run by persistent workgroups
 constexpr int kPass = 256 * (kBK / 8) / kThreads;  // 16-byte chunks per thread per block
 constexpr int kRowsPerPass = kThreads / 8;
 
@@ -132,24 +136,34 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
     __shared__ __attribute__((aligned(16))) __bf16 xt[2][kTile];
     __shared__ __attribute__((aligned(16))) __bf16 wt[2][kTile];
 
-    // XCD-aware order: workgroup b runs on XCD b % 8 and takes position
-    // xcd * per + b / 8 of the grouped tile order.
-    const int nb = gridDim.x, b = blockIdx.x;
-    const int xcd = b & 7, per = nb >> 3, rem = nb & 7;
-    const int L = xcd * per + min(xcd, rem) + (b >> 3);
-    const int group = L / (kGroupM * tiles_n);
-    const int first_m = group * kGroupM;
-    const int gm = min(tiles_m - first_m, kGroupM);
-    const int in_group = L - group * kGroupM * tiles_n;
-    const int tm = first_m + in_group % gm;
-    const int tn = in_group / gm;
-    const int m0 = tm * kBM, n0 = tn * kBN;
+    // Persistent tiles: the grid has at most one workgroup per CU, and round r
+    // of workgroup b computes tile r G + slot(b) of the grouped order (G = the
+    // grid size).  Workgroup b runs on XCD b % 8, and slot(b) gives each XCD a
+    // contiguous range of every round, so the workgroups resident on an XCD
+    // share a few X and W panels through its L2.
+    const int G = gridDim.x, b = blockIdx.x;
+    const int xcd = b & 7, per = G >> 3, rem = G & 7;
+    const int slot = xcd * per + min(xcd, rem) + (b >> 3);
+    const int n_tiles = tiles_m * tiles_n;
+    if (slot >= n_tiles) return;
+    const int n_mine = (n_tiles - 1 - slot) / G + 1;
+    auto origin = [&](int r, int &m0, int &n0) {
+        const int L = r * G + slot;
+        const int group = L / (kGroupM * tiles_n);
+        const int first_m = group * kGroupM;
+        const int gm = min(tiles_m - first_m, kGroupM);
+        const int in_group = L - group * kGroupM * tiles_n;
+        m0 = (first_m + in_group % gm) * kBM;
+        n0 = (in_group / gm) * kBN;
+    };
 
     const unsigned row_bytes = static_cast<unsigned>(K) * sizeof(T);
-    const __amdgpu_buffer_rsrc_t xs =
-        span_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<int64_t>(M - m0) * row_bytes);
-    const __amdgpu_buffer_rsrc_t ws =
-        span_rsrc(w + static_cast<int64_t>(n0) * K, static_cast<int64_t>(N - n0) * row_bytes);
+    auto x_rsrc = [&](int m0) {
+        return span_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<int64_t>(M - m0) * row_bytes);
+    };
+    auto w_rsrc = [&](int n0) {
+        return span_rsrc(w + static_cast<int64_t>(n0) * K, static_cast<int64_t>(N - n0) * row_bytes);
+    };
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -162,25 +176,93 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
 #pragma unroll
         for (int mt = 0; mt < kMT; ++mt) acc[nt][mt] = f32x16{};
 
-    // NSETS register sets carry the blocks from global memory to LDS.  With
-    // two (bf16 storage), block b is loaded into set b & 1 during k-block
-    // b - 2 and stored to LDS buffer b & 1 after k-block b - 1's MFMAs, so each
-    // load has two k-blocks to arrive; with one (fp32 storage, whose loads
-    // need twice the registers) it is loaded during k-block b - 1.  The loop
-    // has no branches: the loads of blocks past the end read within the
-    // resources (the next row's data or zeros) and the last store goes to a
-    // buffer nobody reads.
+    // ---- Y[m][n .. n + 3] of the tile at (m0, n0) from the D^T accumulators,
+    // rounded to T ----
+    auto store_tile = [&](int m0, int n0) {
+#pragma unroll
+        for (int mt = 0; mt < kMT; ++mt) {
+            const int m = m0 + wm * kMT * 32 + mt * 32 + li;
+            if (m >= M) continue;
+            // Per grid axis, the table entry of pair 0 of the axis at token m's
+            // coordinate (QKV epilogue with a rotation only).
+            int tab_row[kRopeMaxAxes] = {};
+            if (QKV && qo.table != nullptr) {
+                int rest = m;
+                for (int a = qo.ax.n_axes - 1; a >= 0; --a) {
+                    const int cc = rest % qo.ax.grid[a];
+                    rest /= qo.ax.grid[a];
+                    tab_row[a] = qo.ax.tab_off[a] + cc * qo.ax.pairs[a] - qo.ax.pair_start[a];
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt)
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const int n = n0 + wn * kNT * 32 + nt * 32 + rb * 8 + g * 4;
+                    if (n >= N) continue;
+                    f32x4 v = {acc[nt][mt][rb * 4 + 0], acc[nt][mt][rb * 4 + 1],
+                               acc[nt][mt][rb * 4 + 2], acc[nt][mt][rb * 4 + 3]};
+                    if constexpr (QKV) {
+                        const int hd = qo.H * qo.d;
+                        const int z = n / hd, r = n - z * hd;
+                        if (z < 2 && qo.table != nullptr) {
+                            const int e = r % qo.d;  // a multiple of 4: pairs e/2 and e/2 + 1
+#pragma unroll
+                            for (int q2 = 0; q2 < 2; ++q2) {
+                                const int p = e / 2 + q2;
+                                int a = 0;
+                                while (a + 1 < qo.ax.n_axes && p >= qo.ax.pair_start[a + 1]) ++a;
+                                const f32x2 cs =
+                                    *reinterpret_cast<const f32x2 *>(qo.table + 2 * (tab_row[a] + p));
+                                const float x0 = v[2 * q2], x1 = v[2 * q2 + 1];
+                                v[2 * q2] = __builtin_fmaf(x0, cs[0], -(x1 * cs[1]));
+                                v[2 * q2 + 1] = __builtin_fmaf(x0, cs[1], x1 * cs[0]);
+                            }
+                        }
+                        store4(qo.dst[z] + static_cast<int64_t>(m) * hd + r, v);
+                    } else {
+                        store4(y + static_cast<int64_t>(m) * N + n, v);
+                    }
+                }
+        }
+    };
+
+    // The k-blocks of the workgroup's tiles form one stream: NSETS register
+    // sets carry its blocks from global memory to LDS.  With two (bf16
+    // storage), stream block s is loaded into set s & 1 during block s - 2 and
+    // stored to LDS buffer s & 1 after block s - 1's MFMAs, so each load has
+    // two k-blocks to arrive, also across a tile boundary (the next tile's
+    // first blocks load during the current tile's last ones and its
+    // epilogue); with one (fp32 storage, whose loads need twice the
+    // registers) it is loaded during block s - 1.  The loads of blocks past
+    // the stream's end read within the last tile's resources (the next row's
+    // data or zeros) and the last store goes to a buffer nobody reads.
     constexpr int NSETS = sizeof(T) == 2 ? 2 : 1;
     const int nkb = K / kBK;
+    int ld_r = 0, ld_kb = 0;  // tile round and k-block of the next load
+    int lm0, ln0;
+    origin(0, lm0, ln0);
+    __amdgpu_buffer_rsrc_t lxs = x_rsrc(lm0), lws = w_rsrc(ln0);
+    auto load_next = [&](Stager<T> &st) {
+        st.load(lxs, lws, row_bytes, ld_kb * kBK, tid);
+        if (++ld_kb == nkb && ld_r + 1 < n_mine) {
+            ld_kb = 0;
+            ++ld_r;
+            origin(ld_r, lm0, ln0);
+            lxs = x_rsrc(lm0);
+            lws = w_rsrc(ln0);
+        }
+    };
+
     Stager<T> st[NSETS];
-    st[0].load(xs, ws, row_bytes, 0, tid);
+    load_next(st[0]);
     st[0].store(xt[0], wt[0], tid);
-    if (NSETS == 2) st[1 % NSETS].load(xs, ws, row_bytes, kBK, tid);
+    if (NSETS == 2) load_next(st[1 % NSETS]);
     __syncthreads();
-    auto step = [&](int kb, Stager<T> &ld, const Stager<T> &sto) {
-        ld.load(xs, ws, row_bytes, (kb + NSETS) * kBK, tid);
-        const __bf16 *xa = xt[kb & 1] + (wm * kMT * 32 + li) * kRow + g * 8;
-        const __bf16 *wa = wt[kb & 1] + (wn * kNT * 32 + li) * kRow + g * 8;
+    auto step = [&](int s, Stager<T> &ld, const Stager<T> &sto) {
+        load_next(ld);
+        const __bf16 *xa = xt[s & 1] + (wm * kMT * 32 + li) * kRow + g * 8;
+        const __bf16 *wa = wt[s & 1] + (wn * kNT * 32 + li) * kRow + g * 8;
 #pragma unroll
         for (int ks = 0; ks < kBK / 16; ++ks) {
             bf16x8 a[kNT], bx[kMT];
@@ -197,63 +279,37 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
                     acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nt], bx[mt], acc[nt][mt],
                                                                           0, 0, 0);
         }
-        sto.store(xt[(kb + 1) & 1], wt[(kb + 1) & 1], tid);
+        sto.store(xt[(s + 1) & 1], wt[(s + 1) & 1], tid);
         interleave_k_block();
         __syncthreads();
     };
-    int kb = 0;
-    for (; kb + 1 < nkb; kb += 2) {
-        step(kb, st[0], st[1 % NSETS]);
-        step(kb + 1, st[1 % NSETS], st[0]);
-    }
-    if (kb < nkb) step(kb, st[0], st[1 % NSETS]);
-
-    // ---- Y[m][n .. n + 3] from the D^T accumulators, rounded to T ----
-#pragma unroll
-    for (int mt = 0; mt < kMT; ++mt) {
-        const int m = m0 + wm * kMT * 32 + mt * 32 + li;
-        if (m >= M) continue;
-        // Per grid axis, the table entry of pair 0 of the axis at token m's
-        // coordinate (QKV epilogue with a rotation only).
-        int tab_row[kRopeMaxAxes] = {};
-        if (QKV && qo.table != nullptr) {
-            int rest = m;
-            for (int a = qo.ax.n_axes - 1; a >= 0; --a) {
-                const int cc = rest % qo.ax.grid[a];
-                rest /= qo.ax.grid[a];
-                tab_row[a] = qo.ax.tab_off[a] + cc * qo.ax.pairs[a] - qo.ax.pair_start[a];
-            }
+    // The k-blocks of one tile run in a loop of two steps without branches
+    // (register set and LDS buffer follow the stream index's parity), so the
+    // compiler's waits for the staged loads stay two blocks deep; the
+    // epilogue sits between tiles.
+    int s = 0;
+    for (int r = 0; r < n_mine; ++r) {
+        int kb = 0;
+        if (s & 1) {
+            step(s, st[1 % NSETS], st[0]);
+            ++s;
+            ++kb;
         }
+        for (; kb + 1 < nkb; kb += 2, s += 2) {
+            step(s, st[0], st[1 % NSETS]);
+            step(s + 1, st[1 % NSETS], st[0]);
+        }
+        if (kb < nkb) {
+            step(s, st[0], st[1 % NSETS]);
+            ++s;
+        }
+        int m0, n0;
+        origin(r, m0, n0);
+        store_tile(m0, n0);
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                const int n = n0 + wn * kNT * 32 + nt * 32 + rb * 8 + g * 4;
-                if (n >= N) continue;
-                f32x4 v = {acc[nt][mt][rb * 4 + 0], acc[nt][mt][rb * 4 + 1],
-                           acc[nt][mt][rb * 4 + 2], acc[nt][mt][rb * 4 + 3]};
-                if constexpr (QKV) {
-                    const int hd = qo.H * qo.d;
-                    const int z = n / hd, r = n - z * hd;
-                    if (z < 2 && qo.table != nullptr) {
-                        const int e = r % qo.d;  // a multiple of 4: pairs e/2 and e/2 + 1
-#pragma unroll
-                        for (int q2 = 0; q2 < 2; ++q2) {
-                            const int p = e / 2 + q2;
-                            int a = 0;
-                            while (a + 1 < qo.ax.n_axes && p >= qo.ax.pair_start[a + 1]) ++a;
-                            const f32x2 cs =
-                                *reinterpret_cast<const f32x2 *>(qo.table + 2 * (tab_row[a] + p));
-                            const float x0 = v[2 * q2], x1 = v[2 * q2 + 1];
-                            v[2 * q2] = __builtin_fmaf(x0, cs[0], -(x1 * cs[1]));
-                            v[2 * q2 + 1] = __builtin_fmaf(x0, cs[1], x1 * cs[0]);
-                        }
-                    }
-                    store4(qo.dst[z] + static_cast<int64_t>(m) * hd + r, v);
-                } else {
-                    store4(y + static_cast<int64_t>(m) * N + n, v);
-                }
-            }
+            for (int mt = 0; mt < kMT; ++mt) acc[nt][mt] = f32x16{};
     }
 }
 
@@ -278,8 +334,17 @@ template <typename T, bool QKV>
 hipError_t launch_typed(const void *x, const void *w, void *y, int M, int N, int K,
                         const QkvOut<T> &qo, hipStream_t stream) {
     const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
-    const int64_t blocks = static_cast<int64_t>(tiles_m) * tiles_n;
-    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    const int64_t tiles = static_cast<int64_t>(tiles_m) * tiles_n;
+    if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+    int device = 0, n_cu = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return e;
+    // Short reductions (K of at most kPersistK) run one persistent workgroup
+    // per CU, whose tiles stream without a pipeline refill; longer ones one
+    // workgroup per tile.
+    const int64_t blocks = K <= kPersistK && tiles > n_cu ? n_cu : tiles;
+    if (blocks < 1) return hipErrorInvalidValue;
     linear_kernel<T, QKV><<<static_cast<unsigned>(blocks), kThreads, 0, stream>>>(
         static_cast<const T *>(x), static_cast<const T *>(w), static_cast<T *>(y), M, N, K, tiles_m,
         tiles_n, qo);
