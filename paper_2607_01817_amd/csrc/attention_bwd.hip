@@ -381,12 +381,24 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt) {
             f32x16 sacc = {}, dpacc = {};
+            // Row operands read two k-steps ahead of their MFMAs (the fences
+            // keep the compiler from moving the reads next to their use).
+            bf16x8 ka[3], va[3];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                ka[kk] = *reinterpret_cast<const bf16x8 *>(kb + row_rd[kk] + mt * 32 * kRowB);
+                va[kk] = *reinterpret_cast<const bf16x8 *>(vb + row_rd[kk] + mt * 32 * kRowB);
+            }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
-                const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kb + row_rd[kk] + mt * 32 * kRowB);
-                const bf16x8 va = *reinterpret_cast<const bf16x8 *>(vb + row_rd[kk] + mt * 32 * kRowB);
-                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
-                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
+                if (kk + 2 < KK) {
+                    ka[(kk + 2) % 3] = *reinterpret_cast<const bf16x8 *>(kb + row_rd[kk + 2] + mt * 32 * kRowB);
+                    va[(kk + 2) % 3] = *reinterpret_cast<const bf16x8 *>(vb + row_rd[kk + 2] + mt * 32 * kRowB);
+                }
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kk % 3], qreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[kk % 3], doreg[kk], dpacc, 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
             // The K^T operands of this half's dQ products, read before the
             // softmax so that its arithmetic covers their latency.
