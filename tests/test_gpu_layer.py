@@ -42,9 +42,12 @@ def _check_close(got: np.ndarray, want: np.ndarray, what: str, rel_max: float = 
 
 @pytest.mark.parametrize("M,N,K,dtype", [
     (1, 8, 64, torch.bfloat16), (300, 264, 128, torch.bfloat16), (257, 520, 640, torch.bfloat16),
-    (512, 256, 256, torch.bfloat16), (77, 40, 192, torch.float32), (256, 512, 64, torch.float32)])
+    (512, 256, 256, torch.bfloat16), (77, 40, 192, torch.float32), (256, 512, 64, torch.float32),
+    (2049, 8200, 320, torch.bfloat16), (2049, 8200, 192, torch.float32)])
 def test_linear_matches_oracle(hcms, M, N, K, dtype):
-    """Row, column and tile tails, both storage types."""
+    """Row, column and tile tails, both storage types; the last two have more
+    tiles (9 x 33) than CUs and a short K, so persistent workgroups take
+    several tiles each, with an odd number of k-blocks (fp32, K = 192)."""
     log(f"[linear] M={M} N={N} K={K} {dtype}")
     g = torch.Generator().manual_seed(M * 1000 + N + K)
     x = torch.randn(M, K, generator=g).to(dtype)
