@@ -56,19 +56,41 @@ def flush_mall(buf: torch.Tensor):
     buf.amax()
 
 
-def time_region(fn, reps: int, stream=None) -> list[float]:
-    """Per-rep milliseconds of fn() from events on `stream` (default: current)."""
-    stream = stream or torch.cuda.current_stream()
-    out = []
-    for _ in range(reps):
+class EventTimer:
+    """Events around calls enqueued back to back on one stream, read after a
+    single synchronisation at the end.  The host stays ahead of the GPU, so a
+    call's span is its GPU work: a synchronisation after every call would leave
+    the GPU idle while the host issues the next one (Python and the ctypes
+    call, tens of microseconds) and count that idle time too."""
+
+    def __init__(self, stream=None):
+        self.stream = stream or torch.cuda.current_stream()
+        self.marks = []
+
+    def time(self, key, fn):
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
+        a.record(self.stream)
         fn()
-        b.record(stream)
-        b.synchronize()
-        out.append(a.elapsed_time(b))
-    return out
+        b.record(self.stream)
+        self.marks.append((key, a, b))
+
+    def results(self) -> dict:
+        self.stream.synchronize()
+        torch.cuda.synchronize()
+        out = {}
+        for key, a, b in self.marks:
+            out.setdefault(key, []).append(a.elapsed_time(b))
+        self.marks = []
+        return out
+
+
+def time_region(fn, reps: int, stream=None) -> list[float]:
+    """Per-rep milliseconds of fn() repeated back to back (EventTimer)."""
+    t = EventTimer(stream)
+    for _ in range(reps):
+        t.time(0, fn)
+    return t.results().get(0, [])
 
 
 def measured_traffic(workload: str, chunks, plan: str) -> float | None:
@@ -168,12 +190,12 @@ def compare_modes(ctx, w, chunks, reps: int, dev, modes=None):
 
     for m in modes:                 # one warm run of each
         run(m)()
-    times = {m: [] for m in modes}
+    timer = EventTimer()
     for r in range(reps + 1):
         for m in (modes if r % 2 == 0 else modes[::-1]):
-            t = time_region(run(m), 1)
-            if r > 0:
-                times[m] += t
+            timer.time((m, r), run(m))
+    spans = timer.results()
+    times = {m: [t for r in range(1, reps + 1) for t in spans[(m, r)]] for m in modes}
     ctx.forward(q, k, v, w.P, w.scale, chunks, mode=hcms.MODE_AUTO, out=out, workspaces=ws)
     res = {"workload": w.name, "chunks": list(chunks), "auto_runs": MODE_NAMES[ctx.last_mode]}
     ser = quartiles(times["serial"])
@@ -216,12 +238,12 @@ def time_model_sweep(ctx, w, reps: int, dev):
 
         for m in modes:
             run(m)
-        times = {m: [] for m in modes}
+        timer = EventTimer()
         for r in range(reps + 1):
             for m in (modes if r % 2 == 0 else modes[::-1]):
-                t = time_region(lambda: run(m), 1)
-                if r > 0:
-                    times[m] += t
+                timer.time((m, r), lambda: run(m))
+        spans = timer.results()
+        times = {m: [t for r in range(1, reps + 1) for t in spans[(m, r)]] for m in modes}
         for m in modes:
             med[m].append(float(np.median(times[m])))
         ctx.set_timing(reps)
@@ -267,9 +289,9 @@ def adaptive_chunks(ctx, sweeps):
         g0 = 1 and g0 -> 0);
       * t_copy = the layout kernels at C = 1 over 4 H head-tensors;
       * beta = (Alg. 1 - serial) at C = 1 over its 7 synchronisations;
-      * drain (rounds per attention launch on the critical path) and a
-        constant T_0 per workload by least squares on the auto plans' step
-        times' residuals.
+      * per workload, the drain (rounds per attention launch on the
+        critical path) and a constant T_0 by least squares on its auto
+        plans' step-time residuals (drain >= 0).
     Reports the model's prediction of the auto plan per C against the
     measured auto time and whether the chosen C measures within 1 % of the
     sweep's best."""
@@ -291,28 +313,28 @@ def adaptive_chunks(ctx, sweeps):
         S, H = sw["S"], sw["H"]
         par[sw["workload"]] = (kappa * S, sw["layout_kernels_ms"][0] / (4 * H),
                                max(0.0, (sw["pipelined_ms"][0] - sw["serial_ms"][0]) / 7))
-    # Drain and T_0 from the step times: residual = T_0(workload) + drain x
-    # (the plan's launches on the critical path x t_round).
-    rows, ys = [], []
-    names = [sw["workload"] for sw in sweeps]
+    # Per workload, the drain and T_0 from its step times: residual = T_0 +
+    # drain x (the plan's launches on the critical path x t_round).
+    t0, drains = {}, {}
     for sw in sweeps:
         t_round, t_copy, beta = par[sw["workload"]]
+        rows, ys = [], []
         for C in sw["chunk_counts"]:
             sz = hcms.default_chunks(sw["H"], C)
-            for mode, meas in ((hcms.MODE_AUTO, sw["auto_ms"][C - 1]),):
-                p0 = hcms.model_plan_time(sw["S"], 128, sz, mode, n, t_round, g0, t_copy, beta)
-                p1 = hcms.model_plan_time(sw["S"], 128, sz, mode, n, t_round, g0, t_copy, beta,
-                                          drain=1.0)
-                rows.append([1.0 if nm == sw["workload"] else 0.0 for nm in names] + [p1 - p0])
-                ys.append(meas - p0)
-    sol, *_ = np.linalg.lstsq(np.asarray(rows), np.asarray(ys), rcond=None)
-    t0 = dict(zip(names, (float(x) for x in sol[:-1])))
-    drain = float(max(0.0, sol[-1]))
-    out = {"kappa_ms_per_key": float(kappa), "g0": round(g0, 4), "drain_rounds": round(drain, 4),
-           "configs": []}
+            p0 = hcms.model_plan_time(sw["S"], 128, sz, hcms.MODE_AUTO, n, t_round, g0, t_copy, beta)
+            p1 = hcms.model_plan_time(sw["S"], 128, sz, hcms.MODE_AUTO, n, t_round, g0, t_copy, beta,
+                                      drain=1.0)
+            rows.append([1.0, p1 - p0])
+            ys.append(sw["auto_ms"][C - 1] - p0)
+        (a0, a1), *_ = np.linalg.lstsq(np.asarray(rows), np.asarray(ys), rcond=None)
+        if a1 < 0.0:   # no drain: T_0 alone
+            a1, a0 = 0.0, float(np.mean(ys))
+        t0[sw["workload"]], drains[sw["workload"]] = float(a0), float(a1)
+    out = {"kappa_ms_per_key": float(kappa), "g0": round(g0, 4), "configs": []}
     for sw in sweeps:
         S, H = sw["S"], sw["H"]
         t_round, t_copy, beta = par[sw["workload"]]
+        drain = drains[sw["workload"]]
         pred = [t0[sw["workload"]] +
                 hcms.model_plan_time(S, 128, hcms.default_chunks(H, C), hcms.MODE_AUTO, n, t_round,
                                      g0, t_copy, beta, drain=drain) for C in sw["chunk_counts"]]
@@ -324,7 +346,7 @@ def adaptive_chunks(ctx, sweeps):
         out["configs"].append({
             "workload": sw["workload"], "t_round_ms": round(t_round, 4),
             "t_copy_ms": round(t_copy, 5), "beta_ms": round(beta, 5),
-            "t0_ms": round(t0[sw["workload"]], 4),
+            "t0_ms": round(t0[sw["workload"]], 4), "drain_rounds": round(drain, 4),
             "predicted_auto_ms": [round(x, 4) for x in pred],
             "measured_auto_ms": meas,
             "prediction_error": [round((p_ - m_) / m_, 4) for p_, m_ in zip(pred, meas)],
@@ -394,14 +416,14 @@ def training_step(ctx, w, chunks, reps: int, dev):
     for _ in range(3):
         fwd(hcms.MODE_AUTO)
         bwd(hcms.MODE_AUTO)
-    times = {m: {"fwd": [], "bwd": []} for m in ("serial", "auto")}
+    timer = EventTimer()
     for r in range(reps + 1):
         for m in (("serial", "auto") if r % 2 == 0 else ("auto", "serial")):
-            tf = time_region(lambda: fwd(MODES[m]), 1)
-            tb = time_region(lambda: bwd(MODES[m]), 1)
-            if r > 0:
-                times[m]["fwd"] += tf
-                times[m]["bwd"] += tb
+            timer.time((m, "fwd", r), lambda: fwd(MODES[m]))
+            timer.time((m, "bwd", r), lambda: bwd(MODES[m]))
+    spans = timer.results()
+    times = {m: {p: [t for r in range(1, reps + 1) for t in spans[(m, p, r)]] for p in ("fwd", "bwd")}
+             for m in ("serial", "auto")}
     ctx.set_timing(reps)
     for _ in range(reps):
         bwd(hcms.MODE_SERIAL)
@@ -820,8 +842,7 @@ def main():
                 for _ in range(reps):
                     flush_mall(scratch)
                     cold += time_region(fn, 1)
-                for _ in range(reps):
-                    warm += time_region(fn, 1)
+                warm = time_region(fn, reps)
                 mc, mw = statistics.median(cold), statistics.median(warm)
                 entry[name] = {
                     "GBps_cold": round(nbytes / (mc * 1e-3) / 1e9, 1),
