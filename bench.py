@@ -413,6 +413,12 @@ def training_step(ctx, w, chunks, reps: int, dev):
         ctx.backward(dout, w.P, w.scale, chunks, fws, lse, mode=mode, dq=grads[0], dk=grads[1],
                      dv=grads[2])
 
+    # The score-gradient workspace: two regions (main and compute stream) of
+    # the largest chunk's heads.
+    per_head = hcms.backward_ds_bytes(w.S, w.d, q.dtype)
+    ds = (torch.empty(2 * max(chunks) * per_head, dtype=torch.uint8, device=dev)
+          if per_head else None)
+    ctx.set_ds_workspace(ds)
     for _ in range(3):
         fwd(hcms.MODE_AUTO)
         bwd(hcms.MODE_AUTO)
@@ -424,15 +430,23 @@ def training_step(ctx, w, chunks, reps: int, dev):
     spans = timer.results()
     times = {m: {p: [t for r in range(1, reps + 1) for t in spans[(m, p, r)]] for p in ("fwd", "bwd")}
              for m in ("serial", "auto")}
-    ctx.set_timing(reps)
-    for _ in range(reps):
-        bwd(hcms.MODE_SERIAL)
-    torch.cuda.synchronize()
-    attn_ms = ctx.kernel_ms(hcms.OP_ATTENTION)
-    ctx.set_timing(0)
-    C = len(chunks)
-    alg = [10.0 * w.S * w.S * chunks[i % C] * w.d for i in range(len(attn_ms))]
-    achieved = sum(alg) / (sum(attn_ms) * 1e-3) / 1e12
+    def launches():
+        ctx.set_timing(reps)
+        for _ in range(reps):
+            bwd(hcms.MODE_SERIAL)
+        torch.cuda.synchronize()
+        ms = ctx.kernel_ms(hcms.OP_ATTENTION)
+        ctx.set_timing(0)
+        C = len(chunks)
+        alg = [10.0 * w.S * w.S * chunks[i % C] * w.d for i in range(len(ms))]
+        return ms, sum(alg) / (sum(ms) * 1e-3) / 1e12
+
+    attn_ms, achieved = launches()
+    # The same launches without the workspace (the query-parallel dQ kernel).
+    ctx.set_ds_workspace(None)
+    bwd(hcms.MODE_SERIAL)
+    plain_ms, plain = launches()
+    del ds
     res = {"workload": w.name, "chunks": list(chunks)}
     for m in times:
         f = quartiles(times[m]["fwd"])
@@ -445,10 +459,18 @@ def training_step(ctx, w, chunks, reps: int, dev):
     res["backward_roofline"] = {
         "bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
         "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-        "kernels": "attention_dq_dma_kernel + attention_dkdv_dma_kernel (d = 128, bf16)",
-        "per_launch": f"10*S^2*H_c*d FLOP per chunk (executed: 14*S^2*H_c*d, Q K^T and dO V^T "
-                      f"are computed in both launches); avg {statistics.mean(attn_ms):.4f} ms over "
-                      f"{len(attn_ms)} chunk backward launches, serial schedule"}
+        "kernels": "attention_delta_kernel + attention_dkdv_dma_kernel<true> (dK, dV, and dS "
+                   "stored as bf16) + attention_dq_ds_kernel (dQ = scale dS K from the stored dS); "
+                   "d = 128, bf16, score-gradient workspace of 2 regions x "
+                   f"{max(chunks)} heads x {per_head / 2**30:.2f} GiB",
+        "per_launch": f"10*S^2*H_c*d FLOP per chunk, executed as such; avg "
+                      f"{statistics.mean(attn_ms):.4f} ms over {len(attn_ms)} chunk backward "
+                      f"passes, serial schedule",
+        "without_workspace": {
+            "achieved": round(plain, 2), "frac": round(plain / MFMA_BF16_PEAK_TFLOPS, 4),
+            "avg_ms": round(statistics.mean(plain_ms), 4),
+            "kernels": "attention_dq_dma_kernel (D, dQ; recomputes Q K^T and dO V^T) + "
+                       "attention_dkdv_dma_kernel<false>: 14*S^2*H_c*d FLOP executed"}}
     res["note"] = "step_TFLOPs counts 4 S^2 H d (forward) + 10 S^2 H d (backward)"
     del q, k, v, dout, fws, lse, out, grads
     return res

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define HCMS_ABI_VERSION 2
+#define HCMS_ABI_VERSION 3
 
 #if defined(__GNUC__)
 #define HCMS_API __attribute__((visibility("default")))
@@ -155,22 +155,42 @@ HCMS_API int hcms_attention_lse(const void *q, const void *k, const void *v, voi
  *   dV[h][j] = sum_i P_ij dO[h][i]
  *   dQ[h][i] = scale sum_j P_ij (<dO[h][i], V[h][j]> - D_i) K[h][j]
  *   dK[h][j] = scale sum_i P_ij (<dO[h][i], V[h][j]> - D_i) Q[h][i]
- * Per chunk, in order on `stream`: one query-parallel launch (D into delta,
- * then dq) and one key-parallel launch (dk, dv).  No atomics: deterministic,
- * and the result does not depend on the chunking.  Operands are rounded to
- * bf16 for the MFMAs (fp32 storage included), accumulation is fp32, dq, dk,
- * dv are rounded to the storage type.
+ * Per chunk, in order on `stream`, without a score-gradient workspace: one
+ * query-parallel launch (D into delta, then dq) and one key-parallel launch
+ * (dk, dv); the query-parallel one recomputes the scores and dP, so the two
+ * execute 14 S^2 d FLOP per head for the 10 S^2 d of the five products.
+ * With a workspace of at least hcms_backward_ds_bytes for one head (d = 128,
+ * bf16; ignored otherwise): D into delta, then per group of
+ * ds_bytes / (that size) heads the key-parallel launch, which also stores
+ * every dS_ij (rounded to bf16, as its dK product uses it) in the workspace,
+ * and dq as one product over the stored dS (10 S^2 d FLOP per head, plus
+ * 2 S^2 bytes written and read).  dk and dv are the same bits either way; dq
+ * differs from the other path's only in its fp32 summation order.  No
+ * atomics: deterministic, and the result does not depend on the chunking.
+ * Operands are rounded to bf16 for the MFMAs (fp32 storage included),
+ * accumulation is fp32, dq, dk, dv are rounded to the storage type.
  *   q, k, v, out : the forward's inputs and output, [H][S][d]
  *   dout         : dL/dO, [H][S][d]
  *   lse          : [H][S] fp32 from hcms_attention_lse on the same q, k, v, scale
  *   dq, dk, dv   : outputs, [H][S][d], disjoint from every input and each other
  *   delta        : [H][S] fp32 workspace (receives D)
- * Errors: as hcms_attention, plus NULL, ALIGN and ALIAS for the added buffers.
+ *   ds, ds_bytes : device workspace for the score gradients, 256-byte
+ *                  aligned, disjoint from every other buffer; NULL or too
+ *                  small for one head: the path without it
+ * Errors: as hcms_attention, plus NULL, ALIGN and ALIAS for the added buffers,
+ * ARG for ds_bytes < 0.
  */
 HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v, const void *out,
                                      const void *dout, const float *lse, void *dq, void *dk,
-                                     void *dv, float *delta, int S, int H, int d, float scale,
-                                     const int *chunk_sizes, int n_chunks, int dtype, void *stream);
+                                     void *dv, float *delta, void *ds, int64_t ds_bytes, int S,
+                                     int H, int d, float scale, const int *chunk_sizes,
+                                     int n_chunks, int dtype, void *stream);
+
+/* Bytes of score-gradient workspace that one head of hcms_attention_backward
+   (or of hcms_backward, per region) needs: ceil(S / 32) * 8 * ceil(S / 256) *
+   2 KiB, about 2 S^2 bytes; 0 where the path does not apply (d != 128 or fp32
+   storage).  Errors: NULL, SHAPE (S < 0), DTYPE. */
+HCMS_API int hcms_backward_ds_bytes(int S, int d, int dtype, int64_t *bytes_out);
 
 /*
  * hcms_attention_backward without the delta workspace, for callers that
@@ -180,8 +200,9 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
  * HCMS_NOALLOC_DELTA_MAX floats (16 MiB), allocated with the library's code
  * object and held until the process ends.  The call itself allocates nothing
  * (no hipMalloc, no hipFree); the caller passes every input and output.
- * Arguments, results and errors are those of hcms_attention_backward (dq, dk,
- * dv bit-identical to it), plus CAPACITY when S * H > HCMS_NOALLOC_DELTA_MAX.
+ * Arguments, results and errors are those of hcms_attention_backward without
+ * a score-gradient workspace (dq, dk, dv bit-identical to it), plus CAPACITY
+ * when S * H > HCMS_NOALLOC_DELTA_MAX.
  * The first call on a device looks up that device's copy of the array.
  * Calls on one device share its array: two calls whose launches can overlap
  * on one GPU (different streams without an ordering between them) race and
@@ -403,6 +424,17 @@ HCMS_API int hcms_ctx_create(int device, int max_chunks, hcms_ctx **out);
 HCMS_API int hcms_ctx_last_mode(const hcms_ctx *ctx);
 HCMS_API int hcms_ctx_num_cu(const hcms_ctx *ctx);
 
+/* Give hcms_backward a caller-owned score-gradient workspace (see
+   hcms_attention_backward): `bytes` bytes at `ws`, 256-byte aligned, used as
+   two regions of floor(bytes / 2) (rounded down to 256 bytes), one for the
+   backward launches on the main stream and one for those on the compute
+   stream, so that lanes mode can run two chunks at once.  A region smaller
+   than one head's hcms_backward_ds_bytes leaves the path without it, in every
+   mode.  ws NULL or bytes 0 removes it.  The memory must stay valid, and must
+   not be touched by the caller, while a backward that uses it is pending.
+   Errors: NULL (ctx), ARG (bytes < 0), ALIGN. */
+HCMS_API int hcms_ctx_set_ds_workspace(hcms_ctx *ctx, void *ws, int64_t bytes);
+
 /* Destroy a context (its events).  The caller must not destroy it while work
    that waits on its events is still pending.  NULL is accepted. */
 HCMS_API int hcms_ctx_destroy(hcms_ctx *ctx);
@@ -481,8 +513,10 @@ HCMS_API int hcms_forward_slots(hcms_ctx *ctx, const void *q_seq, const void *k_
  * mode) (PACK, ATTENTION and UNPACK ops):
  *   PACK c      dout_seq's heads of chunk c into do_hm ([P][S/P][H][d] ->
  *               [H_c][S][d], the gradient's all-to-all to head shards);
- *   ATTENTION c hcms_attention_backward of the chunk (D into delta, then dQ;
- *               then dK, dV into dq_hm, dk_hm, dv_hm);
+ *   ATTENTION c hcms_attention_backward of the chunk into dq_hm, dk_hm,
+ *               dv_hm (D into delta), with the context's score-gradient
+ *               region of the stream it runs on, if any
+ *               (hcms_ctx_set_ds_workspace);
  *   UNPACK c    dq_hm, dk_hm, dv_hm of chunk c into the head slots of
  *               dq_seq, dk_seq, dv_seq (the all-to-all back to sequence
  *               shards).

@@ -57,6 +57,7 @@ def load():
                            "`python -m paper_2607_01817_amd.build` (no CPU fallback exists)")
     lib = ctypes.CDLL(LIB_PATH)
     i, vp, f, d = ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_double
+    i64 = ctypes.c_int64
     ip = ctypes.POINTER(ctypes.c_int)
     dp = ctypes.POINTER(ctypes.c_double)
     sig = {
@@ -68,8 +69,10 @@ def load():
         "hcms_unpack": ([vp, vp, i, i, i, i, i, i, i, vp], i),
         "hcms_attention": ([vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
         "hcms_attention_lse": ([vp, vp, vp, vp, vp, i, i, i, f, ip, i, i, vp], i),
-        "hcms_attention_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, f, ip, i, i,
-                                     vp], i),
+        "hcms_attention_backward": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i, i, i, f,
+                                     ip, i, i, vp], i),
+        "hcms_backward_ds_bytes": ([i, i, i, ctypes.POINTER(i64)], i),
+        "hcms_ctx_set_ds_workspace": ([vp, vp, i64], i),
         "hcms_attention_backward_noalloc": ([vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, f, ip,
                                              i, i, vp], i),
         "hcms_plan": ([i, i, ctypes.POINTER(Op), i], i),
@@ -333,11 +336,29 @@ def attention_lse(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: floa
     return out, lse
 
 
+def backward_ds_bytes(S: int, d: int, dtype: torch.dtype = torch.bfloat16) -> int:
+    """Bytes of score-gradient workspace one head of the backward needs (0
+    where that path does not apply: d != 128 or float32 storage)."""
+    out = ctypes.c_int64()
+    _check(load().hcms_backward_ds_bytes(S, d, _DTYPES[dtype], ctypes.byref(out)))
+    return out.value
+
+
+def _ds_arg(ds):
+    if ds is None:
+        return None, 0
+    if not ds.is_cuda or not ds.is_contiguous():
+        raise ValueError("ds must be a contiguous device tensor")
+    return ds.data_ptr(), ds.numel() * ds.element_size()
+
+
 def attention_backward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
                        dout: torch.Tensor, lse: torch.Tensor, scale: float, chunk_sizes=None,
-                       dq=None, dk=None, dv=None, delta=None, stream=None):
+                       dq=None, dk=None, dv=None, delta=None, ds=None, stream=None):
     """``(dq, dk, dv)`` of head-major attention for output gradient ``dout``;
-    ``lse`` comes from :func:`attention_lse` on the same inputs."""
+    ``lse`` comes from :func:`attention_lse` on the same inputs.  ``ds``, a
+    device tensor of at least :func:`backward_ds_bytes` per head, turns on
+    the path that stores the score gradients and computes dq from them."""
     _same_hm((k, v, out, dout), ("k", "v", "out", "dout"), q)
     H, S, d = q.shape
     dq = torch.empty_like(q) if dq is None else dq
@@ -347,10 +368,11 @@ def attention_backward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: t
     lse = _stats(lse, "lse", H, S, q.device)
     delta = _stats(delta, "delta", H, S, q.device)
     sizes, n = _ints(chunk_sizes if chunk_sizes is not None else [H])
+    ds_ptr, ds_bytes = _ds_arg(ds)
     _check(load().hcms_attention_backward(
         q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), dout.data_ptr(), lse.data_ptr(),
-        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta.data_ptr(), S, H, d, float(scale),
-        sizes, n, _dtype(q), _stream(stream)))
+        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta.data_ptr(), ds_ptr, ds_bytes, S, H, d,
+        float(scale), sizes, n, _dtype(q), _stream(stream)))
     return dq, dk, dv
 
 
@@ -463,10 +485,20 @@ class Context:
         self._ws_key = None
         self._bws = None
         self._bws_key = None
+        self._ds = None
 
     @property
     def num_cu(self) -> int:
         return _check(load().hcms_ctx_num_cu(self._h))
+
+    def set_ds_workspace(self, ds):
+        """Give :meth:`backward` a score-gradient workspace (a contiguous
+        device tensor, used as two equal regions, one per stream; see
+        :func:`backward_ds_bytes`), or remove it (None).  The context keeps a
+        reference to the tensor."""
+        ptr, nbytes = _ds_arg(ds)
+        _check(load().hcms_ctx_set_ds_workspace(self._h, ptr, nbytes))
+        self._ds = ds
 
     @property
     def last_mode(self) -> int:

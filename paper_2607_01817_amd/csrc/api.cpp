@@ -447,6 +447,11 @@ struct hcms_ctx {
     // at a time).  No region: every tile whole, with the same results.
     void *split_mem = nullptr;
     hcms::SplitScratch split[2] = {};
+    // Caller-owned score-gradient workspace of hcms_backward: two regions of
+    // ds_region bytes, one for backward launches on the main stream, one for
+    // those on the compute stream (NULL: none).
+    char *ds = nullptr;
+    int64_t ds_region = 0;
 };
 
 namespace {
@@ -993,11 +998,29 @@ static int check_backward_args(const void *q, const void *k, const void *v, cons
     return HCMS_OK;
 }
 
+// A score-gradient workspace (NULL: none) must be 256-byte aligned and
+// disjoint from the `n` tensors of `bytes` bytes each and the two [H][S]
+// statistics.
+static int check_ds_workspace(const void *ds, int64_t ds_bytes, const void *const *tensors, int n,
+                              int64_t bytes, const float *lse, const float *delta, int S, int H) {
+    if (ds_bytes < 0) return fail(HCMS_ERR_ARG, "ds_bytes=%lld must be >= 0", static_cast<long long>(ds_bytes));
+    if (!ds || ds_bytes == 0 || S == 0) return HCMS_OK;
+    if (reinterpret_cast<uintptr_t>(ds) % 256 != 0)
+        return fail(HCMS_ERR_ALIGN, "the score-gradient workspace must be 256-byte aligned");
+    for (int i = 0; i < n; ++i)
+        if (overlaps(ds, ds_bytes, tensors[i], bytes))
+            return fail(HCMS_ERR_ALIAS, "the score-gradient workspace overlaps tensor %d", i);
+    const int64_t sb = int64_t{S} * H * 4;
+    if (overlaps(ds, ds_bytes, lse, sb) || (delta && overlaps(ds, ds_bytes, delta, sb)))
+        return fail(HCMS_ERR_ALIAS, "the score-gradient workspace overlaps lse or delta");
+    return HCMS_OK;
+}
+
 // The chunks' backward launches, in order on `stream`.
 static int run_backward(const void *q, const void *k, const void *v, const void *out,
                         const void *dout, const float *lse, void *dq, void *dk, void *dv,
-                        float *delta, int S, int d, float scale, const int *chunk_sizes,
-                        int n_chunks, int dtype, hipStream_t stream) {
+                        float *delta, void *ds, int64_t ds_bytes, int S, int d, float scale,
+                        const int *chunk_sizes, int n_chunks, int dtype, hipStream_t stream) {
     const int64_t head = static_cast<int64_t>(S) * d * elem_bytes(dtype);
     int h0 = 0;
     for (int i = 0; i < n_chunks; ++i) {
@@ -1007,7 +1030,7 @@ static int run_backward(const void *q, const void *k, const void *v, const void 
         auto atw = [off](void *p) { return static_cast<char *>(p) + off; };
         const hipError_t e = hcms::launch_attention_backward(
             at(q), at(k), at(v), at(out), at(dout), lse + soff, atw(dq), atw(dk), atw(dv),
-            delta + soff, S, chunk_sizes[i], d, scale, dtype, stream);
+            delta + soff, ds, ds_bytes, S, chunk_sizes[i], d, scale, dtype, stream);
         if (e != hipSuccess) return hip_fail(e, "attention backward launch");
         h0 += chunk_sizes[i];
     }
@@ -1016,14 +1039,28 @@ static int run_backward(const void *q, const void *k, const void *v, const void 
 
 int hcms_attention_backward(const void *q, const void *k, const void *v, const void *out,
                             const void *dout, const float *lse, void *dq, void *dk, void *dv,
-                            float *delta, int S, int H, int d, float scale,
-                            const int *chunk_sizes, int n_chunks, int dtype, void *stream) {
-    const int st = check_backward_args(q, k, v, out, dout, lse, dq, dk, dv, true, delta, S, H, d,
-                                       scale, chunk_sizes, n_chunks, dtype);
+                            float *delta, void *ds, int64_t ds_bytes, int S, int H, int d,
+                            float scale, const int *chunk_sizes, int n_chunks, int dtype,
+                            void *stream) {
+    int st = check_backward_args(q, k, v, out, dout, lse, dq, dk, dv, true, delta, S, H, d, scale,
+                                 chunk_sizes, n_chunks, dtype);
     if (st != HCMS_OK) return st;
+    const void *all[8] = {q, k, v, out, dout, dq, dk, dv};
+    const int64_t bytes = static_cast<int64_t>(S) * H * d * elem_bytes(dtype);
+    if ((st = check_ds_workspace(ds, ds_bytes, all, 8, bytes, lse, delta, S, H)) != HCMS_OK) return st;
     if (S == 0) return ok();
-    return run_backward(q, k, v, out, dout, lse, dq, dk, dv, delta, S, d, scale, chunk_sizes,
-                        n_chunks, dtype, static_cast<hipStream_t>(stream));
+    return run_backward(q, k, v, out, dout, lse, dq, dk, dv, delta, ds, ds_bytes, S, d, scale,
+                        chunk_sizes, n_chunks, dtype, static_cast<hipStream_t>(stream));
+}
+
+int hcms_backward_ds_bytes(int S, int d, int dtype, int64_t *bytes_out) {
+    if (!bytes_out) return fail(HCMS_ERR_NULL, "bytes_out is NULL");
+    *bytes_out = 0;
+    if (S < 0) return fail(HCMS_ERR_SHAPE, "S=%d must be >= 0", S);
+    int st;
+    if ((st = check_dtype(dtype)) != HCMS_OK) return st;
+    *bytes_out = hcms::attention_backward_ds_head_bytes(S, d, dtype);
+    return ok();
 }
 
 int hcms_attention_backward_noalloc(const void *q, const void *k, const void *v, const void *out,
@@ -1040,8 +1077,8 @@ int hcms_attention_backward_noalloc(const void *q, const void *k, const void *v,
     if (S == 0) return ok();
     float *delta = nullptr;
     if ((st = scratch_for_current_device(&delta)) != HCMS_OK) return st;
-    return run_backward(q, k, v, out, dout, lse, dq, dk, dv, delta, S, d, scale, chunk_sizes,
-                        n_chunks, dtype, static_cast<hipStream_t>(stream));
+    return run_backward(q, k, v, out, dout, lse, dq, dk, dv, delta, nullptr, 0, S, d, scale,
+                        chunk_sizes, n_chunks, dtype, static_cast<hipStream_t>(stream));
 }
 
 int hcms_plan(int n_chunks, int mode, hcms_op *ops, int cap) {
@@ -1084,6 +1121,16 @@ int hcms_ctx_last_mode(const hcms_ctx *ctx) {
     if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
     ok();
     return ctx->last_mode;
+}
+
+int hcms_ctx_set_ds_workspace(hcms_ctx *ctx, void *ws, int64_t bytes) {
+    if (!ctx) return fail(HCMS_ERR_NULL, "ctx is NULL");
+    if (bytes < 0) return fail(HCMS_ERR_ARG, "bytes=%lld must be >= 0", static_cast<long long>(bytes));
+    if (ws && reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return fail(HCMS_ERR_ALIGN, "the score-gradient workspace must be 256-byte aligned");
+    ctx->ds = ws && bytes > 0 ? static_cast<char *>(ws) : nullptr;
+    ctx->ds_region = ctx->ds ? bytes / 2 / 256 * 256 : 0;
+    return ok();
 }
 
 int hcms_ctx_num_cu(const hcms_ctx *ctx) {
@@ -1371,6 +1418,9 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
     }
     if (S > 0 && overlaps(lse, int64_t{S} * H * 4, delta, int64_t{S} * H * 4))
         return fail(HCMS_ERR_ALIAS, "lse and delta overlap");
+    if ((st = check_ds_workspace(ctx->ds, 2 * ctx->ds_region, all, 12, bytes, lse, delta, S, H)) !=
+        HCMS_OK)
+        return st;
     if (S == 0) return ok();
 
     const int64_t head_bytes = static_cast<int64_t>(S) * d * elem_bytes(dtype);
@@ -1386,10 +1436,15 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
         }
         if (kind == HCMS_OP_ATTENTION) {
             const int64_t so = static_cast<int64_t>(h0) * S;
+            // Launches on one stream are ordered, so each stream's region
+            // serves one chunk at a time.
+            char *ds = ctx->ds ? ctx->ds + (s == static_cast<hipStream_t>(main_stream) ? 0 : ctx->ds_region)
+                              : nullptr;
             return hcms::launch_attention_backward(at(q_hm, h0), at(k_hm, h0), at(v_hm, h0),
                                                    at(o_hm, h0), at(do_hm, h0), lse + so,
                                                    at(dq_hm, h0), at(dk_hm, h0), at(dv_hm, h0),
-                                                   delta + so, S, hc, d, scale, dtype, s);
+                                                   delta + so, ds, ctx->ds_region, S, hc, d,
+                                                   scale, dtype, s);
         }
         const void *src[3] = {at(dq_hm, h0), at(dk_hm, h0), at(dv_hm, h0)};
         void *dst[3] = {dq_seq, dk_seq, dv_seq};

@@ -50,6 +50,8 @@
 //
 // Tails: loads go through buffer resources bounded by the head's tensor (rows
 // >= S read as zeros); keys or queries past S get P = 0 and are not stored.
+#include <algorithm>
+
 #include "attention_tiles.h"
 #include "hcms_internal.h"
 
@@ -250,6 +252,8 @@ constexpr int kPerWave = kTileB / (64 * 16) / kWaves;  // DMA instructions per w
 static_assert(kPerWave == 2 && kDist + 1 <= kNB, "wait counts below assume this");
 
 __device__ inline unsigned swz(unsigned r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+constexpr int kDsTileB = kQW * kQB * 2;  // one stored 32 x 32 tile of dS (bf16)
 
 template <int P>
 struct Phase {
@@ -533,10 +537,12 @@ struct QStage {
 // 0 and 1 also load L and D (4 bytes per lane), so they count one more load
 // per block.  L and D enter the scores through one more MFMA each, and the two
 // waves of each SIMD take a step's work in different orders (both below).
+template <bool kDs>
 __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention_dkdv_dma_kernel(
     const __bf16 *__restrict__ q, const __bf16 *__restrict__ k, const __bf16 *__restrict__ v,
     const __bf16 *__restrict__ dout, const float *__restrict__ lse, const float *__restrict__ delta,
-    __bf16 *__restrict__ dk, __bf16 *__restrict__ dv, int S, int n_ktiles, float c, float scale) {
+    __bf16 *__restrict__ dk, __bf16 *__restrict__ dv, char *__restrict__ dsg, int S, int n_ktiles,
+    float c, float scale) {
     using namespace bdma;
     constexpr int D = kD, KK = D / 16, DT = D / 32, NT = 64 * kWaves, KEYS = kQW * kWaves;
     constexpr int QTB = kQB * kRowB;  // one block of 32 queries: 8 KiB
@@ -640,13 +646,30 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
     // pieces at k = 0..2, B holds ones there and zeros elsewhere, so the
     // product adds the exact fp32 value to all 32 keys' entries of that query
     // (its accumulator row), with no broadcast of per-row values.
-    const bf16x8 ones = g == 0 ? bf16x8{1, 1, 1, 0, 0, 0, 0, 0} : bf16x8{};
+    // A fourth term at k = 3 takes keys past S out: A holds -2^100 there and
+    // B holds 1 in the column of a key past S (0 for the others, whose sums
+    // gain an exact -0), so such a key's score and dP become about -2^100,
+    // its P exactly 0 and its dS exactly -0 for every query.  Their dK and dV
+    // are never stored; the stored dS (kDs) needs them finite and zero.
+    const __bf16 past = kj < S ? static_cast<__bf16>(0.f) : static_cast<__bf16>(1.f);
+    const bf16x8 ones = g == 0 ? bf16x8{1, 1, 1, past, 0, 0, 0, 0} : bf16x8{};
     const float inv_c = 1.0f / c;
     auto pieces = [](float x) {
         __bf16 h, m, l;
         split3(x, h, m, l);
-        return bf16x8{h, m, l, 0, 0, 0, 0, 0};
+        return bf16x8{h, m, l, static_cast<__bf16>(-0x1p100f), 0, 0, 0, 0};
     };
+    // Score gradients kept for the dQ product (kDs): the wave's 32 keys are
+    // key tile kw = 8 ktile + wave; the 32 x 32 tile of query block i sits at
+    // byte ((head nqb + i) nkw + kw) 2 KiB of dsg, lane (li, g)'s dsb[h] at
+    // h KiB + 32 li + 16 g in it (see attention_dq_ds_kernel).
+    const int nkw = 8 * n_ktiles;
+    char *const ds_wave =
+        kDs ? dsg + (static_cast<int64_t>(head) * ((S + kQB - 1) / kQB) * nkw + ktile * 8 + wave) *
+                        kDsTileB
+            : nullptr;
+    const int64_t ds_step = static_cast<int64_t>(nkw) * kDsTileB;
+    const unsigned ds_lane = li * 32 + g * 16;
 
     // s = Q K^T - L / c and dp = dO V^T - D of the block in buffer bi, rows =
     // queries; the statistic is added last, so dp - D rounds once, as a
@@ -690,6 +713,11 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
             }
             pb[h] = __builtin_convertvector(p, bf16x8);
             dsb[h] = __builtin_convertvector(ds, bf16x8);
+        }
+        if constexpr (kDs) {
+            char *dst = ds_wave + i * ds_step;
+            *reinterpret_cast<bf16x8 *>(dst + ds_lane) = dsb[0];
+            *reinterpret_cast<bf16x8 *>(dst + 1024 + ds_lane) = dsb[1];
         }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
@@ -763,6 +791,198 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
                 store4(vrow + dt * 32 + rb * 8 + g * 4, xv);
             }
     }
+}
+
+// ---------------------------------------------------------------------------
+// dQ from stored score gradients
+// ---------------------------------------------------------------------------
+// With a score-gradient workspace the key-parallel launch (kDs) also stores
+// every dS tile it computes, as rounded to bf16 for its own dK product, and
+// dQ becomes one product over that matrix, dQ^T = scale K^T dS^T: 2 S^2 d
+// FLOP per head in place of the query-parallel kernel's 6 S^2 d, which
+// recomputes the scores and dP.  The product reads the S x S bf16 dS once
+// (128 FLOP per byte), so HBM bandwidth bounds it.
+//
+// Stored layout, per head: the tile of query block i (32 queries) and key
+// tile kw (32 keys) at byte (i nkw + kw) 2 KiB, nkw = 8 ceil(S / 256).  A
+// tile is two 1 KiB halves h, each row-major [32 keys][16 query positions]
+// (32-byte rows); position 8 g + r of half h is query (rr / 4) 8 + 4 g +
+// rr % 4 of the block, rr = 8 h + r (the key-parallel kernel's accumulator
+// rows).  Keys past S hold exact zeros there.
+//
+// A workgroup has 8 waves; wave w owns query block 8 qtile + w and builds
+// its dQ^T (128 x 32) in four 32 x 32 accumulators.  A step takes 64 keys:
+// their K rows (16 KiB, shared, with the swizzle of attention_dq_dma_kernel)
+// and each wave's two dS tiles (4 KiB, its own) go straight into LDS, two
+// steps ahead through three buffers.  Both operands come out of LDS by
+// ds_read_b64_tr_b16 at the same key rows, so each product pairs equal keys:
+// A = K^T (head dimension = lane % 32), B = dS^T (query position = lane % 32).
+namespace dsq {
+constexpr int kWaves = 8;
+constexpr int kKB = 64;                                       // keys per step
+constexpr int kKTileB = kKB * bdma::kRowB;                    // 16 KiB of K rows
+constexpr int kDsWaveB = 2 * bdma::kDsTileB;                  // 4 KiB of dS per wave and step
+constexpr int kStageB = kKTileB + kWaves * kDsWaveB;          // 48 KiB
+constexpr int kNB = 3;                                        // LDS buffers
+constexpr int kKLoads = kKTileB / 1024 / kWaves;              // K loads per wave and step
+constexpr int kDLoads = kDsWaveB / 1024;                      // dS loads per wave and step
+static_assert(kKLoads == 2 && kDLoads == 4 && kNB * kStageB <= 160 * 1024, "layout assumed below");
+}  // namespace dsq
+
+__global__ __launch_bounds__(64 * dsq::kWaves, dsq::kWaves / 4) void attention_dq_ds_kernel(
+    const __bf16 *__restrict__ k, const char *__restrict__ dsg, __bf16 *__restrict__ dq, int S,
+    int n_qtiles, int nkw, float scale) {
+    using namespace dsq;
+    using bdma::kRowB;
+    using bdma::kDsTileB;
+    using bdma::swz;
+    constexpr int D = bdma::kD, DT = D / 32;
+    __shared__ __attribute__((aligned(1024))) char lds[kNB * kStageB];
+
+    const int logical = xcd_logical(blockIdx.x, gridDim.x);
+    const int head = logical / n_qtiles;
+    const int qtile = logical - head * n_qtiles;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 31;
+    const int nqb = (S + kQB - 1) / kQB;
+    const int qb = qtile * kWaves + wave;
+    const int qbc = min(qb, nqb - 1);  // a block past S reads the last one and stores nothing
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, static_cast<int64_t>(S) * D * 2);
+    const __amdgpu_buffer_rsrc_t dr =
+        head_rsrc(dsg + (static_cast<int64_t>(head) * nqb + qbc) * nkw * kDsTileB,
+                  static_cast<int64_t>(nkw) * kDsTileB);
+
+    // Lane offsets: K rows as in attention_dq_dma_kernel (row 4 (2 wave + i)
+    // + lane / 16, chunk at position lane % 16); dS tiles copied as stored;
+    // transposing reads of 16-key steps (lane t = lane % 16 of group
+    // G = lane / 16, rows 4 (G / 2) + t / 4 and 8 more).
+    unsigned src_k[kKLoads];
+#pragma unroll
+    for (int i = 0; i < kKLoads; ++i) {
+        const unsigned r = 4 * (kKLoads * wave + i) + (lane >> 4), p = lane & 15;
+        src_k[i] = r * kRowB + ((p ^ swz(r)) << 4);
+    }
+    unsigned tr_k[2][DT], tr_d[2];
+    {
+        const unsigned G = lane >> 4, t = lane & 15;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            const unsigned r = 4 * (G >> 1) + (t >> 2) + 8 * hh;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const unsigned col = dt * 32 + 16 * (G & 1) + 4 * (t & 3);
+                tr_k[hh][dt] = r * kRowB + (((col >> 3) ^ swz(r)) << 4) + ((col & 7) << 1);
+            }
+            tr_d[hh] = (G & 1) * 1024 + r * 32 + (t & 3) * 8;
+        }
+    }
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<uintptr_t>(lds));
+    auto issue = [&](int j, int buf) {
+        const unsigned st = lds0 + buf * kStageB;
+#pragma unroll
+        for (int i = 0; i < kKLoads; ++i)
+            load_lds(st + (kKLoads * wave + i) * 1024, kr, src_k[i], j * kKTileB);
+#pragma unroll
+        for (int i = 0; i < kDLoads; ++i)
+            load_lds(st + kKTileB + wave * kDsWaveB + i * 1024, dr, lane * 16 + i * 1024, j * kDsWaveB);
+    };
+
+    typedef __attribute__((address_space(3))) bf16x4 LdsV4;
+    f32x16 acc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x16{};
+    auto step = [&](int buf) {
+        const char *kb = lds + buf * kStageB;
+        const char *db = kb + kKTileB + wave * kDsWaveB;
+#pragma unroll
+        for (int ks = 0; ks < kKB / 16; ++ks) {
+            const char *d0 = db + (ks >> 1) * kDsTileB + (ks & 1) * 16 * 32;
+            const bf16x4 blo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(d0 + tr_d[0]));
+            const bf16x4 bhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(d0 + tr_d[1]));
+            const bf16x8 b = __builtin_shufflevector(blo, bhi, 0, 1, 2, 3, 4, 5, 6, 7);
+            const char *k0 = kb + ks * 16 * kRowB;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const bf16x4 alo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(k0 + tr_k[0][dt]));
+                const bf16x4 ahi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LdsV4 *)(k0 + tr_k[1][dt]));
+                const bf16x8 a = __builtin_shufflevector(alo, ahi, 0, 1, 2, 3, 4, 5, 6, 7);
+                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[dt], 0, 0, 0);
+            }
+        }
+    };
+
+    // Step j waits for block j (only block j + 1's loads may be pending),
+    // then, past the barrier that ends every wave's step j - 1, loads block
+    // j + 2 into that step's buffer.  Blocks past the last read zeros (K) or
+    // tiles of keys past S (dS), and are not used.
+    const int nblk = (S + kKB - 1) / kKB;
+    issue(0, 0);
+    issue(1, 1);
+    int buf = 0;
+    for (int j = 0; j < nblk; ++j) {
+        wait_vm<kKLoads + kDLoads>();
+        __syncthreads();
+        issue(j + 2, buf == 0 ? 2 : buf - 1);
+        step(buf);
+        buf = buf == kNB - 1 ? 0 : buf + 1;
+    }
+    wait_vm<0>();  // no load into LDS is pending when the workgroup ends
+
+    // Lane l holds query position n = l % 32 of its block and, per
+    // accumulator, head-dimension rows 8 rb + 4 g + 0..3.
+    if (qb < nqb) {
+        const int hh = li >> 4, r = li & 7, rr = 8 * hh + r;
+        const int qi = qb * kQB + (rr >> 2) * 8 + ((li >> 3) & 1) * 4 + (rr & 3);
+        const int g = lane >> 5;
+        if (qi < S) {
+            __bf16 *row = dq + hoff + static_cast<int64_t>(qi) * D;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const f32x4 x = {acc[dt][rb * 4 + 0] * scale, acc[dt][rb * 4 + 1] * scale,
+                                     acc[dt][rb * 4 + 2] * scale, acc[dt][rb * 4 + 3] * scale};
+                    store4(row + dt * 32 + rb * 8 + g * 4, x);
+                }
+        }
+    }
+}
+
+// D_i = <dO_i, O_i> for the path with stored score gradients (elsewhere the
+// query-parallel kernel's prologue computes it), with that prologue's
+// products in its order, so the key-parallel launch gets the same D either
+// way.  A wave covers 32 queries; lane (li, g) sums half of query li's row.
+__global__ __launch_bounds__(256) void attention_delta_kernel(const __bf16 *__restrict__ o,
+                                                              const __bf16 *__restrict__ dout,
+                                                              float *__restrict__ delta, int S,
+                                                              int nqb, int n_waves) {
+    constexpr int D = bdma::kD, KK = D / 16;
+    const int wv = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (wv >= n_waves) return;
+    const int head = wv / nqb, qb = wv - head * nqb;
+    const int lane = threadIdx.x & 63, li = lane & 31, g = lane >> 5;
+    const int qi = qb * kQB + li;
+    const int64_t hoff = static_cast<int64_t>(head) * S * D;
+    const int64_t hbytes = static_cast<int64_t>(S) * D * 2;
+    const __amdgpu_buffer_rsrc_t or_ = head_rsrc(o + hoff, hbytes);
+    const __amdgpu_buffer_rsrc_t dr = head_rsrc(dout + hoff, hbytes);
+    float dpart = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        const unsigned off = static_cast<unsigned>(qi * D + kk * 16 + g * 8) * 2;
+        const bf16x8 dv = __builtin_bit_cast(bf16x8, load8<__bf16>(dr, off));
+        const bf16x8 ov = __builtin_bit_cast(bf16x8, load8<__bf16>(or_, off));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bf16x2 a = {dv[2 * e], dv[2 * e + 1]};
+            const bf16x2 b = {ov[2 * e], ov[2 * e + 1]};
+            dpart = __builtin_amdgcn_fdot2_f32_bf16(a, b, dpart, false);
+        }
+    }
+    const float Di = swap_halves_sum(dpart);
+    if (g == 0 && qi < S) delta[static_cast<int64_t>(head) * S + qi] = Di;
 }
 
 template <int D, typename T>
@@ -902,16 +1122,67 @@ constexpr bool kDqDma = HCMS_BWD_DQ_DMA != 0;
 // d = 128 with bf16 storage runs attention_dkdv_dma_kernel.
 constexpr bool kDkdvDma = HCMS_BWD_DKDV_DMA != 0;
 
+// Bytes of stored score gradients per head (attention_dq_ds_kernel's
+// layout): ceil(S / 32) query blocks x 8 ceil(S / 256) key tiles x 2 KiB.
+int64_t ds_head_bytes(int S) {
+    const int64_t nqb = (static_cast<int64_t>(S) + kQB - 1) / kQB;
+    const int64_t nkw = 8 * ((static_cast<int64_t>(S) + KTile<bdma::kD>::keys - 1) / KTile<bdma::kD>::keys);
+    return nqb * nkw * bdma::kDsTileB;
+}
+
+// The path with stored score gradients, for `group` heads at a time: D for
+// every head, then per group the key-parallel launch (dK, dV, and dS into
+// ds) and the dQ product over ds.
+hipError_t launch_bwd_ds(const __bf16 *q, const __bf16 *k, const __bf16 *v, const __bf16 *o,
+                         const __bf16 *dout, const float *lse, __bf16 *dq, __bf16 *dk, __bf16 *dv,
+                         float *delta, char *ds, int S, int n_heads, int group, float c, float scale,
+                         hipStream_t stream) {
+    constexpr int D = bdma::kD;
+    const int nqb = (S + kQB - 1) / kQB;
+    const int64_t n_waves = static_cast<int64_t>(nqb) * n_heads;
+    if ((n_waves + 3) / 4 > 0x7fffffff) return hipErrorInvalidValue;
+    attention_delta_kernel<<<static_cast<unsigned>((n_waves + 3) / 4), 256, 0, stream>>>(
+        o, dout, delta, S, nqb, static_cast<int>(n_waves));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int n_tiles = (S + KTile<D>::keys - 1) / KTile<D>::keys;
+    const int n_qt = (S + kQW * dsq::kWaves - 1) / (kQW * dsq::kWaves);
+    for (int h0 = 0; h0 < n_heads; h0 += group) {
+        const int hg = min(group, n_heads - h0);
+        const int64_t off = static_cast<int64_t>(h0) * S * D, soff = static_cast<int64_t>(h0) * S;
+        attention_dkdv_dma_kernel<true><<<static_cast<unsigned>(static_cast<int64_t>(n_tiles) * hg),
+                                          KTile<D>::threads, 0, stream>>>(
+            q + off, k + off, v + off, dout + off, lse + soff, delta + soff, dk + off, dv + off, ds, S,
+            n_tiles, c, scale);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        attention_dq_ds_kernel<<<static_cast<unsigned>(static_cast<int64_t>(n_qt) * hg),
+                                 64 * dsq::kWaves, 0, stream>>>(k + off, ds, dq + off, S, n_qt,
+                                                                8 * n_tiles, scale);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <int D, typename T>
 hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const void *o,
                             const void *dout, const float *lse, void *dq, void *dk, void *dv,
-                            float *delta, int S, int n_heads, float c, float scale,
-                            hipStream_t stream) {
+                            float *delta, void *ds, int64_t ds_bytes, int S, int n_heads, float c,
+                            float scale, hipStream_t stream) {
     const int n_qt = (S + kQW * QTile<D>::waves - 1) / (kQW * QTile<D>::waves);
     const int64_t qblocks = static_cast<int64_t>(n_qt) * n_heads;
     const int n_tiles = (S + KTile<D>::keys - 1) / KTile<D>::keys;
     const int64_t blocks = static_cast<int64_t>(n_tiles) * n_heads;
     if (blocks > 0x7fffffff || qblocks > 0x7fffffff) return hipErrorInvalidValue;
+    if constexpr (D == bdma::kD && sizeof(T) == 2 && kDkdvDma) {
+        const int64_t group = ds ? std::min<int64_t>(n_heads, ds_bytes / ds_head_bytes(S)) : 0;
+        if (group >= 1)
+            return launch_bwd_ds(static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k),
+                                 static_cast<const __bf16 *>(v), static_cast<const __bf16 *>(o),
+                                 static_cast<const __bf16 *>(dout), lse, static_cast<__bf16 *>(dq),
+                                 static_cast<__bf16 *>(dk), static_cast<__bf16 *>(dv), delta,
+                                 static_cast<char *>(ds), S, n_heads, static_cast<int>(group), c,
+                                 scale, stream);
+    }
     if constexpr (D == bdma::kD && sizeof(T) == 2 && kDqDma) {
         static_assert(QTile<D>::waves == bdma::kWaves, "the DMA kernel covers 256 queries in 8 waves");
         attention_dq_dma_kernel<<<static_cast<unsigned>(qblocks), QTile<D>::threads, 0, stream>>>(
@@ -928,10 +1199,10 @@ hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const v
     if (e != hipSuccess) return e;
     if constexpr (D == bdma::kD && sizeof(T) == 2 && kDkdvDma) {
         static_assert(KTile<D>::waves == bdma::kWaves, "the DMA kernel covers 256 keys in 8 waves");
-        attention_dkdv_dma_kernel<<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
+        attention_dkdv_dma_kernel<false><<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
             static_cast<const __bf16 *>(q), static_cast<const __bf16 *>(k), static_cast<const __bf16 *>(v),
             static_cast<const __bf16 *>(dout), lse, delta, static_cast<__bf16 *>(dk),
-            static_cast<__bf16 *>(dv), S, n_tiles, c, scale);
+            static_cast<__bf16 *>(dv), nullptr, S, n_tiles, c, scale);
     } else {
         attention_dkdv_kernel<D, T><<<static_cast<unsigned>(blocks), KTile<D>::threads, 0, stream>>>(
             static_cast<const T *>(q), static_cast<const T *>(k), static_cast<const T *>(v),
@@ -943,24 +1214,30 @@ hipError_t launch_bwd_typed(const void *q, const void *k, const void *v, const v
 
 }  // namespace
 
+int64_t attention_backward_ds_head_bytes(int S, int d, int dtype) {
+    if (S <= 0 || d != bdma::kD || dtype != 0 || !kDkdvDma) return 0;
+    return ds_head_bytes(S);
+}
+
 hipError_t launch_attention_backward(const void *q, const void *k, const void *v, const void *o,
                                      const void *dout, const float *lse, void *dq, void *dk,
-                                     void *dv, float *delta, int S, int n_heads, int d,
-                                     float scale, int dtype, hipStream_t stream) {
+                                     void *dv, float *delta, void *ds, int64_t ds_bytes, int S,
+                                     int n_heads, int d, float scale, int dtype,
+                                     hipStream_t stream) {
     if (S == 0 || n_heads == 0) return hipSuccess;
     const float c = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
     if (d == 128 && dtype == 0)
-        return launch_bwd_typed<128, __bf16>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
-                                             scale, stream);
+        return launch_bwd_typed<128, __bf16>(q, k, v, o, dout, lse, dq, dk, dv, delta, ds, ds_bytes, S,
+                                             n_heads, c, scale, stream);
     if (d == 64 && dtype == 0)
-        return launch_bwd_typed<64, __bf16>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
-                                            scale, stream);
+        return launch_bwd_typed<64, __bf16>(q, k, v, o, dout, lse, dq, dk, dv, delta, ds, ds_bytes, S,
+                                            n_heads, c, scale, stream);
     if (d == 128 && dtype == 1)
-        return launch_bwd_typed<128, float>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
-                                            scale, stream);
+        return launch_bwd_typed<128, float>(q, k, v, o, dout, lse, dq, dk, dv, delta, ds, ds_bytes, S,
+                                            n_heads, c, scale, stream);
     if (d == 64 && dtype == 1)
-        return launch_bwd_typed<64, float>(q, k, v, o, dout, lse, dq, dk, dv, delta, S, n_heads, c,
-                                           scale, stream);
+        return launch_bwd_typed<64, float>(q, k, v, o, dout, lse, dq, dk, dv, delta, ds, ds_bytes, S,
+                                           n_heads, c, scale, stream);
     return hipErrorInvalidValue;
 }
 

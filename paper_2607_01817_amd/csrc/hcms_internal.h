@@ -93,13 +93,21 @@ hipError_t launch_attention_riding(const void *q, const void *k, const void *v, 
                                    const RidingCopy *copies, int n_copies, int64_t H, int n_cu,
                                    const SplitScratch *split, bool *riding, hipStream_t stream);
 // Backward of attention for `n_heads` consecutive heads (head-major buffers
-// starting at the chunk's first head; lse and delta [n_heads][S] fp32): one
-// query-parallel launch writing delta = <dO, O> and dq, then one key-parallel
-// launch writing dk and dv.
+// starting at the chunk's first head; lse and delta [n_heads][S] fp32).
+// Without a score-gradient workspace (ds NULL, or ds_bytes below one head's
+// attention_backward_ds_head_bytes): one query-parallel launch writing
+// delta = <dO, O> and dq, then one key-parallel launch writing dk and dv.
+// With one (d = 128, bf16): delta first, then per group of
+// ds_bytes / head-bytes heads the key-parallel launch (dk, dv, and dS into
+// ds) and the dQ product over the stored dS.
 hipError_t launch_attention_backward(const void *q, const void *k, const void *v, const void *o,
                                      const void *dout, const float *lse, void *dq, void *dk,
-                                     void *dv, float *delta, int S, int n_heads, int d,
-                                     float scale, int dtype, hipStream_t stream);
+                                     void *dv, float *delta, void *ds, int64_t ds_bytes, int S,
+                                     int n_heads, int d, float scale, int dtype,
+                                     hipStream_t stream);
+// Bytes of score-gradient workspace one head needs (0: the path does not
+// apply to this d and dtype).
+int64_t attention_backward_ds_head_bytes(int S, int d, int dtype);
 
 // Rotary position embedding on a latent grid of n_axes axes (row-major, the
 // last axis fastest): the d/2 pairs of a head vector form consecutive groups

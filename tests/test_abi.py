@@ -43,7 +43,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert hcms.abi_version() == 2
+    assert hcms.abi_version() == 3
     names = {OK: "HCMS_OK", ENULL: "HCMS_ERR_NULL", ESHAPE: "HCMS_ERR_SHAPE",
              ECHUNKS: "HCMS_ERR_CHUNKS", EDTYPE: "HCMS_ERR_DTYPE", EALIGN: "HCMS_ERR_ALIGN",
              EHIP: "HCMS_ERR_HIP", EARG: "HCMS_ERR_ARG", EALIAS: "HCMS_ERR_ALIAS",
@@ -470,9 +470,9 @@ def test_training_forward_and_backward_validation(lib):
     assert fwd(lse=A + 64) == EALIAS
     assert fwd(S=0, lse=None, q=None) == OK
 
-    def bwd(dout=E, dq=F, dk=G_, dv=H_, lse=L, delta=Dl, S=512, d=64):
-        return lib.hcms_attention_backward(A, B, C_, D_, dout, lse, dq, dk, dv, delta, S, 4, d,
-                                           0.125, sizes, 2, 1, None)
+    def bwd(dout=E, dq=F, dk=G_, dv=H_, lse=L, delta=Dl, S=512, d=64, ds=None, ds_bytes=0):
+        return lib.hcms_attention_backward(A, B, C_, D_, dout, lse, dq, dk, dv, delta, ds,
+                                           ds_bytes, S, 4, d, 0.125, sizes, 2, 1, None)
 
     assert bwd(dout=None) == ENULL
     assert bwd(dq=None) == ENULL
@@ -486,6 +486,34 @@ def test_training_forward_and_backward_validation(lib):
     assert bwd(delta=F + 16) == EALIAS  # workspace over a gradient
     assert bwd(d=96) == ESHAPE
     assert bwd(S=0, dout=None, dq=None, dk=None, dv=None, lse=None, delta=None) == OK
+    # The score-gradient workspace: size, alignment, overlaps.
+    W = 0xA0000000
+    assert bwd(ds=W, ds_bytes=-1) == EARG
+    assert bwd(ds=W + 16, ds_bytes=1 << 20) == EALIGN
+    assert bwd(ds=F - 256, ds_bytes=1 << 20) == EALIAS   # over a gradient
+    assert bwd(ds=A, ds_bytes=1 << 20) == EALIAS         # over an input
+    assert bwd(ds=L - 256, ds_bytes=1 << 20) == EALIAS   # over lse
+    assert bwd(ds=Dl, ds_bytes=1 << 20) == EALIAS        # over delta
+    assert bwd(S=0, dout=None, dq=None, dk=None, dv=None, lse=None, delta=None, ds=W + 16,
+               ds_bytes=1) == OK
+
+
+def test_backward_ds_bytes(lib):
+    """Workspace per head of the path that stores the score gradients:
+    ceil(S / 32) query blocks x 8 ceil(S / 256) key tiles x 2 KiB at d = 128
+    with bf16 storage, none elsewhere."""
+    out = ctypes.c_int64()
+    for S, want in ((56160, 1755 * 8 * 220 * 2048), (1, 1 * 8 * 2048), (0, 0),
+                    (257, 9 * 16 * 2048), (32760, 1024 * 8 * 128 * 2048)):
+        assert lib.hcms_backward_ds_bytes(S, 128, 0, ctypes.byref(out)) == OK
+        assert out.value == want, (S, out.value, want)
+    assert hcms.backward_ds_bytes(56160, 128) == 1755 * 1760 * 2048
+    for d, dt in ((64, 0), (128, 1), (64, 1)):
+        assert lib.hcms_backward_ds_bytes(4096, d, dt, ctypes.byref(out)) == OK and out.value == 0
+    assert lib.hcms_backward_ds_bytes(-1, 128, 0, ctypes.byref(out)) == ESHAPE
+    assert lib.hcms_backward_ds_bytes(64, 128, 7, ctypes.byref(out)) == EDTYPE
+    assert lib.hcms_backward_ds_bytes(64, 128, 0, None) == ENULL
+    assert lib.hcms_ctx_set_ds_workspace(None, None, 0) == ENULL
 
 
 def test_noalloc_backward_validation(lib):
