@@ -187,9 +187,9 @@ HCMS_API int hcms_attention_backward(const void *q, const void *k, const void *v
                                      int n_chunks, int dtype, void *stream);
 
 /* Bytes of score-gradient workspace that one head of hcms_attention_backward
-   (or of hcms_backward, per region) needs: ceil(S / 32) * 8 * ceil(S / 256) *
-   2 KiB, about 2 S^2 bytes; 0 where the path does not apply (d != 128 or fp32
-   storage).  Errors: NULL, SHAPE (S < 0), DTYPE. */
+   (or of hcms_backward, per region) needs: 8 ceil(S / 256)^2 * 16 KiB, about
+   2 S^2 bytes; 0 where the path does not apply (d != 128 or fp32 storage).
+   Errors: NULL, SHAPE (S < 0), DTYPE. */
 HCMS_API int hcms_backward_ds_bytes(int S, int d, int dtype, int64_t *bytes_out);
 
 /*

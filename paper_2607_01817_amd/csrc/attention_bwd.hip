@@ -254,6 +254,7 @@ static_assert(kPerWave == 2 && kDist + 1 <= kNB, "wait counts below assume this"
 __device__ inline unsigned swz(unsigned r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 
 constexpr int kDsTileB = kQW * kQB * 2;  // one stored 32 x 32 tile of dS (bf16)
+constexpr int kDsGroupB = 8 * kDsTileB;   // the tiles of 8 query blocks at one key tile
 
 template <int P>
 struct Phase {
@@ -661,14 +662,14 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
     };
     // Score gradients kept for the dQ product (kDs): the wave's 32 keys are
     // key tile kw = 8 ktile + wave; the 32 x 32 tile of query block i sits at
-    // byte ((head nqb + i) nkw + kw) 2 KiB of dsg, lane (li, g)'s dsb[h] at
+    // byte ((head nqt + i / 8) nkw + kw) 16 KiB + (i % 8) 2 KiB of dsg
+    // (nqt = n_ktiles tiles of 256 queries), lane (li, g)'s dsb[h] at
     // h KiB + 32 li + 16 g in it (see attention_dq_ds_kernel).
     const int nkw = 8 * n_ktiles;
     char *const ds_wave =
-        kDs ? dsg + (static_cast<int64_t>(head) * ((S + kQB - 1) / kQB) * nkw + ktile * 8 + wave) *
-                        kDsTileB
+        kDs ? dsg + (static_cast<int64_t>(head) * n_ktiles * nkw + ktile * 8 + wave) * kDsGroupB
             : nullptr;
-    const int64_t ds_step = static_cast<int64_t>(nkw) * kDsTileB;
+    const int64_t ds_step = static_cast<int64_t>(nkw) * kDsGroupB;   // per 8 query blocks
     const unsigned ds_lane = li * 32 + g * 16;
 
     // s = Q K^T - L / c and dp = dO V^T - D of the block in buffer bi, rows =
@@ -715,7 +716,7 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
             dsb[h] = __builtin_convertvector(ds, bf16x8);
         }
         if constexpr (kDs) {
-            char *dst = ds_wave + i * ds_step;
+            char *dst = ds_wave + (i >> 3) * ds_step + (i & 7) * kDsTileB;
             *reinterpret_cast<bf16x8 *>(dst + ds_lane) = dsb[0];
             *reinterpret_cast<bf16x8 *>(dst + 1024 + ds_lane) = dsb[1];
         }
@@ -804,11 +805,13 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
 // (128 FLOP per byte), so HBM bandwidth bounds it.
 //
 // Stored layout, per head: the tile of query block i (32 queries) and key
-// tile kw (32 keys) at byte (i nkw + kw) 2 KiB, nkw = 8 ceil(S / 256).  A
-// tile is two 1 KiB halves h, each row-major [32 keys][16 query positions]
-// (32-byte rows); position 8 g + r of half h is query (rr / 4) 8 + 4 g +
-// rr % 4 of the block, rr = 8 h + r (the key-parallel kernel's accumulator
-// rows).  Keys past S hold exact zeros there.
+// tile kw (32 keys) at byte ((i / 8) nkw + kw) 16 KiB + (i % 8) 2 KiB,
+// nkw = 8 ceil(S / 256), so the 8 query blocks of a workgroup below find the
+// tiles of one 64-key step in 32 contiguous KiB.  A tile is two 1 KiB halves
+// h, each row-major [32 keys][16 query positions] (32-byte rows); position
+// 8 g + r of half h is query (rr / 4) 8 + 4 g + rr % 4 of the block,
+// rr = 8 h + r (the key-parallel kernel's accumulator rows).  Keys past S
+// hold exact zeros there; query blocks past S are never written.
 //
 // A workgroup has 8 waves; wave w owns query block 8 qtile + w and builds
 // its dQ^T (128 x 32) in four 32 x 32 accumulators.  A step takes 64 keys:
@@ -846,16 +849,16 @@ __global__ __launch_bounds__(64 * dsq::kWaves, dsq::kWaves / 4) void attention_d
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 31;
     const int nqb = (S + kQB - 1) / kQB;
-    const int qb = qtile * kWaves + wave;
-    const int qbc = min(qb, nqb - 1);  // a block past S reads the last one and stores nothing
+    const int qb = qtile * kWaves + wave;  // a block past S reads unwritten tiles, stores nothing
     const int64_t hoff = static_cast<int64_t>(head) * S * D;
     const __amdgpu_buffer_rsrc_t kr = head_rsrc(k + hoff, static_cast<int64_t>(S) * D * 2);
     const __amdgpu_buffer_rsrc_t dr =
-        head_rsrc(dsg + (static_cast<int64_t>(head) * nqb + qbc) * nkw * kDsTileB,
-                  static_cast<int64_t>(nkw) * kDsTileB);
+        head_rsrc(dsg + (static_cast<int64_t>(head) * n_qtiles + qtile) * nkw * bdma::kDsGroupB,
+                  static_cast<int64_t>(nkw) * bdma::kDsGroupB);
 
     // Lane offsets: K rows as in attention_dq_dma_kernel (row 4 (2 wave + i)
-    // + lane / 16, chunk at position lane % 16); dS tiles copied as stored;
+    // + lane / 16, chunk at position lane % 16); the wave's two dS tiles of a
+    // step (key tiles 2 j and 2 j + 1 of its query block) copied as stored;
     // transposing reads of 16-key steps (lane t = lane % 16 of group
     // G = lane / 16, rows 4 (G / 2) + t / 4 and 8 more).
     unsigned src_k[kKLoads];
@@ -886,7 +889,9 @@ __global__ __launch_bounds__(64 * dsq::kWaves, dsq::kWaves / 4) void attention_d
             load_lds(st + (kKLoads * wave + i) * 1024, kr, src_k[i], j * kKTileB);
 #pragma unroll
         for (int i = 0; i < kDLoads; ++i)
-            load_lds(st + kKTileB + wave * kDsWaveB + i * 1024, dr, lane * 16 + i * 1024, j * kDsWaveB);
+            load_lds(st + kKTileB + wave * kDsWaveB + i * 1024, dr,
+                     (i >> 1) * bdma::kDsGroupB + wave * kDsTileB + (i & 1) * 1024 + lane * 16,
+                     j * 2 * bdma::kDsGroupB);
     };
 
     typedef __attribute__((address_space(3))) bf16x4 LdsV4;
@@ -1123,11 +1128,11 @@ constexpr bool kDqDma = HCMS_BWD_DQ_DMA != 0;
 constexpr bool kDkdvDma = HCMS_BWD_DKDV_DMA != 0;
 
 // Bytes of stored score gradients per head (attention_dq_ds_kernel's
-// layout): ceil(S / 32) query blocks x 8 ceil(S / 256) key tiles x 2 KiB.
+// layout): ceil(S / 256) groups of 8 query blocks x 8 ceil(S / 256) key
+// tiles x 16 KiB.
 int64_t ds_head_bytes(int S) {
-    const int64_t nqb = (static_cast<int64_t>(S) + kQB - 1) / kQB;
-    const int64_t nkw = 8 * ((static_cast<int64_t>(S) + KTile<bdma::kD>::keys - 1) / KTile<bdma::kD>::keys);
-    return nqb * nkw * bdma::kDsTileB;
+    const int64_t n = (static_cast<int64_t>(S) + KTile<bdma::kD>::keys - 1) / KTile<bdma::kD>::keys;
+    return n * 8 * n * bdma::kDsGroupB;
 }
 
 // The path with stored score gradients, for `group` heads at a time: D for

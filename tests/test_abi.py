@@ -500,14 +500,14 @@ def test_training_forward_and_backward_validation(lib):
 
 def test_backward_ds_bytes(lib):
     """Workspace per head of the path that stores the score gradients:
-    ceil(S / 32) query blocks x 8 ceil(S / 256) key tiles x 2 KiB at d = 128
-    with bf16 storage, none elsewhere."""
+    ceil(S / 256) groups of 8 query blocks x 8 ceil(S / 256) key tiles x
+    16 KiB at d = 128 with bf16 storage, none elsewhere."""
     out = ctypes.c_int64()
-    for S, want in ((56160, 1755 * 8 * 220 * 2048), (1, 1 * 8 * 2048), (0, 0),
-                    (257, 9 * 16 * 2048), (32760, 1024 * 8 * 128 * 2048)):
+    for S, want in ((56160, 220 * 1760 * 16384), (1, 8 * 16384), (0, 0),
+                    (257, 2 * 16 * 16384), (32760, 128 * 1024 * 16384)):
         assert lib.hcms_backward_ds_bytes(S, 128, 0, ctypes.byref(out)) == OK
         assert out.value == want, (S, out.value, want)
-    assert hcms.backward_ds_bytes(56160, 128) == 1755 * 1760 * 2048
+    assert hcms.backward_ds_bytes(56160, 128) == 220 * 1760 * 16384
     for d, dt in ((64, 0), (128, 1), (64, 1)):
         assert lib.hcms_backward_ds_bytes(4096, d, dt, ctypes.byref(out)) == OK and out.value == 0
     assert lib.hcms_backward_ds_bytes(-1, 128, 0, ctypes.byref(out)) == ESHAPE
