@@ -120,33 +120,45 @@ def test_backward_bitwise_chunk_invariance_and_determinism(hcms, name):
 
 
 def test_backward_wan_p8_sampled_and_gradient_sums(hcms, oracle_mod):
-    """The Wan-P8 shape (S = 56160, 5 heads, chunks 2 + 2 + 1): head 0 against
-    the oracle on 64 sampled queries (dQ) and 64 sampled keys (dK, dV); every
-    head against the identities sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i."""
+    """The Wan-P8 shape (S = 56160, 5 heads, chunks 2 + 2 + 1), on both paths
+    (without a score-gradient workspace, and with one of two heads as the bench
+    runs it): head 0 against the oracle on 64 sampled queries (dQ) and 64
+    sampled keys (dK, dV); every head against the identities sum_j dK_j = 0
+    and sum_j dV_j = sum_i dO_i; dK and dV the same bits on both paths."""
     w = inputs.WORKLOADS["wan_p8"]
     log("[backward wan_p8] GPU")
     qs, ks, vs = inputs.make_qkv(w)
     dos = inputs.make_dout(w)
     q, k, v, do = (x.permute(1, 0, 2).contiguous() for x in (qs, ks, vs, dos))
-    out, lse, dq, dk, dv = _run(hcms, q, k, v, do, w.scale, (2, 2, 1))
+    qd, kd, vd, dod = (x.cuda() for x in (q, k, v, do))
+    out, lse = hcms.attention_lse(qd, kd, vd, w.scale, (2, 2, 1))
+    plain = [t.cpu() for t in hcms.attention_backward(qd, kd, vd, out, dod, lse, w.scale, (2, 2, 1))]
+    ws = torch.empty(2 * hcms.backward_ds_bytes(w.S, w.d), dtype=torch.uint8, device="cuda")
+    stored = [t.cpu() for t in hcms.attention_backward(qd, kd, vd, out, dod, lse, w.scale,
+                                                       (2, 2, 1), ds=ws)]
+    del ws
+    torch.cuda.synchronize()
+    assert torch.equal(bits(stored[1]), bits(plain[1])) and torch.equal(bits(stored[2]), bits(plain[2]))
     rng = np.random.default_rng(w.seed + 3000)
     qr = np.sort(rng.choice(w.S, 64, replace=False))
     kr = np.sort(rng.choice(w.S, 64, replace=False))
     log("[backward wan_p8] oracle, head 0 (one pass over all queries)")
     Q, K, V, G = (x[0].double().numpy() for x in (q, k, v, do))
     rq, rk, rv = oracle_mod.attention_backward_head(Q, K, V, G, w.scale, qr, kr)
-    _check_grad(dq[0].double().cpu().numpy()[qr], rq, "dq head 0")
-    _check_grad(dk[0].double().cpu().numpy()[kr], rk, "dk head 0")
-    _check_grad(dv[0].double().cpu().numpy()[kr], rv, "dv head 0")
+    for dq, dk, dv in (plain, stored):
+        _check_grad(dq[0].double().numpy()[qr], rq, "dq head 0")
+        _check_grad(dk[0].double().numpy()[kr], rk, "dk head 0")
+        _check_grad(dv[0].double().numpy()[kr], rv, "dv head 0")
     lw = oracle_mod.lse_head(Q, K, w.scale, qr)
     assert np.all(np.abs(lse[0].double().cpu().numpy()[qr] - lw) <= LSE_TOL * np.abs(lw))
+    dq, dk, dv = plain
     for h in range(w.H):
         sk = dk[h].double().sum(dim=0)
         sv = dv[h].double().sum(dim=0)
         sg = do[h].double().sum(dim=0)
         # The sums cancel over 56160 rows; bound them by the rows' magnitudes.
         assert float(sk.abs().max()) <= GRAD_TOL * float(dk[h].double().abs().sum(dim=0).max())
-        assert float((sv.cpu() - sg).abs().max()) <= GRAD_TOL * float(sg.abs().max() + 1)
+        assert float((sv - sg).abs().max()) <= GRAD_TOL * float(sg.abs().max() + 1)
 
 
 # ---------------------------------------------------------------------------
