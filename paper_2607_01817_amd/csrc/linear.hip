@@ -21,7 +21,8 @@
 //     transpose: the MFMA computes Y^T tiles, D[n][m] = sum_k W[n][k] X[m][k],
 //     with W rows as the A operand and X rows as the B operand.  Each lane
 //     then holds one row m and, per 32 x 32 tile, 4 runs of 4 consecutive
-//     columns n: 8-byte stores of bf16, and whole rotation pairs;
+//     columns n: whole rotation pairs; bf16 output goes through LDS so that
+//     it leaves as 16-byte stores covering whole row segments;
 //   * k advances in blocks of 64: the 256 x 64 blocks of X and W are staged
 //     global -> registers -> LDS (rows padded to 144 bytes, so 16 lanes
 //     reading 16 rows hit 16 disjoint groups of 4 banks), double-buffered in
@@ -84,19 +85,44 @@ __device__ inline __amdgpu_buffer_rsrc_t span_rsrc(const void *base, int64_t byt
                                              static_cast<int>(static_cast<uint32_t>(n)), 0x00020000);
 }
 
+// load8 with the byte offset split into a per-lane part and a scalar part
+// (the buffer range check covers both).
+template <typename T>
+__device__ inline u32x4 load8s(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff);
+template <>
+__device__ inline u32x4 load8s<__bf16>(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+template <>
+__device__ inline u32x4 load8s<float>(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    const f32x4 a = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    const f32x4 b = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff + 16, soff, 0));
+    const f32x8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(u32x4, __builtin_convertvector(x, bf16x8));
+}
+
 // Global -> register staging of the 256 x 64 blocks of X and W at column k0.
-// Thread tid moves chunk tid % 8 (8 elements) of rows tid / 8 + kRowsPerPass p.
+// Thread tid moves chunk tid % 8 (8 elements) of rows tid / 8 + kRowsPerPass p:
+// a per-lane offset fixed for the whole launch (row and chunk, the same for X
+// and W) plus the block's column in the scalar offset, so the k-loop computes
+// no addresses (temporaries written there made the compiler wait for the
+// loads in flight on every step).
+template <typename T>
+__device__ inline void stage_offsets(unsigned (&voff)[kPass], unsigned row_bytes, int tid) {
+#pragma unroll
+    for (int p = 0; p < kPass; ++p)
+        voff[p] = static_cast<unsigned>(tid / 8 + kRowsPerPass * p) * row_bytes + (tid & 7) * 8 * sizeof(T);
+}
 template <typename T>
 struct Stager {
     u32x4 xr[kPass], wr[kPass];
-    __device__ void load(__amdgpu_buffer_rsrc_t xs, __amdgpu_buffer_rsrc_t ws, unsigned row_bytes,
-                         int k0, int tid) {
-        const unsigned col = (static_cast<unsigned>(k0) + (tid & 7) * 8) * sizeof(T);
+    __device__ void load(__amdgpu_buffer_rsrc_t xs, __amdgpu_buffer_rsrc_t ws,
+                         const unsigned (&voff)[kPass], int k0) {
+        const unsigned soff = static_cast<unsigned>(k0) * sizeof(T);
 #pragma unroll
         for (int p = 0; p < kPass; ++p) {
-            const unsigned off = static_cast<unsigned>(tid / 8 + kRowsPerPass * p) * row_bytes + col;
-            xr[p] = load8<T>(xs, off);
-            wr[p] = load8<T>(ws, off);
+            xr[p] = load8s<T>(xs, voff[p], soff);
+            wr[p] = load8s<T>(ws, voff[p], soff);
         }
     }
     __device__ void store(__bf16 *xt, __bf16 *wt, int tid) const {
@@ -176,24 +202,58 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
 #pragma unroll
         for (int mt = 0; mt < kMT; ++mt) acc[nt][mt] = f32x16{};
 
-    // ---- Y[m][n .. n + 3] of the tile at (m0, n0) from the D^T accumulators,
-    // rounded to T ----
-    auto store_tile = [&](int m0, int n0) {
+    // ---- Epilogue: Y of the tile at (m0, n0) from the D^T accumulators,
+    // rounded to T.  Lane (li, g) holds token m = ... + li and, per 32 x 32
+    // tile, runs of 4 consecutive features n = ... + 8 rb + 4 g.
+    // Per grid axis, the table entry of pair 0 of the axis at token m's
+    // coordinate (QKV epilogue with a rotation only).
+    auto table_rows = [&](int m, int (&tab_row)[kRopeMaxAxes]) {
+        int rest = m;
+        for (int a = qo.ax.n_axes - 1; a >= 0; --a) {
+            const int cc = rest % qo.ax.grid[a];
+            rest /= qo.ax.grid[a];
+            tab_row[a] = qo.ax.tab_off[a] + cc * qo.ax.pairs[a] - qo.ax.pair_start[a];
+        }
+    };
+    // Features n .. n + 3 (n < N) of a token whose table rows are tab_row,
+    // rotated in place when they are query or key features.
+    auto rotate = [&](f32x4 &v, int n, const int (&tab_row)[kRopeMaxAxes]) {
+        const int hd = qo.H * qo.d;
+        const int z = n / hd, e = (n - z * hd) % qo.d;  // e a multiple of 4: pairs e/2, e/2 + 1
+        if (z >= 2) return;
+#pragma unroll
+        for (int q2 = 0; q2 < 2; ++q2) {
+            const int p = e / 2 + q2;
+            int a = 0;
+            while (a + 1 < qo.ax.n_axes && p >= qo.ax.pair_start[a + 1]) ++a;
+            const f32x2 cs = *reinterpret_cast<const f32x2 *>(qo.table + 2 * (tab_row[a] + p));
+            const float x0 = v[2 * q2], x1 = v[2 * q2 + 1];
+            v[2 * q2] = __builtin_fmaf(x0, cs[0], -(x1 * cs[1]));
+            v[2 * q2 + 1] = __builtin_fmaf(x0, cs[1], x1 * cs[0]);
+        }
+    };
+    // Where feature n of token m goes: Y, or the split q, k, v (8 consecutive
+    // features never straddle two of them: N and H d are multiples of 8).
+    auto dest = [&](int m, int n) -> T * {
+        if constexpr (QKV) {
+            const int hd = qo.H * qo.d;
+            const int z = n / hd;
+            return qo.dst[z] + static_cast<int64_t>(m) * hd + (n - z * hd);
+        } else {
+            return y + static_cast<int64_t>(m) * N + n;
+        }
+    };
+    // Direct stores of each lane's runs: fp32 storage (16 bytes a run) and the
+    // QKV epilogue, whose K = D reductions make its one tile per workgroup
+    // long, so that its stores cost little (staging them, with the rotation,
+    // ran 5 % slower).
+    auto store_direct = [&](int m0, int n0) {
 #pragma unroll
         for (int mt = 0; mt < kMT; ++mt) {
             const int m = m0 + wm * kMT * 32 + mt * 32 + li;
             if (m >= M) continue;
-            // Per grid axis, the table entry of pair 0 of the axis at token m's
-            // coordinate (QKV epilogue with a rotation only).
             int tab_row[kRopeMaxAxes] = {};
-            if (QKV && qo.table != nullptr) {
-                int rest = m;
-                for (int a = qo.ax.n_axes - 1; a >= 0; --a) {
-                    const int cc = rest % qo.ax.grid[a];
-                    rest /= qo.ax.grid[a];
-                    tab_row[a] = qo.ax.tab_off[a] + cc * qo.ax.pairs[a] - qo.ax.pair_start[a];
-                }
-            }
+            if (QKV && qo.table != nullptr) table_rows(m, tab_row);
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
@@ -202,28 +262,47 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
                     if (n >= N) continue;
                     f32x4 v = {acc[nt][mt][rb * 4 + 0], acc[nt][mt][rb * 4 + 1],
                                acc[nt][mt][rb * 4 + 2], acc[nt][mt][rb * 4 + 3]};
-                    if constexpr (QKV) {
-                        const int hd = qo.H * qo.d;
-                        const int z = n / hd, r = n - z * hd;
-                        if (z < 2 && qo.table != nullptr) {
-                            const int e = r % qo.d;  // a multiple of 4: pairs e/2 and e/2 + 1
-#pragma unroll
-                            for (int q2 = 0; q2 < 2; ++q2) {
-                                const int p = e / 2 + q2;
-                                int a = 0;
-                                while (a + 1 < qo.ax.n_axes && p >= qo.ax.pair_start[a + 1]) ++a;
-                                const f32x2 cs =
-                                    *reinterpret_cast<const f32x2 *>(qo.table + 2 * (tab_row[a] + p));
-                                const float x0 = v[2 * q2], x1 = v[2 * q2 + 1];
-                                v[2 * q2] = __builtin_fmaf(x0, cs[0], -(x1 * cs[1]));
-                                v[2 * q2 + 1] = __builtin_fmaf(x0, cs[1], x1 * cs[0]);
-                            }
-                        }
-                        store4(qo.dst[z] + static_cast<int64_t>(m) * hd + r, v);
-                    } else {
-                        store4(y + static_cast<int64_t>(m) * N + n, v);
-                    }
+                    if (QKV && qo.table != nullptr) rotate(v, n, tab_row);
+                    store4(dest(m, n), v);
                 }
+        }
+    };
+    // Plain epilogue, bf16 storage: runs of 8 bytes, 32 rows apart, coalesce
+    // badly (the output projection, K = H d = 640, lost a fifth of its time
+    // to them), so each wave
+    // transposes its 64 x 128 part through LDS, 32 tokens at a time, in a
+    // private 32 x 264-byte region of the buffer the tile's last k-block left
+    // free, and stores whole 256-byte row segments, 16 bytes per lane.
+    constexpr int kStRow = 128 * 2 + 8;  // bytes per staged row, 8 of them padding
+    static_assert(4 * 32 * kStRow <= kTile * 2 && kNT * 32 == 128, "staging fits one buffer");
+    auto store_staged = [&](int m0, int n0, char *stage) {
+#pragma unroll
+        for (int mt = 0; mt < kMT; ++mt) {
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt)
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const int c = nt * 32 + rb * 8 + g * 4;
+                    const f32x4 v = {acc[nt][mt][rb * 4 + 0], acc[nt][mt][rb * 4 + 1],
+                                     acc[nt][mt][rb * 4 + 2], acc[nt][mt][rb * 4 + 3]};
+                    *reinterpret_cast<bf16x4 *>(stage + li * kStRow + c * 2) =
+                        __builtin_convertvector(v, bf16x4);
+                }
+            const int c = (lane & 15) * 8;  // the lane's 8 features of a staged row
+            const int n = n0 + wn * kNT * 32 + c;
+#pragma unroll
+            for (int q0 = 0; q0 < 8; q0 += 4) {
+                u32x4 o[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    o[q] = *reinterpret_cast<const u32x4 *>(stage + ((q0 + q) * 4 + (lane >> 4)) * kStRow + c * 2);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int mm = m0 + wm * kMT * 32 + mt * 32 + (q0 + q) * 4 + (lane >> 4);
+                    if (mm < M && n < N)
+                        *reinterpret_cast<u32x4 *>(y + static_cast<int64_t>(mm) * N + n) = o[q];
+                }
+            }
         }
     };
 
@@ -243,8 +322,10 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
     int lm0, ln0;
     origin(0, lm0, ln0);
     __amdgpu_buffer_rsrc_t lxs = x_rsrc(lm0), lws = w_rsrc(ln0);
+    unsigned voff[kPass];
+    stage_offsets<T>(voff, row_bytes, tid);
     auto load_next = [&](Stager<T> &st) {
-        st.load(lxs, lws, row_bytes, ld_kb * kBK, tid);
+        st.load(lxs, lws, voff, ld_kb * kBK);
         if (++ld_kb == nkb && ld_r + 1 < n_mine) {
             ld_kb = 0;
             ++ld_r;
@@ -305,7 +386,15 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
         }
         int m0, n0;
         origin(r, m0, n0);
-        store_tile(m0, n0);
+        if constexpr (sizeof(T) == 2 && !QKV) {
+            // The buffer of the tile's last block (stream block s - 1) is free
+            // until the next step stores block s + 1 there, after a barrier.
+            char *base = reinterpret_cast<char *>(wave < 4 ? xt[(s - 1) & 1] : wt[(s - 1) & 1]);
+            store_staged(m0, n0, base + (wave & 3) * 32 * kStRow);
+            __syncthreads();
+        } else {
+            store_direct(m0, n0);
+        }
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
