@@ -48,6 +48,13 @@
 // in the last bits.  Either way every query's and key's arithmetic depends on
 // S, d and the data only, never on the chunking.
 //
+// With a caller's score-gradient workspace (d = 128, bf16) dQ comes from the
+// stored dS instead: D = <dO, O> first (attention_delta_kernel), then the
+// key-parallel launch, which also stores every dS tile it computes, then
+// dQ^T = scale K^T dS^T over the stored tiles (attention_dq_ds_kernel): the
+// scores and dP are computed once, 10 S^2 d FLOP per head instead of 14, for
+// 2 S^2 bytes of dS written and read.
+//
 // Tails: loads go through buffer resources bounded by the head's tensor (rows
 // >= S read as zeros); keys or queries past S get P = 0 and are not stored.
 #include <algorithm>
