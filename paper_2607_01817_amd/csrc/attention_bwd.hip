@@ -830,13 +830,16 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
 namespace dsq {
 constexpr int kWaves = 8;
 constexpr int kKB = 64;                                       // keys per step
-constexpr int kKTileB = kKB * bdma::kRowB;                    // 16 KiB of K rows
-constexpr int kDsWaveB = 2 * bdma::kDsTileB;                  // 4 KiB of dS per wave and step
+constexpr int kTiles = kKB / 32;                              // key tiles per step
+constexpr int kKTileB = kKB * bdma::kRowB;                    // K rows of a step
+constexpr int kDsWaveB = kTiles * bdma::kDsTileB;             // dS of a step, per wave
 constexpr int kStageB = kKTileB + kWaves * kDsWaveB;          // 48 KiB
-constexpr int kNB = 3;                                        // LDS buffers
+constexpr int kNB = 3;                                        // LDS buffers (32-key steps
+                                                              // through 6 measured 1.5 % slower)
+constexpr int kDist = kNB - 1;                                // steps a block is loaded ahead
 constexpr int kKLoads = kKTileB / 1024 / kWaves;              // K loads per wave and step
 constexpr int kDLoads = kDsWaveB / 1024;                      // dS loads per wave and step
-static_assert(kKLoads == 2 && kDLoads == 4 && kNB * kStageB <= 160 * 1024, "layout assumed below");
+static_assert(kKLoads >= 1 && kNB * kStageB <= 160 * 1024, "layout assumed below");
 }  // namespace dsq
 
 __global__ __launch_bounds__(64 * dsq::kWaves, dsq::kWaves / 4) void attention_dq_ds_kernel(
@@ -898,7 +901,7 @@ __global__ __launch_bounds__(64 * dsq::kWaves, dsq::kWaves / 4) void attention_d
         for (int i = 0; i < kDLoads; ++i)
             load_lds(st + kKTileB + wave * kDsWaveB + i * 1024, dr,
                      (i >> 1) * bdma::kDsGroupB + wave * kDsTileB + (i & 1) * 1024 + lane * 16,
-                     j * 2 * bdma::kDsGroupB);
+                     j * kTiles * bdma::kDsGroupB);
     };
 
     typedef __attribute__((address_space(3))) bf16x4 LdsV4;
@@ -925,18 +928,18 @@ __global__ __launch_bounds__(64 * dsq::kWaves, dsq::kWaves / 4) void attention_d
         }
     };
 
-    // Step j waits for block j (only block j + 1's loads may be pending),
-    // then, past the barrier that ends every wave's step j - 1, loads block
-    // j + 2 into that step's buffer.  Blocks past the last read zeros (K) or
-    // tiles of keys past S (dS), and are not used.
+    // Step j waits for block j (only the loads of blocks j + 1 .. j + kDist - 1
+    // may be pending), then, past the barrier that ends every wave's step
+    // j - 1, loads block j + kDist into that step's buffer.  Blocks past the
+    // last read zeros (K) or tiles of keys past S (dS), and are not used.
     const int nblk = (S + kKB - 1) / kKB;
-    issue(0, 0);
-    issue(1, 1);
+#pragma unroll
+    for (int j = 0; j < kDist; ++j) issue(j, j);
     int buf = 0;
     for (int j = 0; j < nblk; ++j) {
-        wait_vm<kKLoads + kDLoads>();
+        wait_vm<(kDist - 1) * (kKLoads + kDLoads)>();
         __syncthreads();
-        issue(j + 2, buf == 0 ? 2 : buf - 1);
+        issue(j + kDist, buf == 0 ? kNB - 1 : buf - 1);
         step(buf);
         buf = buf == kNB - 1 ? 0 : buf + 1;
     }
