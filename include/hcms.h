@@ -225,7 +225,8 @@ HCMS_API int hcms_attention_backward_noalloc(const void *q, const void *k, const
 #define HCMS_MODE_PIPELINED 1  /* Alg. 1: copy stream + compute stream + events */
 #define HCMS_MODE_INLINE 2     /* one lane, four synchronisations (see hcms_plan) */
 #define HCMS_MODE_LANES 3      /* chunks alternate between two streams (see hcms_plan) */
-#define HCMS_MODE_AUTO 4       /* the mode hcms_auto_mode picks (fused, inline, lanes or serial);
+#define HCMS_MODE_AUTO 4       /* the mode hcms_auto_mode picks (fused, inline, lanes or serial;
+                                  hcms_backward with stored score gradients: lanes);
                                   hcms_forward, hcms_forward_slots and hcms_backward take it,
                                   hcms_plan does not (no fixed plan) */
 #define HCMS_MODE_SLOTS 5      /* Alg. 1's streams, copies interleaved so slots can be reused */
@@ -527,8 +528,11 @@ HCMS_API int hcms_forward_slots(hcms_ctx *ctx, const void *q_seq, const void *k_
  *   do_hm, dq_hm, dk_hm, dv_hm : device workspaces, [H][S][d] each
  *   delta            : device workspace, [H][S] fp32
  * Streams and modes as hcms_forward; in fused mode the copies run right after
- * each chunk's backward launches (these carry none).  Every mode and chunking
- * gives bit-identical gradients.  Errors: as hcms_forward and
+ * each chunk's backward launches (these carry none).  HCMS_MODE_AUTO runs lanes
+ * when the context's score-gradient workspace applies and there are two chunks
+ * or more (one chunk's HBM-bound dQ product then overlaps the next chunk's
+ * key-parallel launch), else what hcms_auto_mode picks.  Every mode and
+ * chunking gives bit-identical gradients.  Errors: as hcms_forward and
  * hcms_attention_backward.
  */
 HCMS_API int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_seq,

@@ -460,7 +460,8 @@ namespace {
 // HCMS_MODE_AUTO into *mode and returns the row size's log2 unit count.
 int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const int *chunk_sizes,
                    int n_chunks, int dtype, int *mode, int *log2u, void *main_stream,
-                   void *copy_stream, void *compute_stream, bool slotted = false) {
+                   void *copy_stream, void *compute_stream, bool slotted = false,
+                   bool prefer_lanes = false) {
     int st;
     const int m = *mode;
     if (!plan_mode(m) && m != HCMS_MODE_AUTO)
@@ -482,6 +483,10 @@ int check_schedule(hcms_ctx *ctx, int P, int S, int H, int d, float scale, const
         (copy_stream == compute_stream || copy_stream == main_stream || compute_stream == main_stream))
         return fail(HCMS_ERR_ARG, "pipelined and slots modes need three distinct streams");
     int r = m == HCMS_MODE_AUTO ? auto_mode(S, d, dtype, chunk_sizes, n_chunks, ctx->n_cu) : m;
+    // The backward with stored score gradients: one chunk's HBM-bound dQ
+    // product overlaps the next chunk's key-parallel launch in lanes.
+    if (m == HCMS_MODE_AUTO && prefer_lanes && n_chunks >= 2 && compute_stream != main_stream)
+        r = HCMS_MODE_LANES;
     // With two chunk slots the one-lane plan with few synchronisations is not
     // available; auto then runs the serial plan (lanes when it saves a round).
     if (slotted && m == HCMS_MODE_AUTO && r == HCMS_MODE_INLINE) r = HCMS_MODE_SERIAL;
@@ -1398,8 +1403,10 @@ int hcms_backward(hcms_ctx *ctx, const void *dout_seq, void *dq_seq, void *dk_se
         for (int i = 0; i < 12; ++i)
             if (!all[i]) return fail(HCMS_ERR_NULL, "a tensor pointer is NULL");
     int log2u = 0;
+    const int64_t ds_head = hcms::attention_backward_ds_head_bytes(S, d, dtype);
+    const bool ds_path = ctx->ds != nullptr && ds_head > 0 && ctx->ds_region >= ds_head;
     if ((st = check_schedule(ctx, P, S, H, d, scale, chunk_sizes, n_chunks, dtype, &mode, &log2u,
-                             main_stream, copy_stream, compute_stream)) != HCMS_OK)
+                             main_stream, copy_stream, compute_stream, false, ds_path)) != HCMS_OK)
         return st;
     for (int i = 0; i < 12; ++i)
         if (S > 0 && !aligned16(all[i])) return fail(HCMS_ERR_ALIGN, "buffers must be 16-byte aligned");

@@ -183,5 +183,8 @@ def test_ds_pipeline_bitwise_across_modes_and_chunkings(hcms, name):
             got = ctx.backward(dos, w.P, w.scale, sizes, ws, lse2, mode=mode)
             for a, b, nm in zip(got, ref, ("dq", "dk", "dv")):
                 assert torch.equal(bits(a), bits(b)), (name, sizes, mode, nm)
+            if mode == hcms.MODE_AUTO and len(sizes) >= 2:
+                # With the workspace, auto overlaps chunks in two lanes.
+                assert ctx.last_mode == hcms.MODE_LANES, (name, sizes, ctx.last_mode)
     ctx.set_ds_workspace(None)
     ctx.close()
