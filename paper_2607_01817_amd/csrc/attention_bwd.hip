@@ -723,9 +723,13 @@ __global__ __launch_bounds__(64 * bdma::kWaves, bdma::kWaves / 4) void attention
             dsb[h] = __builtin_convertvector(ds, bf16x8);
         }
         if constexpr (kDs) {
-            char *dst = ds_wave + (i >> 3) * ds_step + (i & 7) * kDsTileB;
-            *reinterpret_cast<bf16x8 *>(dst + ds_lane) = dsb[0];
-            *reinterpret_cast<bf16x8 *>(dst + 1024 + ds_lane) = dsb[1];
+            // Through a buffer resource over the 8 tiles of this key tile
+            // (scalar base and offset): no 64-bit lane addresses.
+            const __amdgpu_buffer_rsrc_t dr = head_rsrc(ds_wave + (i >> 3) * ds_step, kDsGroupB);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, dsb[0]), dr, ds_lane,
+                                                   (i & 7) * kDsTileB, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, dsb[1]), dr,
+                                                   ds_lane + 1024, (i & 7) * kDsTileB, 0);
         }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
