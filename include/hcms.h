@@ -368,8 +368,9 @@ HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n,
  * which lasts t_round (g0 + (1 - g0) f) (the clock rises when part of the
  * chip idles; g0 = 1: a partial round costs a full one).  When the attention
  * kernel splits that round's tiles by key segments (hcms_forward's d = 128
- * bf16 launches outside the lanes plan: 3 rem <= n three ways, else
- * 2 rem <= n two ways, with S of 12 key blocks or more) the round holds
+ * bf16 launches: 3 rem <= n three ways, else 2 rem <= n two ways, with S of
+ * 12 key blocks or more; in the lanes plan the last launch of each lane
+ * splits the rem = sum W mod n tiles past the pooled rounds) the round holds
  * ways rem workgroups and lasts a third (three ways) or two thirds (two ways)
  * as long.  Every launch on the critical path adds `drain` rounds (its last
  * workgroups finish at different times).  Inputs measured on the device:
@@ -381,7 +382,8 @@ HCMS_API int hcms_model_fit(const int *chunk_counts, const double *times, int n,
  *   the plan hcms_auto_mode picks) on chunk_sizes:
  *     attention: the sum of the launches' rounds plus C drains
  *       (HCMS_MODE_LANES: the chunks' workgroups pooled into one launch's
- *       rounds, unsplit, plus ceil(C / 2) drains), times t_round;
+ *       rounds, its partial round split as above, plus ceil(C / 2) drains),
+ *       times t_round;
  *     copies on the critical path, in head-tensors times t_copy (a pack moves
  *       3 per head, an unpack 1): all 4 H in serial mode; otherwise chunk 0's
  *       pack and the last chunk's unpack, plus in fused mode the copies a

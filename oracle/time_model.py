@@ -108,7 +108,8 @@ def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_rou
     """Model time of one plan of the chunk sizes ``sizes`` on one GPU with
     ``n_slots`` attention workgroups per round of ``queries_per_wg`` queries;
     ``split``: the attention kernel splits its launches' last rounds (the
-    lanes plan keeps every tile whole); ``drain``: rounds each attention
+    lanes plan splits the partial round of the pooled workgroups, in the
+    lanes' last launches); ``drain``: rounds each attention
     launch on the critical path adds while its last workgroups finish (C of
     them in one lane, ceil(C / 2) when two lanes alternate)."""
     sizes = list(sizes)
@@ -118,7 +119,8 @@ def plan_time(S: int, sizes, mode: int, n_slots: int, queries_per_wg: int, t_rou
     if C == 1:
         mode = SERIAL
     if mode == LANES:
-        attn = launch_rounds(sum(W), n_slots, g0) + drain * math.ceil(C / 2)
+        attn = launch_rounds(sum(W), n_slots, g0, tail_ways(sum(W), n_slots, S, split))
+        attn += drain * math.ceil(C / 2)
     else:
         attn = sum(launch_rounds(w, n_slots, g0, tail_ways(w, n_slots, S, split)) for w in W)
         attn += drain * C

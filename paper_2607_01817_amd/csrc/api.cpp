@@ -683,13 +683,27 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
         return static_cast<char *>(p) + head_bytes * first;
     };
     const auto beside = copy_lds_reserve(mode, f.n_chunks);
-    // The split scratch of the stream an attention launch runs on.  Lanes
-    // keep every tile whole: their two launches already share the rounds.
-    auto split_for = [&](hipStream_t s) -> const hcms::SplitScratch * {
-        if (mode == HCMS_MODE_LANES) return nullptr;
+    // The split scratch of the stream an attention launch runs on.  In the
+    // lanes plan the two lanes' launches share rounds, so none splits its own
+    // last round.  The last launch of each lane (chunks C - 2 and C - 1), whose
+    // tiles close the pooled rounds, splits its last rem tiles instead, rem
+    // the tiles past the last whole pooled round (the chunks' workgroups
+    // summed, mod n_cu): which lane's tiles end the pooled rounds depends on
+    // how the two queues' workgroups interleave, so both split.
+    const int64_t tiles = (static_cast<int64_t>(f.S) + hcms::attention_queries_per_block(f.d) - 1) /
+                          hcms::attention_queries_per_block(f.d);
+    int64_t pooled = 0;
+    for (int c = 0; c < f.n_chunks; ++c) pooled += tiles * f.chunk_sizes[c];
+    hcms::SplitScratch lanes_tail{};
+    auto split_for = [&](hipStream_t s, int c) -> const hcms::SplitScratch * {
         const int r = s == static_cast<hipStream_t>(f.main_stream) ? 0
                       : s == static_cast<hipStream_t>(f.compute_stream) ? 1 : -1;
-        return r >= 0 && f.ctx->split[r].part ? &f.ctx->split[r] : nullptr;
+        if (r < 0 || !f.ctx->split[r].part) return nullptr;
+        if (mode != HCMS_MODE_LANES) return &f.ctx->split[r];
+        if (c < f.n_chunks - 2) return nullptr;
+        lanes_tail = f.ctx->split[r];
+        lanes_tail.tail = pooled % f.ctx->n_cu;
+        return &lanes_tail;
     };
     auto launch = [&](int kind, int c, int h0, int hc, hipStream_t s) -> hipError_t {
         if (kind == HCMS_OP_PACK) {
@@ -701,7 +715,7 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
             return hcms::launch_attention(at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0),
                                           at(f.o_hm, c, h0),
                                           f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr,
-                                          f.S, hc, f.d, c_log2e, f.dtype, split_for(s), s);
+                                          f.S, hc, f.d, c_log2e, f.dtype, split_for(s, c), s);
         const void *src[1] = {at(f.o_hm, c, h0)};
         void *dst[1] = {f.o_seq};
         return hcms::launch_unpack(src, dst, 1, f.S, f.H, h0, hc, log2u, beside(kind, c), s);
@@ -734,7 +748,7 @@ int issue_forward(const ForwardArgs &f, int mode, int log2u) {
         return hcms::launch_attention_riding(
             at(f.q_hm, c, h0), at(f.k_hm, c, h0), at(f.v_hm, c, h0), at(f.o_hm, c, h0),
             f.lse ? f.lse + static_cast<int64_t>(h0) * f.S : nullptr, f.S, hc, f.d, c_log2e,
-            f.dtype, cp, n, f.H, f.ctx->n_cu, split_for(s), riding, s);
+            f.dtype, cp, n, f.H, f.ctx->n_cu, split_for(s, c), riding, s);
     };
     return execute_plan(f.ctx, mode, f.chunk_sizes, f.n_chunks, f.main_stream, f.copy_stream,
                         f.compute_stream, launch, ride);

@@ -1195,12 +1195,15 @@ struct Shape {
 // per CU): when its last round holds rem = W mod n_cu tiles and 3 rem (or
 // 2 rem) workgroups fit in one round, those tiles are split three (or two)
 // ways by key segments, so the last round lasts a third (two thirds) as
-// long.  Needs scratch (none: every tile whole, the same results).
+// long.  With sp->tail >= 0 the last min(tail, W) tiles are the ones split:
+// a launch whose last round is shared with another stream's launch splits
+// the tiles that close the pooled rounds.  Needs scratch (none: every tile
+// whole, the same results).
 TailSplit plan_split(int64_t W, int S, const SplitScratch *sp) {
     TailSplit t{nullptr, nullptr, nullptr, static_cast<int>(W), 0, 1};
     const int nkb = (S + kBC - 1) / kBC;
     if (!sp || !sp->part || sp->n_cu < 2 || dma::n_segments(nkb) != dma::kSeg) return t;
-    const int64_t n = sp->n_cu, rem = W % n;
+    const int64_t n = sp->n_cu, rem = sp->tail >= 0 ? std::min(sp->tail, W) : W % n;
     if (rem == 0) return t;
     const int ways = 3 * rem <= n ? 3 : 2 * rem <= n ? 2 : 0;
     if (ways == 0 || rem * ways > sp->slots || rem > sp->counters) return t;
@@ -1243,12 +1246,13 @@ int attention_blocks_per_cu(int d) { return d == 128 ? Shape<128>::PER_CU : Shap
 
 int64_t attention_split_slot_bytes() { return dma::kStashB + 256 * int64_t{sizeof(float4)}; }
 
-int attention_split_ways(int64_t W, int S, int d, int dtype, int n_cu) {
+int attention_split_ways(int64_t W, int S, int d, int dtype, int n_cu, int64_t tail) {
     if (!(kLdsDma && d == dma::kD && dtype == 0)) return 1;
     SplitScratch sp{};
     sp.part = sp.ml = reinterpret_cast<void *>(uintptr_t{256});   // placeholders: never dereferenced
     sp.n_cu = n_cu;
     sp.slots = sp.counters = n_cu;
+    sp.tail = tail;
     const TailSplit t = plan_split(W, S, &sp);
     return t.n_split > 0 ? t.ways : 1;
 }

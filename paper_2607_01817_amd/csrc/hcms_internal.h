@@ -58,11 +58,16 @@ struct SplitScratch {
     int *count;
     int slots, counters;
     int n_cu;
+    // Tiles at the end of the launch to split: -1 for the launch's own last
+    // round (W mod n_cu); otherwise this many (at most W), for a launch whose
+    // last tiles close a round that other launches' workgroups share.
+    int64_t tail = -1;
 };
 int64_t attention_split_slot_bytes();
 // Workgroups per split tile (2 or 3) a d = 128 bf16 launch of W tiles splits
-// its last round's tiles into on n_cu CUs, or 1 when it splits none.
-int attention_split_ways(int64_t W, int S, int d, int dtype, int n_cu);
+// its last `tail` tiles into on n_cu CUs (tail -1: W mod n_cu), or 1 when it
+// splits none.
+int attention_split_ways(int64_t W, int S, int d, int dtype, int n_cu, int64_t tail = -1);
 
 // lse, if not NULL, receives [n_heads][S] fp32 log2 softmax denominators:
 // P_ij = exp2(scale_log2e * <q_i, k_j> - lse_i).  split: NULL, or scratch

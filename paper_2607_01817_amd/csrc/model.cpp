@@ -99,8 +99,10 @@ double plan_time(int S, int d, int dtype, const int *sizes, int C, int mode, int
     }
     if (C == 1) mode = HCMS_MODE_SERIAL;
     double attn = 0.0;
-    if (mode == HCMS_MODE_LANES) {   // the two lanes' launches keep their tiles whole
-        attn = launch_rounds(total, n, g0, 1) + drain * ((C + 1) / 2);
+    if (mode == HCMS_MODE_LANES) {   // the chunks' workgroups pooled; the remainder past the
+                                     // last whole pooled round split by the lanes' last launches
+        attn = launch_rounds(total, n, g0, hcms::attention_split_ways(total, S, d, dtype, n_cu)) +
+               drain * ((C + 1) / 2);
     } else {
         attn = drain * C;
         for (int c = 0; c < C; ++c) {

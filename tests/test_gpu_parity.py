@@ -333,12 +333,14 @@ def test_auto_mode_runs_the_predicted_plan(hcms, name, sizes):
 def test_forward_is_deterministic(hcms, name, sizes):
     """Repeated forwards give the same bits.  Wan-P8 {5} splits its last round
     of 76 tiles three ways and Small {8} its 128 tiles two ways, so each call
-    also checks that the split tiles' arrival counters are back at zero."""
+    also checks that the split tiles' arrival counters are back at zero.  The
+    lanes plan splits the 76 tiles past the pooled rounds of Wan-P8 {2,2,1}
+    in its last chunk's launch."""
     w = inputs.WORKLOADS[name]
     q, k, v = (x.cuda() for x in workload_inputs(name))
     ref = hcms.attention(_cuda_hm(q), _cuda_hm(k), _cuda_hm(v), w.scale).permute(1, 0, 2)
     ctx = hcms.Context()
-    for mode in (hcms.MODE_SERIAL, hcms.MODE_FUSED):
+    for mode in (hcms.MODE_SERIAL, hcms.MODE_FUSED, hcms.MODE_LANES):
         for _ in range(3):
             got = ctx.forward(q, k, v, w.P, w.scale, sizes, mode=mode)
             assert torch.equal(bits(got), bits(ref)), (name, sizes, mode)

@@ -226,6 +226,13 @@ def test_worked_split_tails():
     assert tm.tail_ways(440, 256, 56160, True) == 1 and tm.tail_ways(220, 256, 56160, True) == 1
     assert tm.tail_ways(1100, 256, 56160, False) == 1
     assert tm.tail_ways(1100, 256, 64 * 11, True) == 1
+    # Lanes pool 2 + 2 + 1 into the one-chunk launch's 1100 workgroups; the
+    # lanes' last launches split the 76 tiles past the 4 pooled rounds, so
+    # the attention takes what the one-chunk launch takes (two drains).
+    assert tm.plan_time(56160, (2, 2, 1), tm.LANES, 256, 256, 1.0, g0, 0.0, 0.0, True) == \
+        pytest.approx(4 + (g0 + (1 - g0) * 228 / 256) / 3)
+    assert tm.plan_time(56160, (2, 2, 1), tm.LANES, 256, 256, 1.0, g0, 0.0, 0.0, False) == \
+        pytest.approx(4 + g0 + (1 - g0) * 76 / 256)
 
 
 def _plan_of(S, d, dtype=0, n_cu=256):

@@ -29,8 +29,10 @@ MUTANTS = {
                                        "return full + length"),
     "partial round costs only its busy share": ("return full + length * (g0 + (1.0 - g0) * f)",
                                                 "return full + length * f"),
-    "lanes do not pool the rounds": ("attn = launch_rounds(sum(W), n_slots, g0)",
+    "lanes do not pool the rounds": ("attn = launch_rounds(sum(W), n_slots, g0, tail_ways(sum(W), n_slots, S, split))",
                                      "attn = sum(launch_rounds(w, n_slots, g0) for w in W)"),
+    "lanes keep the pooled tail whole": ("attn = launch_rounds(sum(W), n_slots, g0, tail_ways(sum(W), n_slots, S, split))",
+                                         "attn = launch_rounds(sum(W), n_slots, g0)"),
     "serial plan moves only the unpacks": ("copies = 4 * H ", "copies = H "),
     "one synchronisation per chunk": ("PIPELINED: 2 * C + 3", "PIPELINED: C + 3"),
     "fused launches always carry": ("if idle >= max(1, n_slots // 8):", "if True:"),
