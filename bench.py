@@ -56,6 +56,73 @@ def flush_mall(buf: torch.Tensor):
     buf.amax()
 
 
+class GpuSensors:
+    """The GPU's clock, power and hotspot temperature through amdsmi's metrics
+    table (read only; reported beside the timings, never used in them).
+    sample() reads once; during(fn) samples every `period` seconds from a
+    host thread while fn runs.  Every reading is None when amdsmi is missing
+    or the device cannot be matched by its PCI address."""
+
+    def __init__(self, dev_index: int = 0):
+        self.handle = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            p = torch.cuda.get_device_properties(dev_index)
+            want = (p.pci_domain_id, p.pci_bus_id, p.pci_device_id)
+            for h in amdsmi.amdsmi_get_processor_handles():
+                dom, bus, rest = amdsmi.amdsmi_get_gpu_device_bdf(h).split(":")
+                if (int(dom, 16), int(bus, 16), int(rest.split(".")[0], 16)) == want:
+                    self.handle = h
+                    break
+            self.amdsmi = amdsmi
+        except Exception:                      # no amdsmi, no permission: nothing reported
+            self.handle = None
+
+    def sample(self):
+        if self.handle is None:
+            return None
+        try:
+            m = self.amdsmi.amdsmi_get_gpu_metrics_info(self.handle)
+            clks = [c for c in m.get("current_gfxclks", []) if isinstance(c, int) and 0 < c < 10000]
+            if not clks and isinstance(m.get("current_gfxclk"), int):
+                clks = [m["current_gfxclk"]]
+            pw, tc = m.get("current_socket_power"), m.get("temperature_hotspot")
+            return {"gfx_mhz": round(sum(clks) / len(clks), 1) if clks else None,
+                    "power_w": pw if isinstance(pw, int) else None,
+                    "hotspot_c": tc if isinstance(tc, int) else None}
+        except Exception:
+            return None
+
+    def during(self, fn, period: float = 0.02):
+        """Runs fn() and returns the readings taken while it ran, summarised."""
+        import threading
+        got, stop = [], threading.Event()
+
+        def poll():
+            while not stop.is_set():
+                r = self.sample()
+                if r is not None:
+                    got.append(r)
+                stop.wait(period)
+
+        th = threading.Thread(target=poll, daemon=True)
+        th.start()
+        try:
+            fn()
+        finally:
+            stop.set()
+            th.join()
+        clk = [r["gfx_mhz"] for r in got if r["gfx_mhz"] is not None]
+        pw = [r["power_w"] for r in got if r["power_w"] is not None]
+        if not clk:
+            return None
+        return {"gfx_mhz_mean": round(statistics.mean(clk), 1), "gfx_mhz_min": min(clk),
+                "gfx_mhz_max": max(clk),
+                "power_w_mean": round(statistics.mean(pw), 1) if pw else None, "samples": len(got),
+                "distinct": len({(r["gfx_mhz"], r["power_w"]) for r in got})}
+
+
 class EventTimer:
     """Events around calls enqueued back to back on one stream, read after a
     single synchronisation at the end.  The host stays ahead of the GPU, so a
@@ -718,9 +785,16 @@ def main():
     def step(m=mode, chunks=sizes):
         ctx.forward(qd, kd, vd, w.P, w.scale, chunks, mode=m, out=out, workspaces=ws)
 
-    for _ in range(args.warmup):
-        step()
     torch.cuda.synchronize()
+    sensors = GpuSensors(0)
+    clock = {"before_warmup": sensors.sample()}
+
+    def warm():
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+
+    clock["warmup"] = sensors.during(warm)
     plan = MODE_NAMES[ctx.last_mode]
 
     # ---- timed region: K steps, nothing but the steps between the events ----
@@ -728,11 +802,21 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t0.record(main_stream)
-    for _ in range(args.steps):
-        step()
-    t1.record(main_stream)
-    torch.cuda.synchronize()
+
+    def timed():
+        t0.record(main_stream)
+        for _ in range(args.steps):
+            step()
+        t1.record(main_stream)
+        torch.cuda.synchronize()
+
+    clock["timed_steps"] = sensors.during(timed)
+    clock["after"] = sensors.sample()
+    clock["source"] = ("amdsmi metrics table: current_gfxclks averaged over the XCDs, "
+                       "current_socket_power, temperature_hotspot; read before the warm-up and "
+                       "after the timed steps, and every 20 ms by a host thread during the "
+                       "warm-up and during the timed steps (the table refreshes more slowly "
+                       "than that: 'distinct' counts the different readings)")
     ms_per_step = t0.elapsed_time(t1) / args.steps
 
     # ---- the same K steps again with every kernel bracketed by events on
@@ -827,6 +911,7 @@ def main():
                         f"{args.steps} steps ({ms_per_step_events:.4f} ms per step with the "
                         f"events), {len(attn_ms)} launches"},
         },
+        "gpu_clock": clock,
     }
     if tuple(sizes) != (w.H,):
         result["roofline"]["one_chunk"] = one_chunk_roofline(ctx, w, qd, kd, vd, out, ws,
