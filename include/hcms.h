@@ -279,6 +279,10 @@ typedef struct hcms_op {
  * and the main stream waits E_done after its own last chunk.  Besides the
  * copies, the attention launches of the two lanes overlap, so that the
  * workgroups of one fill the CUs the last round of the other leaves idle.
+ * No launch splits its own last round; instead the last launch of each lane
+ * (d = 128 bf16) splits its last rem tiles by key segments, rem the
+ * workgroups of all chunks summed, mod n_cu: the tiles past the last whole
+ * pooled round (same results either way).
  * The copy stream is not used.
  * Slots mode uses Alg. 1's streams and events but interleaves the copy stream
  * with the attentions: the copy stream packs chunks 0 and 1, then, for every
