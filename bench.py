@@ -59,9 +59,8 @@ def flush_mall(buf: torch.Tensor):
 class GpuSensors:
     """The GPU's clock, power and hotspot temperature through amdsmi's metrics
     table (read only; reported beside the timings, never used in them).
-    sample() reads once; during(fn) samples every `period` seconds from a
-    host thread while fn runs.  Every reading is None when amdsmi is missing
-    or the device cannot be matched by its PCI address."""
+    Every reading is None when amdsmi is missing or the device cannot be
+    matched by its PCI address."""
 
     def __init__(self, dev_index: int = 0):
         self.handle = None
@@ -93,34 +92,6 @@ class GpuSensors:
                     "hotspot_c": tc if isinstance(tc, int) else None}
         except Exception:
             return None
-
-    def during(self, fn, period: float = 0.02):
-        """Runs fn() and returns the readings taken while it ran, summarised."""
-        import threading
-        got, stop = [], threading.Event()
-
-        def poll():
-            while not stop.is_set():
-                r = self.sample()
-                if r is not None:
-                    got.append(r)
-                stop.wait(period)
-
-        th = threading.Thread(target=poll, daemon=True)
-        th.start()
-        try:
-            fn()
-        finally:
-            stop.set()
-            th.join()
-        clk = [r["gfx_mhz"] for r in got if r["gfx_mhz"] is not None]
-        pw = [r["power_w"] for r in got if r["power_w"] is not None]
-        if not clk:
-            return None
-        return {"gfx_mhz_mean": round(statistics.mean(clk), 1), "gfx_mhz_min": min(clk),
-                "gfx_mhz_max": max(clk),
-                "power_w_mean": round(statistics.mean(pw), 1) if pw else None, "samples": len(got),
-                "distinct": len({(r["gfx_mhz"], r["power_w"]) for r in got})}
 
 
 class EventTimer:
@@ -787,14 +758,10 @@ def main():
 
     torch.cuda.synchronize()
     sensors = GpuSensors(0)
-    clock = {"before_warmup": sensors.sample()}
-
-    def warm():
-        for _ in range(args.warmup):
-            step()
-        torch.cuda.synchronize()
-
-    clock["warmup"] = sensors.during(warm)
+    clock = {"idle_before_warmup": sensors.sample()}
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
     plan = MODE_NAMES[ctx.last_mode]
 
     # ---- timed region: K steps, nothing but the steps between the events ----
@@ -802,21 +769,18 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-
-    def timed():
-        t0.record(main_stream)
-        for _ in range(args.steps):
-            step()
-        t1.record(main_stream)
-        torch.cuda.synchronize()
-
-    clock["timed_steps"] = sensors.during(timed)
-    clock["after"] = sensors.sample()
-    clock["source"] = ("amdsmi metrics table: current_gfxclks averaged over the XCDs, "
-                       "current_socket_power, temperature_hotspot; read before the warm-up and "
-                       "after the timed steps, and every 20 ms by a host thread during the "
-                       "warm-up and during the timed steps (the table refreshes more slowly "
-                       "than that: 'distinct' counts the different readings)")
+    t0.record(main_stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(main_stream)
+    torch.cuda.synchronize()
+    clock["after_timed_steps"] = sensors.sample()
+    clock["source"] = ("amdsmi metrics table (current_gfxclks averaged over the XCDs, "
+                       "current_socket_power, temperature_hotspot), read with the GPU idle before "
+                       "the warm-up and right after the timed steps; the table refreshes about "
+                       "once a second, so the second reading reflects the warm-up and timed steps "
+                       "when they last a second or more (the default run) and may predate them in "
+                       "a shorter run")
     ms_per_step = t0.elapsed_time(t1) / args.steps
 
     # ---- the same K steps again with every kernel bracketed by events on
