@@ -135,8 +135,10 @@ struct Stager {
     }
 };
 
-// Scheduling hint for one k-block: the operand reads of k-step ks + 1 and
-// the LDS stores of the next block run between the MFMAs of k-step ks.
+// Scheduling hint for one k-block: the operand reads of k-step ks + 1 and,
+// when the LDS stores of the next block follow the MFMAs, those stores run
+// between the MFMAs of k-step ks.
+template <bool kStores>
 __device__ inline void interleave_k_block() {
     constexpr int kReads = kNT + kMT;            // operand reads per k-step
     constexpr int kMfma = kNT * kMT;             // MFMAs per k-step
@@ -149,7 +151,8 @@ __device__ inline void interleave_k_block() {
         for (int h = 0; h < 2; ++h) {
             __builtin_amdgcn_sched_group_barrier(0x008, kMfma / 2, 0);           // MFMA
             if (ks + 1 < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, kReads / 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x200, kWrites / (2 * kSteps), 0);  // DS write
+            if constexpr (kStores)
+                __builtin_amdgcn_sched_group_barrier(0x200, kWrites / (2 * kSteps), 0);  // DS write
         }
     }
 }
@@ -340,8 +343,17 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
     st[0].store(xt[0], wt[0], tid);
     if (NSETS == 2) load_next(st[1 % NSETS]);
     __syncthreads();
+    // With two register sets the next block's LDS stores go first, right
+    // after the barrier that ended every wave's reads of that buffer (its
+    // loads were issued a step earlier), then the MFMAs; the plain epilogue's
+    // k-loop keeps hints for the operand reads, the QKV one (one long tile per
+    // workgroup) leaves the order to the compiler, each measured fastest
+    // (about 2 % over the stores between the MFMAs).  With one set the block
+    // is loaded during this step and stored after the MFMAs.
+    constexpr bool kStoreFirst = NSETS == 2;
     auto step = [&](int s, Stager<T> &ld, const Stager<T> &sto) {
         load_next(ld);
+        if constexpr (kStoreFirst) sto.store(xt[(s + 1) & 1], wt[(s + 1) & 1], tid);
         const __bf16 *xa = xt[s & 1] + (wm * kMT * 32 + li) * kRow + g * 8;
         const __bf16 *wa = wt[s & 1] + (wn * kNT * 32 + li) * kRow + g * 8;
 #pragma unroll
@@ -360,8 +372,12 @@ __global__ __launch_bounds__(kThreads, 1) void linear_kernel(const T *__restrict
                     acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nt], bx[mt], acc[nt][mt],
                                                                           0, 0, 0);
         }
-        sto.store(xt[(s + 1) & 1], wt[(s + 1) & 1], tid);
-        interleave_k_block();
+        if constexpr (!kStoreFirst) {
+            sto.store(xt[(s + 1) & 1], wt[(s + 1) & 1], tid);
+            interleave_k_block<true>();
+        } else if constexpr (!QKV) {
+            interleave_k_block<false>();
+        }
         __syncthreads();
     };
     // The k-blocks of one tile run in a loop of two steps without branches
