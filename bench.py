@@ -720,7 +720,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the hot path "
-              "is one GPU's share of HCMS and this build has no multi-GPU exchange.",
+              "is one GPU's share of HCMS and this library has no multi-GPU exchange.",
               file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():

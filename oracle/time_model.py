@@ -15,7 +15,7 @@ one function per equation of the paper, written from its definitions:
   measured points, by numpy's lstsq (the library routine is the step; the
   model is the paper's).
 
-The one-GPU extension (this build's reading; the paper holds the attention
+The one-GPU extension (this library's reading; the paper holds the attention
 time fixed):
 
 * :func:`launch_rounds`  duration, in full rounds, of a launch of W

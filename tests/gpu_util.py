@@ -8,7 +8,7 @@ import torch
 
 from paper_2607_01817_amd import inputs
 
-# Spec tolerance for attention against the fp64 oracle (bf16 operands,
+# The attention tolerance against the fp64 oracle (bf16 operands,
 # fp32 accumulation).
 MAX_ABS = 2e-2
 

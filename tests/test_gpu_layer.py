@@ -10,7 +10,7 @@ Tolerances (bf16 operands, fp32 accumulation, outputs rounded to bf16):
   * rotation table: within 2e-7 of float64 cos / sin (the fp32 rounding);
   * QKV projection: as the GEMM (the rotation is done in fp32 on the fp32
     accumulator before the one rounding);
-  * layer: max-abs error within 2e-2 max|ref|, the benchmark spec's tolerance
+  * layer: max-abs error within 2e-2 max|ref|, the attention tolerance
     normalised by the output's scale.
 Across chunkings and scheduling modes the layer output is bit-identical.
 """
