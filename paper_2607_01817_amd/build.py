@@ -102,6 +102,9 @@ def build(verbose: bool = False) -> str:
         done = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
     objs = [o for o, _ in done]
     res = {k: v for _, r in done for k, v in r.items()}
+    if not res:
+        raise RuntimeError("no kernel-resource-usage remarks found: the resource guard cannot check "
+                           "the kernels (compiler remark format changed?)")
     bad = resource_problems(res)
     if bad:
         raise RuntimeError("kernel resource limits exceeded:\n" + "\n".join(bad))
